@@ -1,0 +1,171 @@
+/*
+ * mustafar.h -- C ABI of the MI355X (gfx950) implementation of MUSTAFAR's
+ * decode hot path (arxiv 2505.22913):
+ *
+ *   1. per-token magnitude pruning of the Key and Value caches to an arbitrary
+ *      unstructured sparsity (Sec. 2: the per-token magnitude method is the
+ *      one the paper keeps for both caches; Appendix A.4 for 80-90%),
+ *   2. compression of the pruned caches into the bitmap-based sparse format
+ *      (Sec. 3: 1x64 tiles, a 64-bit bitmap per tile, per-tile offsets,
+ *      packed non-zeros; Sec. 4.3: non-zeros padded to a multiple of 8),
+ *   3. decode attention computed directly on the compressed caches plus a
+ *      dense local window of recent tokens (Algorithm 1, Sec. 3).
+ *
+ * CONVENTIONS (all entry points)
+ *   - fp16 tensors are passed as pointers to IEEE binary16 bit patterns.
+ *   - Every tensor pointer is a DEVICE pointer owned by the caller. The library
+ *     allocates no device or host memory, keeps no state between calls and
+ *     never synchronises: work is enqueued on `stream` (a hipStream_t; NULL is
+ *     the default stream) and the call returns at once.
+ *   - Arguments are validated on the host before anything is launched; an
+ *     invalid call returns a negative status and enqueues nothing.
+ *   - Status codes: MUSTAFAR_OK (0) or one of the negative codes below;
+ *     mustafar_strerror() gives a message. No exception crosses the ABI.
+ *   - Calls that overlap on one stream are ordered by the stream; the caller
+ *     must not run two calls that write the same cache on different streams
+ *     concurrently.
+ *
+ * THE COMPRESSED CACHE (one per K or V cache of a layer)
+ *   B batch entries x H kv-heads = B*H independent streams. A stream holds the
+ *   compressed tokens of one (batch, kv-head) in arrival order. With T = d/64
+ *   tiles per token, token j of stream s owns tiles s*cap_tokens*T + j*T + t:
+ *     bitmaps[tile]  u64  bit i set  <=> channel 64t+i of the token is kept
+ *     offsets[tile]  u32  index (fp16 elements, relative to the stream's first
+ *                         value) of the tile's first packed non-zero; always a
+ *                         multiple of 8
+ *     values[s*val_stride + offsets[tile] + r]  r < popcount(bitmap): the
+ *                         kept fp16 values of the tile in channel order;
+ *                         then zero (+0.0) fill up to the next multiple of 8
+ *     stream_len[s]  u32  fp16 elements used by stream s (device-side)
+ *   Pruning keeps exactly n_keep = mustafar_keep_count(d, sparsity) channels
+ *   per token: the n_keep of largest magnitude, ties broken towards the lower
+ *   channel index (magnitudes compare as |x|; +0 and -0 are equal). Inputs
+ *   must be finite.
+ */
+#ifndef MUSTAFAR_H
+#define MUSTAFAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MUSTAFAR_TILE 64 /* channels per tile, one bit per wavefront lane */
+#define MUSTAFAR_PAD 8   /* packed non-zeros per tile rounded up to this  */
+
+enum mustafar_status {
+    MUSTAFAR_OK = 0,
+    MUSTAFAR_EINVAL = -1,      /* bad size, pointer, alignment or sparsity      */
+    MUSTAFAR_ECAPACITY = -2,   /* cache has no room for the tokens              */
+    MUSTAFAR_EWORKSPACE = -3,  /* workspace missing or smaller than required    */
+    MUSTAFAR_ELAUNCH = -4,     /* the HIP runtime rejected a launch             */
+    MUSTAFAR_EUNSUPPORTED = -5 /* valid but unsupported shape (d, group size)   */
+};
+
+/* Descriptor of one compressed cache. Pointers are device memory owned by the
+ * caller; the integer fields are host-side and are filled by
+ * mustafar_ccache_init() and advanced by the compress/append calls. */
+typedef struct mustafar_ccache {
+    uint64_t* bitmaps;    /* [B*H][cap_tokens][d/64], 8-byte aligned            */
+    uint32_t* offsets;    /* [B*H][cap_tokens][d/64], 4-byte aligned            */
+    uint16_t* values;     /* [B*H][val_stride] fp16 bits, 16-byte aligned       */
+    uint32_t* stream_len; /* [B*H], 4-byte aligned                              */
+    int32_t B, H, d;      /* batch, kv-heads, head dimension (64, 128 or 256)   */
+    int32_t n_keep;       /* channels kept per token                            */
+    int32_t cap_tokens;   /* tokens each stream can hold                        */
+    int32_t n_tokens;     /* tokens compressed so far (same for every stream)   */
+    int64_t val_stride;   /* fp16 elements reserved per stream, multiple of 8   */
+} mustafar_ccache_t;
+
+/* Channels kept per token for a target sparsity s in [0, 1] (Sec. 2 prunes
+ * each token to the target sparsity; the rounding of s*d to a whole number of
+ * channels is not given by the paper and is fixed here as
+ *   n_keep = d - floor(s*d + 1/2)  (round half up, computed in double).
+ * Returns n_keep in [0, d], or MUSTAFAR_EINVAL if d <= 0 or s is outside
+ * [0, 1] or NaN. Host only. */
+int mustafar_keep_count(int d, float sparsity);
+
+/* Largest number of fp16 elements one token can occupy in a stream:
+ * min(d, floor8(n_keep + 7*d/64)) rounded up to a multiple of 8 -- each tile
+ * adds at most 7 pad slots. -1 on invalid arguments. Host only. */
+int64_t mustafar_token_max_elems(int d, int n_keep);
+
+/* fp16 elements a stream needs to hold cap_tokens tokens in the worst case
+ * (cap_tokens * mustafar_token_max_elems). -1 on invalid arguments. */
+int64_t mustafar_stream_capacity(int d, int n_keep, int cap_tokens);
+
+/* Fills *c for caller-allocated buffers and sets n_tokens = 0. Checks shapes,
+ * alignment and that val_stride >= mustafar_stream_capacity(d, n_keep,
+ * cap_tokens). Host only: touches neither the GPU nor the buffers (the caller
+ * need not clear any buffer). */
+int mustafar_ccache_init(mustafar_ccache_t* c, void* bitmaps, void* offsets, void* values,
+                         void* stream_len, int B, int H, int d, float sparsity,
+                         int cap_tokens, int64_t val_stride);
+
+/* Device workspace needed by mustafar_prune_compress for n_new tokens. */
+size_t mustafar_compress_workspace_bytes(int B, int H, int n_new);
+
+/* Prune and compress n_new tokens per stream and append them after the
+ * c->n_tokens tokens already in c (into an empty cache this is the
+ * compression of the prefill cache before decoding starts, Sec. 3).
+ *   x   [B][H][n_new][d] fp16, 16-byte aligned: the dense new tokens
+ *   ws  device workspace of at least mustafar_compress_workspace_bytes()
+ * On success c->n_tokens += n_new. Errors: EINVAL (bad descriptor, n_new < 1,
+ * misaligned x), ECAPACITY (n_tokens + n_new > cap_tokens), EWORKSPACE. */
+int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void* ws,
+                            size_t ws_bytes, void* stream);
+
+/* Prune, compress and append ONE token per stream (the token that leaves the
+ * dense local window at a decode step, Sec. 3 and Appendix C.2). Needs no
+ * workspace. x_new [B][H][d] fp16, 16-byte aligned. On success
+ * c->n_tokens += 1. The result is bit-identical to compressing all tokens in
+ * one mustafar_prune_compress call. */
+int mustafar_append(mustafar_ccache_t* c, const void* x_new, void* stream);
+
+/* Split-K segment count chosen when a decode call passes n_splits <= 0. */
+int mustafar_attn_default_splits(int B, int Hkv, int n_tokens);
+
+/* Device workspace for the decode-attention calls: fp32 partial results
+ * (running max, running sum, d accumulators) for n_splits token ranges plus
+ * one dense-window segment, for each of the B*Hq query heads. n_splits <= 0
+ * selects mustafar_attn_default_splits(B, Hkv, n_tokens). */
+size_t mustafar_attn_workspace_bytes(int B, int Hq, int Hkv, int d, int n_tokens, int n_splits);
+
+/* Decode attention over compressed caches plus a dense local window
+ * (Algorithm 1). For query head h (kv-head h / (Hq/Hkv), grouped-query
+ * attention with contiguous groups):
+ *   scores = scale * q.k over the Kc->n_tokens compressed tokens (zero-filled
+ *            pruned keys), then over the n_tail window tokens;
+ *   p      = softmax over all of them;
+ *   out    = sum_j p_j v_j (pruned values are zeros).
+ *   q       [B][Hq][d] fp16, 16-byte aligned
+ *   Kc, Vc  compressed caches with B, H = Hkv, d and n_tokens equal
+ *   k_tail, v_tail  [B][Hkv][n_tail][d] fp16, 16-byte aligned; may be NULL
+ *           when n_tail == 0
+ *   scale   score scale; <= 0 selects 1/sqrt(d)
+ *   out     [B][Hq][d] fp16 (round to nearest even), 16-byte aligned
+ *   n_splits  token ranges per stream processed in parallel (<= 0: default)
+ * Errors: EINVAL (shape mismatch, Hq % Hkv != 0, no tokens at all, bad
+ * pointers), EUNSUPPORTED (Hq/Hkv not 1, 2, 4 or 8), EWORKSPACE. */
+int mustafar_sparse_decode_attn(const void* q, int B, int Hq, const mustafar_ccache_t* Kc,
+                                const mustafar_ccache_t* Vc, const void* k_tail,
+                                const void* v_tail, int n_tail, float scale, void* out,
+                                int n_splits, void* ws, size_t ws_bytes, void* stream);
+
+/* The same attention over dense fp16 caches k, v [B][Hkv][n_tokens][d]: the
+ * in-house dense baseline the sparse path is measured against (the paper
+ * compares against a dense batched matrix-vector product, Sec. 4.3). */
+int mustafar_dense_decode_attn(const void* q, int B, int Hq, int Hkv, const void* k,
+                               const void* v, int n_tokens, int d, float scale, void* out,
+                               int n_splits, void* ws, size_t ws_bytes, void* stream);
+
+/* Static message for a status code. */
+const char* mustafar_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MUSTAFAR_H */

@@ -1,0 +1,89 @@
+"""The pins must reject a broken oracle.
+
+Each case plants one plausible mistake in a copy of ``oracle/mustafar_oracle.c``
+(compiled into a temporary library on the CPU) and runs the pins of
+``test_oracle_pins`` against that build; at least one pin must fail. The
+unmodified source must pass the same battery.
+"""
+import os
+import subprocess
+
+import pytest
+
+import oracle
+from tests import test_oracle_pins as pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "mustafar_oracle.c")
+
+# (name, original text, planted text)
+MUTATIONS = [
+    ("tie-break towards the higher channel",
+     "return (a->idx > b->idx) - (a->idx < b->idx);",
+     "return (a->idx < b->idx) - (a->idx > b->idx);"),
+    ("smallest magnitudes kept",
+     "    if (a->mag > b->mag)\n        return -1;\n    if (a->mag < b->mag)\n        return 1;",
+     "    if (a->mag > b->mag)\n        return 1;\n    if (a->mag < b->mag)\n        return -1;"),
+    ("ranked by signed value instead of magnitude",
+     "r[c].mag = fabs(oracle_half_to_double(x[c]));",
+     "r[c].mag = oracle_half_to_double(x[c]);"),
+    ("padding to a multiple of 4", "#define ORACLE_PAD 8 ", "#define ORACLE_PAD 4 "),
+    ("no padding",
+     "int padded = (count + ORACLE_PAD - 1) / ORACLE_PAD * ORACLE_PAD;",
+     "int padded = count;"),
+    ("bitmap bit order reversed", "bm |= (uint64_t)1 << i;", "bm |= (uint64_t)1 << (63 - i);"),
+    ("non-zero pad value", "values[pos + w] = 0x0000;", "values[pos + w] = 0x3c00;"),
+    ("kept count truncates instead of rounding",
+     "floor((double)sparsity * (double)d + 0.5)", "floor((double)sparsity * (double)d)"),
+    ("subnormal exponent off by one", "v = ldexp((double)f, -24);", "v = ldexp((double)f, -25);"),
+    ("score scale dropped", "s[j] = scale * acc;", "s[j] = acc;"),
+    ("keys used as values",
+     "const uint16_t* vj = (j < n_s) ? vc + (int64_t)j * d : vl + (int64_t)(j - n_s) * d;",
+     "const uint16_t* vj = (j < n_s) ? kc + (int64_t)j * d : kl + (int64_t)(j - n_s) * d;"),
+    ("softmax not normalised", "o += (s[j] / l) *", "o += s[j] *"),
+    ("dense window left out of the softmax", "int n = n_s + n_d;", "int n = n_s;"),
+]
+
+
+def _battery():
+    """Run the pins (fixed parameters) and return the name of the first failure."""
+    checks = [
+        ("half decoding", pins.test_half_decoding_matches_numpy_for_every_pattern),
+        ("keep count", lambda: pins.test_keep_count_values(128, 0.7, 38)),
+        ("keep count half up", lambda: pins.test_keep_count_values(128, 0.50390625, 63)),
+        ("stable argsort", lambda: pins.test_prune_equals_stable_argsort(64)),
+        ("brute force", lambda: pins.test_prune_equals_brute_force_enumeration(6)),
+        ("hand example", pins.test_hand_worked_example),
+        ("round trip", lambda: pins.test_round_trip_and_layout_invariants(0.5)),
+        ("sdpa", lambda: pins.test_attention_equals_torch_sdpa_on_zero_filled_caches(4, 32, 0.7)),
+        ("zero query", pins.test_zero_query_gives_the_mean_value_row),
+    ]
+    for name, fn in checks:
+        try:
+            fn()
+        except Exception:  # noqa: BLE001 - any failure of a pin counts
+            return name
+    return None
+
+
+def _build(tmp_path, text, tag):
+    c = tmp_path / f"oracle_{tag}.c"
+    so = tmp_path / f"liboracle_{tag}.so"
+    c.write_text(text)
+    subprocess.run(["gcc", "-O1", "-std=c11", "-shared", "-fPIC", "-o", str(so), str(c), "-lm"],
+                   check=True)
+    return str(so)
+
+
+def test_unmodified_oracle_passes_the_battery(tmp_path):
+    so = _build(tmp_path, open(SRC).read(), "clean")
+    with oracle.using_library(so):
+        assert _battery() is None
+
+
+@pytest.mark.parametrize("name,orig,planted", MUTATIONS, ids=[m[0] for m in MUTATIONS])
+def test_planted_mistake_is_caught(tmp_path, name, orig, planted):
+    text = open(SRC).read()
+    assert text.count(orig) == 1, f"mutation anchor not unique: {orig!r}"
+    so = _build(tmp_path, text.replace(orig, planted), "mut")
+    with oracle.using_library(so):
+        assert _battery() is not None, f"no pin caught: {name}"
