@@ -88,8 +88,9 @@ typedef struct mustafar_ccache {
 int mustafar_keep_count(int d, float sparsity);
 
 /* Largest number of fp16 elements one token can occupy in a stream:
- * min(d, floor8(n_keep + 7*d/64)) rounded up to a multiple of 8 -- each tile
- * adds at most 7 pad slots. -1 on invalid arguments. Host only. */
+ * min(d, floor8(n_keep + 7*min(n_keep, d/64))), floor8 rounding down to a
+ * multiple of 8 -- each tile holding a kept value adds at most 7 pad slots and
+ * the total is a multiple of 8. -1 on invalid arguments. Host only. */
 int64_t mustafar_token_max_elems(int d, int n_keep);
 
 /* fp16 elements a stream needs to hold cap_tokens tokens in the worst case

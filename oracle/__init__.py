@@ -132,7 +132,7 @@ def prune_token(x, k: int) -> np.ndarray:
 def token_max_elems(d: int, k: int) -> int:
     """Worst-case fp16 elements of one compressed token (every tile padded)."""
     T = d // TILE
-    return min(d, (k + (PAD - 1) * T) // PAD * PAD)
+    return min(d, (k + (PAD - 1) * min(k, T)) // PAD * PAD)
 
 
 def compress(x, sparsity: float | None = None, *, k: int | None = None, threads: int = 1) -> dict:

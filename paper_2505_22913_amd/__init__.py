@@ -1,1 +1,239 @@
-"""MI355X-native MUSTAFAR decode hot path (placeholder; binding added with the kernels)."""
+"""MI355X (gfx950) implementation of MUSTAFAR's decode hot path (arxiv 2505.22913).
+
+Thin ctypes binding of ``libmustafar.so``; every step of the path runs in the
+library's HIP kernels. Function names mirror the C ABI in ``include/mustafar.h``;
+this module only turns torch tensors into device pointers, passes the current
+HIP stream and raises ``MustafarError`` on a non-zero status. torch is used for
+device memory and streams only.
+
+The library is loaded on first use; if it has not been built the call raises
+(there is no CPU fallback). Build it with
+``python -m paper_2505_22913_amd.build_lib`` or ``__graft_entry__.build()``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmustafar.so")
+TILE = 64
+PAD = 8
+
+OK, EINVAL, ECAPACITY, EWORKSPACE, ELAUNCH, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+
+_lib = None
+
+
+class MustafarError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: {status} ({strerror(status)})")
+        self.status = status
+
+
+class ccache_t(ctypes.Structure):
+    """Mirror of ``mustafar_ccache_t``."""
+    _fields_ = [("bitmaps", ctypes.c_void_p), ("offsets", ctypes.c_void_p),
+                ("values", ctypes.c_void_p), ("stream_len", ctypes.c_void_p),
+                ("B", ctypes.c_int32), ("H", ctypes.c_int32), ("d", ctypes.c_int32),
+                ("n_keep", ctypes.c_int32), ("cap_tokens", ctypes.c_int32),
+                ("n_tokens", ctypes.c_int32), ("val_stride", ctypes.c_int64)]
+
+
+_SIGS = {
+    "mustafar_keep_count": (ctypes.c_int, [ctypes.c_int, ctypes.c_float]),
+    "mustafar_token_max_elems": (ctypes.c_int64, [ctypes.c_int, ctypes.c_int]),
+    "mustafar_stream_capacity": (ctypes.c_int64, [ctypes.c_int, ctypes.c_int, ctypes.c_int]),
+    "mustafar_ccache_init": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                            ctypes.c_float, ctypes.c_int, ctypes.c_int64]),
+    "mustafar_compress_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int] * 3),
+    "mustafar_prune_compress": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                               ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t,
+                                               ctypes.c_void_p]),
+    "mustafar_append": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                       ctypes.c_void_p]),
+    "mustafar_attn_default_splits": (ctypes.c_int, [ctypes.c_int] * 3),
+    "mustafar_attn_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int] * 6),
+    "mustafar_sparse_decode_attn": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                                   ctypes.POINTER(ccache_t),
+                                                   ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                                   ctypes.c_void_p, ctypes.c_int, ctypes.c_float,
+                                                   ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                                   ctypes.c_size_t, ctypes.c_void_p]),
+    "mustafar_dense_decode_attn": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                                  ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                                  ctypes.c_int, ctypes.c_int, ctypes.c_float,
+                                                  ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                                  ctypes.c_size_t, ctypes.c_void_p]),
+    "mustafar_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if libmustafar.so has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2505_22913_amd.build_lib` (no CPU fallback)")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(handle, name)
+            fn.restype, fn.argtypes = res, args
+        _lib = handle
+    return _lib
+
+
+def strerror(status: int) -> str:
+    try:
+        return lib().mustafar_strerror(int(status)).decode()
+    except Exception:  # noqa: BLE001 - the message is best effort
+        return "unknown"
+
+
+def _check(fn: str, status: int) -> None:
+    if status != OK:
+        raise MustafarError(fn, status)
+
+
+def _dptr(t) -> int | None:
+    """Device pointer of a CUDA (HIP) tensor; None for None."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("libmustafar takes device tensors only")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+# ---- host-only helpers --------------------------------------------------------------------
+def mustafar_keep_count(d: int, sparsity: float) -> int:
+    k = lib().mustafar_keep_count(int(d), float(sparsity))
+    _check("mustafar_keep_count", min(k, 0))
+    return k
+
+
+def mustafar_token_max_elems(d: int, n_keep: int) -> int:
+    return lib().mustafar_token_max_elems(int(d), int(n_keep))
+
+
+def mustafar_stream_capacity(d: int, n_keep: int, cap_tokens: int) -> int:
+    return lib().mustafar_stream_capacity(int(d), int(n_keep), int(cap_tokens))
+
+
+def mustafar_compress_workspace_bytes(B: int, H: int, n_new: int) -> int:
+    return lib().mustafar_compress_workspace_bytes(int(B), int(H), int(n_new))
+
+
+def mustafar_attn_default_splits(B: int, Hkv: int, n_tokens: int) -> int:
+    return lib().mustafar_attn_default_splits(int(B), int(Hkv), int(n_tokens))
+
+
+def mustafar_attn_workspace_bytes(B: int, Hq: int, Hkv: int, d: int, n_tokens: int,
+                                  n_splits: int = 0) -> int:
+    return lib().mustafar_attn_workspace_bytes(int(B), int(Hq), int(Hkv), int(d), int(n_tokens),
+                                               int(n_splits))
+
+
+# ---- the compressed cache -----------------------------------------------------------------
+class CompressedCache:
+    """A compressed K or V cache: device buffers (torch) plus the C descriptor.
+
+    bitmaps u64 [B][H][cap][d/64], offsets u32 [B][H][cap][d/64],
+    values fp16 bits [B][H][val_stride], stream_len u32 [B][H].
+    """
+
+    def __init__(self, B: int, H: int, d: int, sparsity: float, cap_tokens: int, device="cuda"):
+        import torch
+        k = mustafar_keep_count(d, sparsity)
+        T = d // TILE
+        stride = mustafar_stream_capacity(d, k, cap_tokens)
+        stride = max(PAD, (stride + PAD - 1) // PAD * PAD)
+        self.bitmaps = torch.zeros((B, H, cap_tokens, T), dtype=torch.int64, device=device)
+        self.offsets = torch.zeros((B, H, cap_tokens, T), dtype=torch.int32, device=device)
+        self.values = torch.zeros((B, H, stride), dtype=torch.int16, device=device)
+        self.stream_len = torch.zeros((B, H), dtype=torch.int32, device=device)
+        self.desc = ccache_t()
+        _check("mustafar_ccache_init", lib().mustafar_ccache_init(
+            ctypes.byref(self.desc), self.bitmaps.data_ptr(), self.offsets.data_ptr(),
+            self.values.data_ptr(), self.stream_len.data_ptr(), B, H, d, float(sparsity),
+            cap_tokens, stride))
+
+    @property
+    def n_tokens(self) -> int:
+        return self.desc.n_tokens
+
+    @property
+    def n_keep(self) -> int:
+        return self.desc.n_keep
+
+    @property
+    def shape(self):
+        return self.desc.B, self.desc.H, self.desc.d
+
+
+def mustafar_prune_compress(cache: CompressedCache, x, ws=None, stream=None) -> None:
+    """Append x [B][H][n_new][d] (fp16, device) to the cache, pruned and compressed."""
+    import torch
+    n_new = int(x.shape[2])
+    need = mustafar_compress_workspace_bytes(cache.desc.B, cache.desc.H, n_new)
+    if ws is None:
+        ws = torch.empty(max(need, 4), dtype=torch.uint8, device=x.device)
+    _check("mustafar_prune_compress", lib().mustafar_prune_compress(
+        ctypes.byref(cache.desc), _dptr(x), n_new, _dptr(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+def mustafar_append(cache: CompressedCache, x_new, stream=None) -> None:
+    """Append one token per stream, x_new [B][H][d] (fp16, device)."""
+    _check("mustafar_append", lib().mustafar_append(ctypes.byref(cache.desc), _dptr(x_new),
+                                                    _stream(stream)))
+
+
+def _attn_ws(B, Hq, Hkv, d, n, n_splits, ws, device):
+    import torch
+    need = mustafar_attn_workspace_bytes(B, Hq, Hkv, d, n, n_splits)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=device)
+    return ws
+
+
+def mustafar_sparse_decode_attn(q, Kc: CompressedCache, Vc: CompressedCache, k_tail=None,
+                                v_tail=None, scale: float = 0.0, out=None, n_splits: int = 0,
+                                ws=None, stream=None):
+    """Algorithm 1: attention of q [B][Hq][d] over the compressed caches plus the dense
+    window [B][Hkv][n_tail][d]. Returns out [B][Hq][d] fp16."""
+    import torch
+    B, Hq, d = (int(s) for s in q.shape)
+    Hkv = Kc.desc.H
+    n_tail = 0 if k_tail is None else int(k_tail.shape[2])
+    if out is None:
+        out = torch.empty((B, Hq, d), dtype=torch.float16, device=q.device)
+    ws = _attn_ws(B, Hq, Hkv, d, Kc.n_tokens, n_splits, ws, q.device)
+    _check("mustafar_sparse_decode_attn", lib().mustafar_sparse_decode_attn(
+        _dptr(q), B, Hq, ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), _dptr(k_tail),
+        _dptr(v_tail), n_tail, float(scale), _dptr(out), int(n_splits), _dptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
+    return out
+
+
+def mustafar_dense_decode_attn(q, k, v, scale: float = 0.0, out=None, n_splits: int = 0, ws=None,
+                               stream=None):
+    """Dense baseline: q [B][Hq][d] over k, v [B][Hkv][N][d] fp16. Returns out fp16."""
+    import torch
+    B, Hq, d = (int(s) for s in q.shape)
+    Hkv, N = int(k.shape[1]), int(k.shape[2])
+    if out is None:
+        out = torch.empty((B, Hq, d), dtype=torch.float16, device=q.device)
+    ws = _attn_ws(B, Hq, Hkv, d, N, n_splits, ws, q.device)
+    _check("mustafar_dense_decode_attn", lib().mustafar_dense_decode_attn(
+        _dptr(q), B, Hq, Hkv, _dptr(k), _dptr(v), N, d, float(scale), _dptr(out), int(n_splits),
+        _dptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+    return out

@@ -1,0 +1,270 @@
+// C ABI of libmustafar (declared in include/mustafar.h): host-side validation,
+// launch geometry and workspace layout. Every check runs before any launch, so
+// an invalid call enqueues nothing and never touches the GPU.
+#include <math.h>
+#include <stdint.h>
+
+#include "mf_launch.h"
+#include "mustafar.h"
+
+namespace {
+
+constexpr int kTile = MUSTAFAR_TILE;
+constexpr int kPad = MUSTAFAR_PAD;
+constexpr int kMaxGrid = 65535;            // grid.y limit for the stream index
+constexpr int kTargetWaves = 4096;         // decode: segments to fill 256 CUs several times
+constexpr int kMinSegTokens = 128;         // decode: smallest useful segment
+constexpr int kSegAlign = 64;              // segments are whole 64-token blocks
+
+bool aligned(const void* p, uintptr_t a) { return p && ((uintptr_t)p % a) == 0; }
+bool head_dim_ok(int d) { return d == 64 || d == 128 || d == 256; }
+
+int status_of(hipError_t e) { return e == hipSuccess ? MUSTAFAR_OK : MUSTAFAR_ELAUNCH; }
+
+int check_cache(const mustafar_ccache_t* c) {
+  if (!c) return MUSTAFAR_EINVAL;
+  if (!aligned(c->bitmaps, 8) || !aligned(c->offsets, 4) || !aligned(c->values, 16) ||
+      !aligned(c->stream_len, 4))
+    return MUSTAFAR_EINVAL;
+  if (c->B < 1 || c->H < 1 || (int64_t)c->B * c->H > kMaxGrid) return MUSTAFAR_EINVAL;
+  if (!head_dim_ok(c->d)) return MUSTAFAR_EINVAL;
+  if (c->n_keep < 0 || c->n_keep > c->d) return MUSTAFAR_EINVAL;
+  if (c->cap_tokens < 1 || c->n_tokens < 0 || c->n_tokens > c->cap_tokens) return MUSTAFAR_EINVAL;
+  if (c->val_stride % kPad != 0 ||
+      c->val_stride < mustafar_stream_capacity(c->d, c->n_keep, c->cap_tokens))
+    return MUSTAFAR_EINVAL;
+  return MUSTAFAR_OK;
+}
+
+mf::CacheView view_of(const mustafar_ccache_t* c) {
+  mf::CacheView v;
+  v.bitmaps = c->bitmaps;
+  v.offsets = c->offsets;
+  v.values = c->values;
+  v.stream_len = c->stream_len;
+  v.BH = c->B * c->H;
+  v.T = c->d / kTile;
+  v.n_keep = c->n_keep;
+  v.cap_tokens = c->cap_tokens;
+  v.val_stride = c->val_stride;
+  return v;
+}
+
+mf::SparseSide side_of(const mustafar_ccache_t* c) {
+  mf::SparseSide s;
+  s.bitmaps = c->bitmaps;
+  s.offsets = c->offsets;
+  s.values = c->values;
+  s.val_stride = c->val_stride;
+  s.cap_tokens = c->cap_tokens;
+  s.n_keep = c->n_keep;
+  return s;
+}
+
+int round_up(int x, int a) { return (x + a - 1) / a * a; }
+
+// Segment size (tokens, multiple of 64) for n tokens split n_splits ways.
+int seg_tokens(int n, int n_splits) {
+  if (n <= 0) return kSegAlign;
+  return round_up((n + n_splits - 1) / n_splits, kSegAlign);
+}
+
+int n_segments(int n, int seg) { return n <= 0 ? 0 : (n + seg - 1) / seg; }
+
+float scale_log2_of(float scale, int d) {
+  const double s = scale > 0.f ? (double)scale : 1.0 / sqrt((double)d);
+  return (float)(s * 1.4426950408889634);  // log2(e): scores live in the exp2 domain
+}
+
+}  // namespace
+
+extern "C" {
+
+int mustafar_keep_count(int d, float sparsity) {
+  if (d <= 0 || !(sparsity >= 0.f && sparsity <= 1.f)) return MUSTAFAR_EINVAL;
+  const int pruned = (int)floor((double)sparsity * (double)d + 0.5);
+  int k = d - pruned;
+  if (k < 0) k = 0;
+  if (k > d) k = d;
+  return k;
+}
+
+int64_t mustafar_token_max_elems(int d, int n_keep) {
+  if (!head_dim_ok(d) || n_keep < 0 || n_keep > d) return -1;
+  const int T = d / kTile;
+  const int nonempty = n_keep < T ? n_keep : T;  // only tiles with a kept value are padded
+  const int64_t m = (int64_t)(n_keep + (kPad - 1) * nonempty) / kPad * kPad;
+  return m < d ? m : d;
+}
+
+int64_t mustafar_stream_capacity(int d, int n_keep, int cap_tokens) {
+  const int64_t per = mustafar_token_max_elems(d, n_keep);
+  if (per < 0 || cap_tokens < 0) return -1;
+  return per * cap_tokens;
+}
+
+int mustafar_ccache_init(mustafar_ccache_t* c, void* bitmaps, void* offsets, void* values,
+                         void* stream_len, int B, int H, int d, float sparsity, int cap_tokens,
+                         int64_t val_stride) {
+  if (!c) return MUSTAFAR_EINVAL;
+  const int k = mustafar_keep_count(d, sparsity);
+  if (k < 0) return MUSTAFAR_EINVAL;
+  mustafar_ccache_t t;
+  t.bitmaps = (uint64_t*)bitmaps;
+  t.offsets = (uint32_t*)offsets;
+  t.values = (uint16_t*)values;
+  t.stream_len = (uint32_t*)stream_len;
+  t.B = B;
+  t.H = H;
+  t.d = d;
+  t.n_keep = k;
+  t.cap_tokens = cap_tokens;
+  t.n_tokens = 0;
+  t.val_stride = val_stride;
+  const int st = check_cache(&t);
+  if (st != MUSTAFAR_OK) return st;
+  *c = t;
+  return MUSTAFAR_OK;
+}
+
+size_t mustafar_compress_workspace_bytes(int B, int H, int n_new) {
+  if (B < 1 || H < 1 || n_new < 1) return 0;
+  const int64_t n_chunks = (n_new + mf::kCompressChunk - 1) / mf::kCompressChunk;
+  return (size_t)((int64_t)B * H * (n_chunks + 1) * sizeof(uint32_t));
+}
+
+int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void* ws,
+                            size_t ws_bytes, void* stream) {
+  int st = check_cache(c);
+  if (st != MUSTAFAR_OK) return st;
+  if (n_new < 1 || !aligned(x, 16)) return MUSTAFAR_EINVAL;
+  if ((int64_t)c->n_tokens + n_new > c->cap_tokens) return MUSTAFAR_ECAPACITY;
+  const size_t need = mustafar_compress_workspace_bytes(c->B, c->H, n_new);
+  if (!aligned(ws, 4) || ws_bytes < need) return MUSTAFAR_EWORKSPACE;
+  const hipError_t e = mf::launch_compress(view_of(c), (const uint16_t*)x, n_new, c->n_tokens,
+                                           (uint32_t*)ws, (hipStream_t)stream);
+  st = status_of(e);
+  if (st == MUSTAFAR_OK) c->n_tokens += n_new;
+  return st;
+}
+
+int mustafar_append(mustafar_ccache_t* c, const void* x_new, void* stream) {
+  int st = check_cache(c);
+  if (st != MUSTAFAR_OK) return st;
+  if (!aligned(x_new, 16)) return MUSTAFAR_EINVAL;
+  if (c->n_tokens + 1 > c->cap_tokens) return MUSTAFAR_ECAPACITY;
+  st = status_of(mf::launch_append(view_of(c), (const uint16_t*)x_new, c->n_tokens,
+                                   (hipStream_t)stream));
+  if (st == MUSTAFAR_OK) c->n_tokens += 1;
+  return st;
+}
+
+int mustafar_attn_default_splits(int B, int Hkv, int n_tokens) {
+  if (B < 1 || Hkv < 1 || n_tokens < 1) return 1;
+  const int64_t streams = (int64_t)B * Hkv;
+  int64_t want = (kTargetWaves + streams - 1) / streams;
+  const int64_t most = (n_tokens + kMinSegTokens - 1) / kMinSegTokens;
+  if (want > most) want = most;
+  if (want < 1) want = 1;
+  return (int)want;
+}
+
+size_t mustafar_attn_workspace_bytes(int B, int Hq, int Hkv, int d, int n_tokens, int n_splits) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || d < 1 || n_tokens < 0) return 0;
+  if (n_splits <= 0) n_splits = mustafar_attn_default_splits(B, Hkv, n_tokens);
+  // Segments actually launched never exceed n_splits over the tokens plus one window segment.
+  const int64_t n_seg = (int64_t)n_splits + 1;
+  return (size_t)(n_seg * B * Hq * (int64_t)(d + 2) * (int64_t)sizeof(float));
+}
+
+static int decode_common(const void* q, int B, int Hq, int Hkv, int d, int n_s, int n_dense,
+                         int dense_is_window, int n_splits, float scale, void* out, void* ws,
+                         size_t ws_bytes, mf::AttnShape* sh, float** ws_ml, float** ws_o) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return MUSTAFAR_EINVAL;
+  if ((int64_t)B * Hkv > kMaxGrid) return MUSTAFAR_EINVAL;
+  if (!head_dim_ok(d)) return MUSTAFAR_EINVAL;
+  if (n_s < 0 || n_dense < 0 || (int64_t)n_s + n_dense < 1) return MUSTAFAR_EINVAL;
+  if (!aligned(q, 16) || !aligned(out, 16)) return MUSTAFAR_EINVAL;
+  const int G = Hq / Hkv;
+  if (G != 1 && G != 2 && G != 4 && G != 8) return MUSTAFAR_EUNSUPPORTED;
+  const int n_main = dense_is_window ? n_s : n_dense;
+  if (n_splits <= 0) n_splits = mustafar_attn_default_splits(B, Hkv, n_main > 0 ? n_main : 1);
+  if (n_splits > (1 << 20)) return MUSTAFAR_EINVAL;
+  const size_t need = mustafar_attn_workspace_bytes(B, Hq, Hkv, d, n_main, n_splits);
+  if (!aligned(ws, 16) || ws_bytes < need) return MUSTAFAR_EWORKSPACE;
+
+  sh->BHkv = B * Hkv;
+  sh->G = G;
+  sh->T = d / kTile;
+  sh->n_s = n_s;
+  sh->n_dense = n_dense;
+  if (dense_is_window) {
+    sh->sparse_seg_tokens = seg_tokens(n_s, n_splits);
+    sh->n_sparse_segs = n_segments(n_s, sh->sparse_seg_tokens);
+    sh->dense_seg_tokens = round_up(n_dense > 0 ? n_dense : 1, kSegAlign);
+    sh->n_dense_segs = n_dense > 0 ? 1 : 0;
+  } else {
+    sh->sparse_seg_tokens = kSegAlign;
+    sh->n_sparse_segs = 0;
+    sh->dense_seg_tokens = seg_tokens(n_dense, n_splits);
+    sh->n_dense_segs = n_segments(n_dense, sh->dense_seg_tokens);
+  }
+  sh->scale_log2 = scale_log2_of(scale, d);
+  const int64_t n_seg = sh->n_sparse_segs + sh->n_dense_segs;
+  const int64_t BHq = (int64_t)B * Hq;
+  *ws_ml = (float*)ws;
+  *ws_o = (float*)ws + n_seg * BHq * 2;
+  return MUSTAFAR_OK;
+}
+
+int mustafar_sparse_decode_attn(const void* q, int B, int Hq, const mustafar_ccache_t* Kc,
+                                const mustafar_ccache_t* Vc, const void* k_tail,
+                                const void* v_tail, int n_tail, float scale, void* out,
+                                int n_splits, void* ws, size_t ws_bytes, void* stream) {
+  int st = check_cache(Kc);
+  if (st != MUSTAFAR_OK) return st;
+  st = check_cache(Vc);
+  if (st != MUSTAFAR_OK) return st;
+  if (Kc->B != B || Vc->B != B || Kc->H != Vc->H || Kc->d != Vc->d ||
+      Kc->n_tokens != Vc->n_tokens)
+    return MUSTAFAR_EINVAL;
+  if (n_tail < 0) return MUSTAFAR_EINVAL;
+  if (n_tail > 0 && (!aligned(k_tail, 16) || !aligned(v_tail, 16))) return MUSTAFAR_EINVAL;
+  mf::AttnShape sh;
+  float *ws_ml, *ws_o;
+  st = decode_common(q, B, Hq, Kc->H, Kc->d, Kc->n_tokens, n_tail, 1, n_splits, scale, out, ws,
+                     ws_bytes, &sh, &ws_ml, &ws_o);
+  if (st != MUSTAFAR_OK) return st;
+  return status_of(mf::launch_attention(sh, (const uint16_t*)q, side_of(Kc), side_of(Vc),
+                                        (const uint16_t*)k_tail, (const uint16_t*)v_tail, ws_ml,
+                                        ws_o, (uint16_t*)out, (hipStream_t)stream));
+}
+
+int mustafar_dense_decode_attn(const void* q, int B, int Hq, int Hkv, const void* k,
+                               const void* v, int n_tokens, int d, float scale, void* out,
+                               int n_splits, void* ws, size_t ws_bytes, void* stream) {
+  if (n_tokens < 1 || !aligned(k, 16) || !aligned(v, 16)) return MUSTAFAR_EINVAL;
+  mf::AttnShape sh;
+  float *ws_ml, *ws_o;
+  int st = decode_common(q, B, Hq, Hkv, d, 0, n_tokens, 0, n_splits, scale, out, ws, ws_bytes, &sh,
+                         &ws_ml, &ws_o);
+  if (st != MUSTAFAR_OK) return st;
+  mf::SparseSide none = {nullptr, nullptr, nullptr, 0, 1, 0};
+  return status_of(mf::launch_attention(sh, (const uint16_t*)q, none, none, (const uint16_t*)k,
+                                        (const uint16_t*)v, ws_ml, ws_o, (uint16_t*)out,
+                                        (hipStream_t)stream));
+}
+
+const char* mustafar_strerror(int status) {
+  switch (status) {
+    case MUSTAFAR_OK: return "success";
+    case MUSTAFAR_EINVAL: return "invalid argument (size, pointer, alignment or sparsity)";
+    case MUSTAFAR_ECAPACITY: return "compressed cache has no room for the new tokens";
+    case MUSTAFAR_EWORKSPACE: return "workspace missing, misaligned or too small";
+    case MUSTAFAR_ELAUNCH: return "the HIP runtime rejected a kernel launch";
+    case MUSTAFAR_EUNSUPPORTED: return "unsupported shape (head dim or query group size)";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

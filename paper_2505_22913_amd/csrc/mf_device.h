@@ -1,0 +1,50 @@
+// Device-side helpers shared by the gfx950 kernels of libmustafar (wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mf {
+
+constexpr int kWave = 64;  // CDNA wavefront width: one lane per tile channel
+constexpr int kTile = 64;  // channels per compressed tile (Sec. 3)
+constexpr int kPad = 8;    // packed non-zeros per tile rounded up to 8 (Sec. 4.3)
+
+__device__ __forceinline__ uint32_t lane_id() {
+  return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+
+// Number of set bits of `mask` at positions below this lane, plus `acc`.
+__device__ __forceinline__ uint32_t mbcnt(uint64_t mask, uint32_t acc) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, acc));
+}
+
+__device__ __forceinline__ uint32_t pad8(uint32_t n) { return (n + (kPad - 1)) & ~uint32_t(kPad - 1); }
+
+__device__ __forceinline__ float half_bits_to_float(uint16_t h) {
+  return (float)__builtin_bit_cast(_Float16, h);
+}
+
+// Butterfly reductions over the 64 lanes of a wave.
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) v = fmaxf(v, __shfl_xor(v, s, kWave));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) v += __shfl_xor(v, s, kWave);
+  return v;
+}
+
+__device__ __forceinline__ int wave_sum_i(int v) {
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) v += __shfl_xor(v, s, kWave);
+  return v;
+}
+
+}  // namespace mf

@@ -1,0 +1,57 @@
+// Internal launch interface between the C-ABI layer (api.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mf {
+
+// Tokens per workgroup of the two-launch compression (4 waves x 64 tokens).
+constexpr int kCompressChunk = 256;
+
+struct CacheView {
+  uint64_t* bitmaps;
+  uint32_t* offsets;
+  uint16_t* values;
+  uint32_t* stream_len;
+  int BH;            // streams = batch * kv-heads
+  int T;             // tiles per token = d / 64
+  int n_keep;        // kept channels per token
+  int cap_tokens;    // token capacity per stream
+  int64_t val_stride;
+};
+
+// Compress n_new tokens per stream (x: [BH][n_new][64T] fp16) after tok0 tokens.
+// ws: u32 [BH][n_chunks] chunk totals followed by u32 [BH] stream bases.
+hipError_t launch_compress(const CacheView& c, const uint16_t* x, int n_new, int tok0, uint32_t* ws,
+                           hipStream_t s);
+// Compress one token per stream (x: [BH][64T]) as token tok0.
+hipError_t launch_append(const CacheView& c, const uint16_t* x, int tok0, hipStream_t s);
+
+struct SparseSide {
+  const uint64_t* bitmaps;
+  const uint32_t* offsets;
+  const uint16_t* values;
+  int64_t val_stride;
+  int cap_tokens;
+  int n_keep;
+};
+
+struct AttnShape {
+  int BHkv;       // streams
+  int G;          // query heads per kv-head
+  int T;          // tiles per token
+  int n_s;        // compressed tokens per stream (0 for the dense kernel)
+  int n_dense;    // dense tokens per stream (window, or the whole dense cache)
+  int n_sparse_segs, sparse_seg_tokens;
+  int n_dense_segs, dense_seg_tokens;
+  float scale_log2;  // score scale times log2(e)
+};
+
+// Partial results of every segment into ws_ml [n_seg][BHq] (max, sum) and
+// ws_o [n_seg][BHq][d], then the merge into out [BHq][d] fp16.
+hipError_t launch_attention(const AttnShape& sh, const uint16_t* q, const SparseSide& K,
+                            const SparseSide& V, const uint16_t* kd, const uint16_t* vd,
+                            float* ws_ml, float* ws_o, uint16_t* out, hipStream_t s);
+
+}  // namespace mf

@@ -1,0 +1,180 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library must load on a machine without a GPU, export every function that
+include/mustafar.h declares, lay out mustafar_ccache_t as the C compiler does,
+and reject every invalid call before anything is launched.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import oracle
+import paper_2505_22913_amd as mf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mustafar.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(mf.LIB_PATH):
+        from paper_2505_22913_amd import build_lib
+        build_lib.build()
+    return mf.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mustafar_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_expected_entry_points():
+    names = declared_functions()
+    for n in ("mustafar_prune_compress", "mustafar_append", "mustafar_sparse_decode_attn",
+              "mustafar_dense_decode_attn", "mustafar_keep_count", "mustafar_strerror"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", mf.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT\s+(mustafar_\w+)", out))
+    missing = [n for n in declared_functions() if n not in exported]
+    assert not missing, missing
+    for n in declared_functions():
+        assert hasattr(lib, n)
+
+
+def test_struct_layout_matches_the_c_compiler(tmp_path):
+    prog = tmp_path / "layout.c"
+    prog.write_text(
+        '#include <stddef.h>\n#include <stdio.h>\n#include "mustafar.h"\n'
+        "int main(void){printf(\"%zu %zu %zu %zu %zu\\n\", sizeof(mustafar_ccache_t),"
+        " offsetof(mustafar_ccache_t, B), offsetof(mustafar_ccache_t, n_keep),"
+        " offsetof(mustafar_ccache_t, n_tokens), offsetof(mustafar_ccache_t, val_stride));"
+        "return 0;}\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c11", f"-I{os.path.dirname(HEADER)}", "-o", str(exe), str(prog)],
+                   check=True)
+    c_vals = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                             check=True).stdout.split()]
+    T = mf.ccache_t
+    assert c_vals == [ctypes.sizeof(T), T.B.offset, T.n_keep.offset, T.n_tokens.offset,
+                      T.val_stride.offset]
+
+
+def test_keep_count_agrees_with_the_oracle_reading(lib):
+    for d in (64, 128, 256):
+        for i in range(0, 1001):
+            s = i / 1000.0
+            assert mf.mustafar_keep_count(d, s) == oracle.keep_count(d, s), (d, s)
+    for bad in (-0.01, 1.01, float("nan")):
+        assert lib.mustafar_keep_count(128, bad) == mf.EINVAL
+    assert lib.mustafar_keep_count(0, 0.5) == mf.EINVAL
+
+
+def test_capacity_bounds(lib):
+    assert mf.mustafar_token_max_elems(128, 64) == 72    # two tiles, each padded by < 8
+    assert mf.mustafar_token_max_elems(128, 128) == 128  # full tiles need no padding
+    assert mf.mustafar_token_max_elems(128, 0) == 0
+    assert mf.mustafar_token_max_elems(128, 1) == 8
+    assert mf.mustafar_token_max_elems(64, 38) == 40
+    assert mf.mustafar_token_max_elems(256, 77) == 104
+    assert mf.mustafar_token_max_elems(96, 10) == -1      # not a whole number of tiles
+    assert mf.mustafar_stream_capacity(128, 38, 1000) == 1000 * 48
+
+
+def _fake_cache(B=2, H=4, d=128, s=0.5, cap=100, stride=None):
+    """Descriptor over fake (never dereferenced) aligned addresses."""
+    c = mf.ccache_t()
+    k = max(mf.lib().mustafar_keep_count(d, s), 0)
+    if stride is None:
+        stride = max(mf.mustafar_stream_capacity(d, k, cap), 8)
+    st = mf.lib().mustafar_ccache_init(ctypes.byref(c), 0x100000, 0x200000, 0x300000, 0x400000,
+                                       B, H, d, s, cap, stride)
+    return c, st
+
+
+def test_ccache_init_validates(lib):
+    c, st = _fake_cache()
+    assert st == mf.OK and c.n_keep == 64 and c.n_tokens == 0
+    assert _fake_cache(d=96)[1] == mf.EINVAL
+    assert _fake_cache(s=1.5)[1] == mf.EINVAL
+    assert _fake_cache(cap=0)[1] == mf.EINVAL
+    assert _fake_cache(stride=8)[1] == mf.EINVAL                    # below worst case
+    assert _fake_cache(stride=100 * 72 + 4)[1] == mf.EINVAL         # not a multiple of 8
+    c2 = mf.ccache_t()
+    assert lib.mustafar_ccache_init(ctypes.byref(c2), 0x100001, 0x200000, 0x300000, 0x400000,
+                                    1, 1, 128, 0.5, 10, 720) == mf.EINVAL  # misaligned bitmaps
+    assert lib.mustafar_ccache_init(ctypes.byref(c2), 0, 0x200000, 0x300000, 0x400000,
+                                    1, 1, 128, 0.5, 10, 720) == mf.EINVAL  # null
+
+
+def test_compress_and_append_reject_before_launch(lib):
+    c, _ = _fake_cache(B=2, H=4, cap=100)
+    ws_need = lib.mustafar_compress_workspace_bytes(2, 4, 50)
+    assert ws_need == 2 * 4 * (1 + 1) * 4
+    x = 0x500000
+    assert lib.mustafar_prune_compress(ctypes.byref(c), x, 0, 0x600000, ws_need, None) == mf.EINVAL
+    assert lib.mustafar_prune_compress(ctypes.byref(c), x + 2, 50, 0x600000, ws_need,
+                                       None) == mf.EINVAL
+    assert lib.mustafar_prune_compress(ctypes.byref(c), x, 101, 0x600000, 10 ** 6,
+                                       None) == mf.ECAPACITY
+    assert lib.mustafar_prune_compress(ctypes.byref(c), x, 50, 0x600000, ws_need - 1,
+                                       None) == mf.EWORKSPACE
+    assert lib.mustafar_prune_compress(ctypes.byref(c), x, 50, None, ws_need,
+                                       None) == mf.EWORKSPACE
+    c.n_tokens = 100
+    assert lib.mustafar_append(ctypes.byref(c), x, None) == mf.ECAPACITY
+    assert lib.mustafar_prune_compress(ctypes.byref(c), x, 1, 0x600000, 10 ** 6,
+                                       None) == mf.ECAPACITY
+    c.n_tokens = 101
+    assert lib.mustafar_append(ctypes.byref(c), x, None) == mf.EINVAL   # corrupt descriptor
+    assert c.n_tokens == 101                                             # nothing changed
+
+
+def test_decode_attention_rejects_before_launch(lib):
+    K, _ = _fake_cache(B=2, H=4)
+    V, _ = _fake_cache(B=2, H=4, s=0.7)
+    K.n_tokens = V.n_tokens = 50
+    q, out, kt, vt = 0x700000, 0x800000, 0x900000, 0xa00000
+    need = lib.mustafar_attn_workspace_bytes(2, 16, 4, 128, 50, 0)
+    assert need > 0
+    call = lambda **kw: lib.mustafar_sparse_decode_attn(  # noqa: E731
+        kw.get("q", q), kw.get("B", 2), kw.get("Hq", 16), ctypes.byref(kw.get("K", K)),
+        ctypes.byref(kw.get("V", V)), kw.get("kt", kt), kw.get("vt", vt), kw.get("n_tail", 32),
+        0.0, kw.get("out", out), kw.get("splits", 0), kw.get("ws", 0xb00000),
+        kw.get("ws_bytes", need), None)
+    assert call(Hq=12) == mf.EUNSUPPORTED       # group size 3
+    assert call(Hq=10) == mf.EINVAL             # not a multiple of Hkv
+    assert call(B=3) == mf.EINVAL               # batch mismatch with the caches
+    assert call(q=q + 8) == mf.EINVAL           # misaligned q
+    assert call(out=None) == mf.EINVAL
+    assert call(kt=None) == mf.EINVAL           # window tokens but no window
+    assert call(n_tail=-1) == mf.EINVAL
+    assert call(ws_bytes=need - 4) == mf.EWORKSPACE
+    assert call(ws=None) == mf.EWORKSPACE
+    V2, _ = _fake_cache(B=2, H=4, s=0.7)
+    V2.n_tokens = 49
+    assert call(V=V2) == mf.EINVAL              # K and V token counts differ
+    K0, _ = _fake_cache(B=2, H=4)
+    V0, _ = _fake_cache(B=2, H=4)
+    assert call(K=K0, V=V0, n_tail=0, kt=None, vt=None) == mf.EINVAL   # no tokens at all
+    dense = lambda **kw: lib.mustafar_dense_decode_attn(  # noqa: E731
+        q, 2, kw.get("Hq", 16), 4, kw.get("k", kt), vt, kw.get("n", 50), kw.get("d", 128), 0.0,
+        out, 0, 0xb00000, kw.get("ws_bytes", need), None)
+    assert dense(n=0) == mf.EINVAL
+    assert dense(d=100) == mf.EINVAL
+    assert dense(Hq=24) == mf.EUNSUPPORTED
+    assert dense(k=kt + 4) == mf.EINVAL
+    assert dense(ws_bytes=16) == mf.EWORKSPACE
+
+
+def test_strerror_covers_every_status(lib):
+    for code in (mf.OK, mf.EINVAL, mf.ECAPACITY, mf.EWORKSPACE, mf.ELAUNCH, mf.EUNSUPPORTED):
+        assert mf.strerror(code) not in ("", "unknown status")
+    assert mf.strerror(-99) == "unknown status"

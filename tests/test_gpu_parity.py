@@ -1,0 +1,194 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Compression: bitmaps, offsets, stream lengths and packed values (padding
+included) must equal the oracle bit for bit. Attention: per output vector,
+max|o_gpu - o_ref| / max|o_ref| <= 2e-3 (fp16 in/out, fp32 accumulation on
+the GPU, float64 in the oracle); the fp16 rounding of the output alone is
+below 2.5e-4 of max|o|.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2505_22913_amd as mf
+from paper_2505_22913_amd import synth
+from tests.gpu_common import (ATTN_TOL, all_pairs, announce, attn_error, compare_format,
+                              read_cache, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+def _compress_gpu(x: np.ndarray, s: float, cap=None):
+    B, H, N, d = x.shape
+    cache = mf.CompressedCache(B, H, d, s, cap or N)
+    mf.mustafar_prune_compress(cache, to_dev(x))
+    return cache
+
+
+def _tie_heavy(B, H, N, d, seed):
+    rng = np.random.default_rng(seed)
+    mags = np.array([0.0, 2.0 ** -24, 2.0 ** -20, 0.5, 1.0, 1.0, 1.0, 2.0], dtype=np.float32)
+    x = rng.choice(mags, size=(B, H, N, d)) * rng.choice([-1.0, 1.0], size=(B, H, N, d))
+    return x.astype(np.float16)
+
+
+# ---------------------------------------------------------------------------------------------
+# compression
+# ---------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("s", [0.0, 0.3, 0.5, 0.7, 0.8, 0.9, 1.0])
+@pytest.mark.parametrize("N", [1, 63, 64, 65, 257, 1000])
+def test_compress_bit_exact_d128(N, s):
+    announce(f"compress d=128 N={N} s={s}")
+    K, V = synth.make_kv(2, 3, N, 128, seed=100 + N)
+    for x in (K, V):
+        got = read_cache(_compress_gpu(x, s))
+        compare_format(got, oracle.compress(x, s), N, all_pairs(2, 3))
+
+
+@pytest.mark.parametrize("d", [64, 256])
+@pytest.mark.parametrize("s", [0.0, 0.5, 0.7, 0.9, 1.0])
+def test_compress_bit_exact_other_head_dims(d, s):
+    announce(f"compress d={d} s={s}")
+    N = 300
+    K, V = synth.make_kv(1, 4, N, d, seed=200 + d)
+    for x in (K, V):
+        got = read_cache(_compress_gpu(x, s))
+        compare_format(got, oracle.compress(x, s), N, all_pairs(1, 4))
+
+
+@pytest.mark.parametrize("d", [64, 128, 256])
+@pytest.mark.parametrize("s", [0.25, 0.5, 0.7, 0.95])
+def test_compress_ties_zeros_and_subnormals(d, s):
+    announce(f"compress ties d={d} s={s}")
+    x = _tie_heavy(2, 2, 130, d, seed=d)
+    x[0, 0, 0] = np.float16(1.0)             # a token of all-equal magnitudes
+    x[0, 0, 1] = np.float16(-1.0)
+    x[0, 0, 2] = np.float16(0.0)             # all zeros: ties everywhere at +0
+    x[0, 0, 3, ::2] = np.float16(-0.0)       # -0 and +0 compare equal
+    got = read_cache(_compress_gpu(x, s))
+    compare_format(got, oracle.compress(x, s), 130, all_pairs(2, 2))
+
+
+def test_compress_in_pieces_and_append_equal_compress_all():
+    announce("compress pieces + append")
+    B, H, d = 2, 4, 128
+    n0, n1, n2 = 300, 100, 57
+    K, _ = synth.make_kv(B, H, n0 + n1 + n2, d, seed=7)
+    for s in (0.5, 0.7):
+        cache = mf.CompressedCache(B, H, d, s, n0 + n1 + n2)
+        mf.mustafar_prune_compress(cache, to_dev(np.ascontiguousarray(K[:, :, :n0])))
+        mf.mustafar_prune_compress(cache, to_dev(np.ascontiguousarray(K[:, :, n0:n0 + n1])))
+        for j in range(n0 + n1, n0 + n1 + n2):
+            mf.mustafar_append(cache, to_dev(np.ascontiguousarray(K[:, :, j])))
+        assert cache.n_tokens == n0 + n1 + n2
+        compare_format(read_cache(cache), oracle.compress(K, s), n0 + n1 + n2, all_pairs(B, H))
+
+
+def test_append_into_empty_cache_and_capacity_error():
+    announce("append empty + capacity")
+    B, H, d = 1, 2, 64
+    K, _ = synth.make_kv(B, H, 3, d, seed=8)
+    cache = mf.CompressedCache(B, H, d, 0.5, 3)
+    for j in range(3):
+        mf.mustafar_append(cache, to_dev(np.ascontiguousarray(K[:, :, j])))
+    compare_format(read_cache(cache), oracle.compress(K, 0.5), 3, all_pairs(B, H))
+    with pytest.raises(mf.MustafarError) as e:
+        mf.mustafar_append(cache, to_dev(np.ascontiguousarray(K[:, :, 0])))
+    assert e.value.status == mf.ECAPACITY
+
+
+# ---------------------------------------------------------------------------------------------
+# decode attention
+# ---------------------------------------------------------------------------------------------
+def _attn_case(B, Hkv, G, Ns, Nd, d, sK, sV, splits, seed, scale=0.0):
+    announce(f"attn B={B} Hkv={Hkv} G={G} Ns={Ns} Nd={Nd} d={d} s=({sK},{sV}) splits={splits}")
+    K, V = synth.make_kv(B, Hkv, Ns, d, seed=seed)
+    KL, VL = synth.make_tail(B, Hkv, Nd, d, seed=seed)
+    q = synth.make_q(B, Hkv * G, d, seed=seed)
+    cap = max(Ns, 1)
+    Kc = mf.CompressedCache(B, Hkv, d, sK, cap)
+    Vc = mf.CompressedCache(B, Hkv, d, sV, cap)
+    if Ns > 0:
+        mf.mustafar_prune_compress(Kc, to_dev(K))
+        mf.mustafar_prune_compress(Vc, to_dev(V))
+    kt = to_dev(KL) if Nd > 0 else None
+    vt = to_dev(VL) if Nd > 0 else None
+    out = mf.mustafar_sparse_decode_attn(to_dev(q), Kc, Vc, kt, vt, scale=scale, n_splits=splits)
+    got = out.cpu().numpy()
+    ref = oracle.sparse_decode_attention(q, oracle.compress(K, sK), oracle.compress(V, sV),
+                                         KL, VL, scale=scale)
+    err = attn_error(got, ref)
+    assert err <= ATTN_TOL, err
+    return err
+
+
+@pytest.mark.parametrize("G", [1, 2, 4, 8])
+@pytest.mark.parametrize("Nd", [0, 1, 31, 32])
+def test_attention_group_sizes_and_windows(G, Nd):
+    _attn_case(B=2, Hkv=2, G=G, Ns=700, Nd=Nd, d=128, sK=0.5, sV=0.7, splits=0, seed=G * 10 + Nd)
+
+
+@pytest.mark.parametrize("Ns", [0, 1, 64, 4095])
+@pytest.mark.parametrize("splits", [1, 2, 7, 64])
+def test_attention_lengths_and_splits(Ns, splits):
+    _attn_case(B=1, Hkv=4, G=4, Ns=Ns, Nd=32, d=128, sK=0.7, sV=0.7, splits=splits, seed=Ns + 3)
+
+
+@pytest.mark.parametrize("d", [64, 256])
+@pytest.mark.parametrize("G", [1, 4])
+def test_attention_other_head_dims(d, G):
+    _attn_case(B=2, Hkv=2, G=G, Ns=333, Nd=32, d=d, sK=0.5, sV=0.5, splits=0, seed=d + G)
+
+
+@pytest.mark.parametrize("sK,sV", [(0.0, 0.0), (0.9, 0.9), (1.0, 0.5), (0.5, 1.0), (1.0, 1.0)])
+def test_attention_extreme_sparsities(sK, sV):
+    _attn_case(B=1, Hkv=2, G=2, Ns=200, Nd=5, d=128, sK=sK, sV=sV, splits=3, seed=31)
+
+
+def test_attention_custom_scale():
+    _attn_case(B=1, Hkv=2, G=1, Ns=128, Nd=32, d=128, sK=0.5, sV=0.5, splits=2, seed=5,
+               scale=0.02)
+
+
+def test_attention_only_window():
+    _attn_case(B=2, Hkv=2, G=2, Ns=0, Nd=200, d=128, sK=0.5, sV=0.5, splits=0, seed=6)
+
+
+@pytest.mark.parametrize("G", [1, 4])
+@pytest.mark.parametrize("splits", [0, 1, 5])
+def test_dense_attention_parity(G, splits):
+    announce(f"dense attn G={G} splits={splits}")
+    B, Hkv, N, d = 2, 3, 1000, 128
+    K, V = synth.make_kv(B, Hkv, N, d, seed=9)
+    q = synth.make_q(B, Hkv * G, d, seed=9)
+    got = mf.mustafar_dense_decode_attn(to_dev(q), to_dev(K), to_dev(V), n_splits=splits)
+    ref = oracle.decode_attention(q, np.zeros((B, Hkv, 0, d), np.float16),
+                                  np.zeros((B, Hkv, 0, d), np.float16), K, V)
+    assert attn_error(got.cpu().numpy(), ref) <= ATTN_TOL
+
+
+def test_decode_loop_append_then_attend():
+    """Paper's decode step: the token leaving the window is pruned, compressed and
+    appended, then attention runs over compressed + window (Sec. 3)."""
+    B, Hkv, G, d, n0, steps, W = 1, 4, 4, 128, 500, 12, 32
+    announce("decode loop")
+    K, V = synth.make_kv(B, Hkv, n0 + steps + W, d, seed=12)
+    q = synth.make_q(B, Hkv * G, d, seed=12)
+    Kc = mf.CompressedCache(B, Hkv, d, 0.7, n0 + steps)
+    Vc = mf.CompressedCache(B, Hkv, d, 0.7, n0 + steps)
+    mf.mustafar_prune_compress(Kc, to_dev(np.ascontiguousarray(K[:, :, :n0])))
+    mf.mustafar_prune_compress(Vc, to_dev(np.ascontiguousarray(V[:, :, :n0])))
+    qd = to_dev(q)
+    for step in range(steps + 1):
+        ns = n0 + step
+        win_k = np.ascontiguousarray(K[:, :, ns:ns + W])
+        win_v = np.ascontiguousarray(V[:, :, ns:ns + W])
+        got = mf.mustafar_sparse_decode_attn(qd, Kc, Vc, to_dev(win_k), to_dev(win_v))
+        if step in (0, 1, steps):
+            ref = oracle.sparse_decode_attention(
+                q, oracle.compress(np.ascontiguousarray(K[:, :, :ns]), 0.7),
+                oracle.compress(np.ascontiguousarray(V[:, :, :ns]), 0.7), win_k, win_v)
+            assert attn_error(got.cpu().numpy(), ref) <= ATTN_TOL, step
+        if step < steps:
+            mf.mustafar_append(Kc, to_dev(np.ascontiguousarray(K[:, :, ns])))
+            mf.mustafar_append(Vc, to_dev(np.ascontiguousarray(V[:, :, ns])))
