@@ -1,0 +1,253 @@
+"""Benchmark of the MUSTAFAR decode hot path on one MI355X.
+
+A step is one decode step of the method on the whole batch (Sec. 3): the token
+leaving the dense local window of every (batch, kv-head) is pruned, compressed
+and appended to the compressed K and V caches, then sparse decode attention
+runs over compressed caches + the 32-token dense window (Algorithm 1).
+value = batch * steps / time: decode tokens per second of the whole job.
+
+Also measured (reported in the same JSON line):
+  * the bulk prune+compress of the whole prefill cache (K and V),
+  * the attention call alone: time, algorithmic HBM GB/s and roofline fraction
+    (bytes the format makes the kernel read: 12 B of bitmap+offset per tile,
+    the packed values with padding, the window, q and the output),
+  * the in-house dense fp16 decode-attention kernel on the same tokens,
+  * the CPU oracle on a bounded sample of streams (cpu_baseline).
+
+Inputs are synthetic (paper_2505_22913_amd.synth), generated on the GPU and
+resident in HBM before any timed region starts.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "sparse decode-attn tokens/s + HBM GB/s (% roofline); prune+compress tokens/s"
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mha-b16-32k")
+    ap.add_argument("--splits", type=int, default=0, help="split-K segments (0: library default)")
+    ap.add_argument("--seed", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-streams", type=int, default=48)
+    ap.add_argument("--cpu-threads", type=int, default=0, help="0: min(16, cpu count)")
+    return ap.parse_args()
+
+
+def attn_alg_bytes(w, k_len_total: int, v_len_total: int, n_s: int) -> int:
+    """Bytes one sparse attention launch must move (format + window + q + out)."""
+    T = w.d // 64
+    tiles = w.B * w.Hkv * n_s * T
+    meta = 12 * tiles * 2                       # K and V: 8-byte bitmap + 4-byte offset per tile
+    vals = 2 * (k_len_total + v_len_total)      # packed fp16 values incl. padding
+    window = 2 * 2 * w.B * w.Hkv * w.n_tail * w.d
+    qo = 2 * 2 * w.B * w.Hq * w.d
+    return meta + vals + window + qo
+
+
+def cpu_baseline(w, K, V, KL, VL, q, sample: int, threads: int) -> dict:
+    """Oracle (untuned, as in the test suite) on `sample` (b, h) streams of the
+    same workload; the decode-step time is scaled to all B*Hkv streams."""
+    import numpy as np
+
+    import oracle
+    BH = w.B * w.Hkv
+    sample = max(1, min(sample, BH))
+    picks = np.linspace(0, BH - 1, sample).round().astype(int)
+    Ks = np.stack([K[p // w.Hkv, p % w.Hkv].cpu().numpy() for p in picks])[:, None]
+    Vs = np.stack([V[p // w.Hkv, p % w.Hkv].cpu().numpy() for p in picks])[:, None]
+    KLs = np.stack([KL[p // w.Hkv, p % w.Hkv].cpu().numpy() for p in picks])[:, None]
+    VLs = np.stack([VL[p // w.Hkv, p % w.Hkv].cpu().numpy() for p in picks])[:, None]
+    G = w.G
+    qs = np.stack([q[p // w.Hkv, (p % w.Hkv) * G:(p % w.Hkv + 1) * G].cpu().numpy()
+                   for p in picks])
+    Ks = Ks.reshape(sample, 1, w.N, w.d)
+    Vs = Vs.reshape(sample, 1, w.N, w.d)
+    oracle.build()
+    t0 = time.perf_counter()
+    ek = oracle.compress(Ks, w.sK, threads=threads)
+    ev = oracle.compress(Vs, w.sV, threads=threads)
+    t_pc = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.sparse_decode_attention(qs, ek, ev, KLs.reshape(sample, 1, w.n_tail, w.d),
+                                   VLs.reshape(sample, 1, w.n_tail, w.d), threads=threads)
+    t_attn = time.perf_counter() - t0
+    scale = BH / sample
+    step_s = t_attn * scale            # the append of one token per stream is negligible
+    return {"value": w.B / step_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{sample} of {BH} (batch, kv-head) streams of the same workload; "
+                      f"decode attention (decompress + float64 Algorithm 1) scaled by {scale:.2f}",
+            "attn_s_per_step_est": step_s,
+            "prune_compress_tokens_per_s": sample * w.N / t_pc,
+            "wall_s": t_pc + t_attn}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build measures one GPU only; the (batch, kv-head) "
+                                   "streams shard without communication (see the design notes)",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2505_22913_amd as mf
+    from paper_2505_22913_amd import synth
+
+    w = synth.WORKLOADS[args.workload]
+    steps, warm = args.steps, args.warmup
+    torch.cuda.set_device(0)
+    dev = "cuda"
+    cap = w.N + warm + steps + 1
+
+    # ---- synthetic inputs, resident in HBM ----
+    K, V = synth.make_kv_torch(w.B, w.Hkv, w.N + w.n_tail, w.d, seed=args.seed, device=dev)
+    KL = K[:, :, w.N:].contiguous()                    # dense window
+    VL = V[:, :, w.N:].contiguous()
+    Kp = K[:, :, :w.N].contiguous()
+    Vp = V[:, :, :w.N].contiguous()
+    gq = torch.Generator(device=dev)
+    gq.manual_seed(args.seed)
+    q = torch.randn((w.B, w.Hq, w.d), generator=gq, device=dev).half()
+    new_k = KL[:, :, 0].contiguous()                  # the token leaving the window each step
+    new_v = VL[:, :, 0].contiguous()
+    Kc = mf.CompressedCache(w.B, w.Hkv, w.d, w.sK, cap, device=dev)
+    Vc = mf.CompressedCache(w.B, w.Hkv, w.d, w.sV, cap, device=dev)
+    ws_c = torch.empty(mf.mustafar_compress_workspace_bytes(w.B, w.Hkv, w.N), dtype=torch.uint8,
+                       device=dev)
+    ws_a = torch.empty(mf.mustafar_attn_workspace_bytes(w.B, w.Hq, w.Hkv, w.d, cap, args.splits),
+                       dtype=torch.uint8, device=dev)
+    out = torch.empty((w.B, w.Hq, w.d), dtype=torch.float16, device=dev)
+    torch.cuda.synchronize()
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+
+    # ---- bulk prune + compress of the prefill cache (K and V), timed ----
+    pc_ms = []
+    for rep in range(3):
+        Kc.desc.n_tokens = 0
+        Vc.desc.n_tokens = 0
+        a, b = ev(), ev()
+        a.record()
+        mf.mustafar_prune_compress(Kc, Kp, ws_c)
+        mf.mustafar_prune_compress(Vc, Vp, ws_c)
+        b.record()
+        torch.cuda.synchronize()
+        pc_ms.append(a.elapsed_time(b))
+    t_pc = float(np.median(pc_ms)) / 1e3
+    k_len0 = int(Kc.stream_len.to(torch.int64).sum().item())
+    v_len0 = int(Vc.stream_len.to(torch.int64).sum().item())
+
+    # ---- dense baseline over the same tokens ----
+    ws_d = torch.empty(mf.mustafar_attn_workspace_bytes(w.B, w.Hq, w.Hkv, w.d, w.N + w.n_tail,
+                                                        args.splits), dtype=torch.uint8, device=dev)
+    for _ in range(3):
+        mf.mustafar_dense_decode_attn(q, K, V, out=out, n_splits=args.splits, ws=ws_d)
+    torch.cuda.synchronize()
+    a, b = ev(), ev()
+    n_dense_reps = 10
+    a.record()
+    for _ in range(n_dense_reps):
+        mf.mustafar_dense_decode_attn(q, K, V, out=out, n_splits=args.splits, ws=ws_d)
+    b.record()
+    torch.cuda.synchronize()
+    t_dense = a.elapsed_time(b) / 1e3 / n_dense_reps
+    dense_bytes = 2 * 2 * w.B * w.Hkv * (w.N + w.n_tail) * w.d + 4 * w.B * w.Hq * w.d
+
+    # ---- decode steps: append (prune+compress one token per stream) + attention ----
+    def step(marks=None):
+        mf.mustafar_append(Kc, new_k)
+        mf.mustafar_append(Vc, new_v)
+        if marks is not None:
+            marks[0].record()
+        mf.mustafar_sparse_decode_attn(q, Kc, Vc, KL, VL, out=out, n_splits=args.splits, ws=ws_a)
+        if marks is not None:
+            marks[1].record()
+
+    for _ in range(warm):
+        step()
+    torch.cuda.synchronize()
+    n_s_start = Kc.n_tokens
+    marks = [(ev(), ev()) for _ in range(steps)]
+    t_start, t_end = ev(), ev()
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record()
+    for i in range(steps):
+        step(marks[i])
+    t_end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_s = t_start.elapsed_time(t_end) / 1e3
+    attn_s = float(np.mean([m[0].elapsed_time(m[1]) for m in marks])) / 1e3
+    n_s_end = Kc.n_tokens
+
+    # algorithmic bytes of the attention launches, averaged over the timed steps
+    k_len1 = int(Kc.stream_len.to(torch.int64).sum().item())
+    v_len1 = int(Vc.stream_len.to(torch.int64).sum().item())
+    per_tok_k = (k_len1 - k_len0) / max(1, n_s_end - w.N)
+    per_tok_v = (v_len1 - v_len0) / max(1, n_s_end - w.N)
+    alg = []
+    for n_s in range(n_s_start + 1, n_s_end + 1):
+        extra = n_s - w.N
+        alg.append(attn_alg_bytes(w, int(k_len0 + per_tok_k * extra), int(v_len0 + per_tok_v * extra),
+                                  n_s))
+    alg_bytes = float(np.mean(alg))
+    attn_gbs = alg_bytes / attn_s / 1e9
+    dense_kv = 2 * 2 * w.B * w.Hkv * w.N * w.d
+    comp_kv = 12 * w.B * w.Hkv * w.N * (w.d // 64) * 2 + 2 * (k_len0 + v_len0)
+
+    result = {
+        "metric": METRIC,
+        "value": w.B * steps / total_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warm,
+        "ms_per_step": total_s / steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic (seeded; K with 4 outlier channels x10 per head, V and q N(0,1))",
+        "config": {"workload": w.name, "batch": w.B, "q_heads": w.Hq, "kv_heads": w.Hkv,
+                   "context": w.N, "head_dim": w.d, "window": w.n_tail, "k_sparsity": w.sK,
+                   "v_sparsity": w.sV, "splits": args.splits or
+                   mf.mustafar_attn_default_splits(w.B, w.Hkv, n_s_end)},
+        "attention": {"us": attn_s * 1e6, "tokens_per_s": w.B / attn_s,
+                      "kv_tokens_per_s": w.B * w.Hkv * (n_s_end + w.n_tail) / attn_s,
+                      "alg_bytes": alg_bytes, "gb_s": attn_gbs},
+        "roofline": {"bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": attn_gbs / HBM_PEAK_GBS, "traffic": None},
+        "dense_baseline": {"us": t_dense * 1e6, "tokens_per_s": w.B / t_dense,
+                           "gb_s": dense_bytes / t_dense / 1e9},
+        "speedup_vs_dense": t_dense / attn_s,
+        "prune_compress": {"ms": t_pc * 1e3, "tokens_per_s": w.B * w.Hkv * w.N / t_pc,
+                           "gb_s": (dense_kv + comp_kv) / t_pc / 1e9},
+        "append_us_per_step": (total_s / steps - attn_s) * 1e6,
+        "compression_ratio": comp_kv / dense_kv,
+        "wall_s_timed": wall,
+    }
+    if not args.no_cpu_baseline:
+        threads = args.cpu_threads or min(16, os.cpu_count() or 1)
+        result["cpu_baseline"] = cpu_baseline(w, Kp, Vp, KL, VL, q, args.cpu_sample_streams,
+                                              threads)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

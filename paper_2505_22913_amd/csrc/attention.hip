@@ -4,23 +4,38 @@
 // one-wave workgroup computes, for the G query heads of its kv-head, the
 // running max, running sum and unnormalised output of one segment (online
 // softmax), and k_merge combines the segments with their log-sum-exp weights.
-// Compressed segments come first, then the dense window, so the softmax spans
-// concat(S_C, S_L) exactly as Algorithm 1 states; the merge is order-free.
+// The sparse call launches the compressed segments and the dense-window
+// segment in one grid, so the softmax spans concat(S_C, S_L) as Algorithm 1
+// states (the merge is order-free). The dense baseline reuses the dense body.
 //
-// Compressed blocks are handled "load as compressed, expand in LDS":
-//   * the packed values of a block of NB = 64/T tokens are one contiguous run
-//     of the stream; they are staged into LDS with 16-byte coalesced loads;
-//   * lane (j, t) owns tile t of token j and walks the set bits of its bitmap,
-//     reading its packed values in order: the q.k partial uses q from LDS, the
-//     value tile is expanded into a dense LDS tile (zeros where pruned);
-//   * p.V then runs with one lane per channel over the dense value tile.
-// All arithmetic on fp16 data accumulates in fp32.
+// Compressed blocks of NB = 64/T tokens ("load as compressed, expand in LDS"):
+//   * the packed values of a block are one contiguous run of the stream; the
+//     next block's runs are fetched into registers with 16-byte coalesced
+//     loads while the current block is computed, then written to LDS;
+//   * lane (j, t) owns tile t of token j and walks the set bits of each
+//     32-bit half of its bitmap with v_ffbl, reading its packed values in
+//     order. A lane with no bits left gets the index -1, which points at a
+//     zero slot of the q table (its product is 0) and at a scratch slot of the
+//     expanded value tile, so the walk has no per-element branch; it runs in
+//     groups of 4 while any lane has bits left;
+//   * p.V runs with one lane per channel over the expanded value tile, two
+//     tokens at a time with v_dot2 (fp16 probabilities, fp32 accumulation).
 #include "mf_device.h"
 #include "mf_launch.h"
 
 namespace mf {
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Reinterpret 32 bits as two fp16. Takes the word BY VALUE: __builtin_bit_cast
+// applied directly to an ext-vector element (w.y) reinterprets element 0.
+__device__ __forceinline__ half2_t as_h2(uint32_t w) { return __builtin_bit_cast(half2_t, w); }
+
+// Per tile and per 32-channel half, one scratch slot precedes the channels:
+// [s][ch 0..31][s][ch 32..63] -- slot of channel c is 1 + c + (c >= 32).
+constexpr int kSlots = 66;
 
 struct AttnArgs {
   const uint16_t* q;
@@ -37,197 +52,421 @@ struct AttnArgs {
   int kmaxK, kmaxV;  // worst-case fp16 elements per token of each cache
 };
 
-__device__ __forceinline__ uint32_t first_set_and_clear(uint32_t& bits) {
-  const uint32_t c = (uint32_t)__builtin_ctz(bits);
-  bits &= bits - 1u;
-  return c;
+__device__ __forceinline__ uint32_t ffbl(uint32_t x) {  // 0xffffffff when x == 0
+  uint32_t r;
+  asm("v_ffbl_b32 %0, %1" : "=v"(r) : "v"(x));
+  return r;
 }
 
-template <int T, int G>
-__device__ __forceinline__ void softmax_update(float (&acc)[G], bool valid, uint32_t t, uint32_t j,
-                                               float scale_log2, float (&m_run)[G],
-                                               float (&l_run)[G], float (&o)[G][T],
-                                               float* __restrict__ ps) {
-#pragma unroll
-  for (int sft = 1; sft < T; sft <<= 1) {
-#pragma unroll
-    for (int g = 0; g < G; ++g) acc[g] += __shfl_xor(acc[g], sft, kWave);
-  }
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const float sc = valid ? acc[g] * scale_log2 : -INFINITY;
-    const float mnew = fmaxf(m_run[g], wave_max(sc));
-    const float alpha = __builtin_amdgcn_exp2f(m_run[g] - mnew);
-    const float pj = valid ? __builtin_amdgcn_exp2f(sc - mnew) : 0.f;
-    const float bsum = wave_sum(t == 0 ? pj : 0.f);
-    l_run[g] = l_run[g] * alpha + bsum;
-    m_run[g] = mnew;
-#pragma unroll
-    for (int tt = 0; tt < T; ++tt) o[g][tt] *= alpha;
-    if (t == 0 && valid) ps[j * G + g] = pj;
-  }
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
 }
 
-// grid (n_sparse_segs + n_dense_segs, BHkv), one wave per workgroup.
+__device__ __forceinline__ float swz_xor16(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
+}
+
+__device__ __forceinline__ float readlane_f(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+
+// Max / sum over all 64 lanes, returned wave-uniform: DPP within 16-lane rows,
+// a swizzle across row pairs, then the two 32-lane halves.
+__device__ __forceinline__ float wave_max_u(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp<0x124>(v));  // row_ror:4
+  v = fmaxf(v, dpp<0x128>(v));  // row_ror:8
+  v = fmaxf(v, swz_xor16(v));
+  return fmaxf(readlane_f(v, 0), readlane_f(v, 32));
+}
+
+__device__ __forceinline__ float wave_sum_u(float v) {
+  v += dpp<0xB1>(v);
+  v += dpp<0x4E>(v);
+  v += dpp<0x124>(v);
+  v += dpp<0x128>(v);
+  v += swz_xor16(v);
+  return readlane_f(v, 0) + readlane_f(v, 32);
+}
+
+// Sum over the T lanes (adjacent, T in {1,2,4}) that hold the tiles of one token.
+template <int T>
+__device__ __forceinline__ float tile_sum(float v) {
+  if constexpr (T >= 2) v += dpp<0xB1>(v);
+  if constexpr (T >= 4) v += dpp<0x4E>(v);
+  return v;
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)p;
+}
+
+template <typename V>
+__device__ __forceinline__ V lds_load(uint32_t byte_addr) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) V*>(byte_addr);
+}
+
+template <typename V>
+__device__ __forceinline__ void lds_store(uint32_t byte_addr, V v) {
+  *reinterpret_cast<__attribute__((address_space(3))) V*>(byte_addr) = v;
+}
+
+// ------------------------------------------------------------------------------------------
+// Dense segment body: the local window of the sparse call, or a range of a dense cache.
+// ------------------------------------------------------------------------------------------
 template <int T, int G>
-__global__ __launch_bounds__(64) void k_attn_partial(AttnArgs a) {
+__device__ __forceinline__ void dense_body(const AttnArgs& a, int dseg, int bh, unsigned char* smem,
+                                           float (&m_run)[G], float (&l_run)[G],
+                                           float (&o)[G][T]) {
   constexpr int d = kTile * T;
-  constexpr int NB = kWave / T;  // tokens per block: lane = (token j, tile t)
-  extern __shared__ __align__(16) unsigned char smem[];
-  uint16_t* qs = reinterpret_cast<uint16_t*>(smem);                       // [G][d]
-  float* ps = reinterpret_cast<float*>(smem + G * d * 2);                 // [NB][G]
-  uint16_t* vdense = reinterpret_cast<uint16_t*>(smem + G * d * 2 + NB * G * 4);  // [NB][d]
-  uint16_t* kst = vdense + NB * d;                                        // [NB*kmaxK]
-  uint16_t* vst = kst + ((NB * a.kmaxK + 7) & ~7);                        // [NB*kmaxV]
-
-  const int seg = blockIdx.x, bh = blockIdx.y;
+  constexpr int NB = kWave / T;
+  uint16_t* qs = reinterpret_cast<uint16_t*>(smem);           // [G][d]
+  float* ps = reinterpret_cast<float*>(smem + G * d * 2);     // [NB][G]
   const uint32_t lane = lane_id();
   const uint32_t j = lane / T, t = lane % T;
-
   const uint16_t* qsrc = a.q + (int64_t)bh * G * d;
   for (int i = lane; i < G * d; i += kWave) qs[i] = qsrc[i];
   __syncthreads();
 
-  float m_run[G], l_run[G], o[G][T];
+  const int j0 = dseg * a.dense_seg_tokens;
+  const int j1 = min(j0 + a.dense_seg_tokens, a.n_dense);
+  const uint16_t* kd = a.kd + (int64_t)bh * a.n_dense * d;
+  const uint16_t* vd = a.vd + (int64_t)bh * a.n_dense * d;
+  for (int b0 = j0; b0 < j1; b0 += NB) {
+    const int nb = min(NB, j1 - b0);
+    const bool valid = (int)j < nb;
+    float acc[G];
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    m_run[g] = -INFINITY;
-    l_run[g] = 0.f;
+    for (int g = 0; g < G; ++g) acc[g] = 0.f;
+    if (valid) {
+      const uint4* kr = reinterpret_cast<const uint4*>(kd + (int64_t)(b0 + (int)j) * d + kTile * t);
 #pragma unroll
-    for (int tt = 0; tt < T; ++tt) o[g][tt] = 0.f;
+      for (int i = 0; i < kTile / 8; ++i) {
+        const uint4 u = kr[i];
+        const half2_t k2[4] = {as_h2(u.x), as_h2(u.y),
+                               as_h2(u.z), as_h2(u.w)};
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const uint4 qq = *reinterpret_cast<const uint4*>(qs + g * d + kTile * t + 8 * i);
+          acc[g] = __builtin_amdgcn_fdot2(k2[0], as_h2(qq.x), acc[g], false);
+          acc[g] = __builtin_amdgcn_fdot2(k2[1], as_h2(qq.y), acc[g], false);
+          acc[g] = __builtin_amdgcn_fdot2(k2[2], as_h2(qq.z), acc[g], false);
+          acc[g] = __builtin_amdgcn_fdot2(k2[3], as_h2(qq.w), acc[g], false);
+        }
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float sc = valid ? tile_sum<T>(acc[g]) * a.scale_log2 : -INFINITY;
+      const float mnew = fmaxf(m_run[g], wave_max_u(sc));
+      const float alpha = __builtin_amdgcn_exp2f(m_run[g] - mnew);
+      const float pj = valid ? __builtin_amdgcn_exp2f(sc - mnew) : 0.f;
+      l_run[g] = l_run[g] * alpha + wave_sum_u(t == 0 ? pj : 0.f);
+      m_run[g] = mnew;
+#pragma unroll
+      for (int tt = 0; tt < T; ++tt) o[g][tt] *= alpha;
+      if (t == 0 && valid) ps[j * G + g] = pj;
+    }
+    __syncthreads();
+    for (int jj = 0; jj < nb; ++jj) {
+      float pv[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) pv[g] = ps[jj * G + g];
+      const uint16_t* vr = vd + (int64_t)(b0 + jj) * d;
+#pragma unroll
+      for (int tt = 0; tt < T; ++tt) {
+        const float v = half_bits_to_float(vr[lane + kTile * tt]);
+#pragma unroll
+        for (int g = 0; g < G; ++g) o[g][tt] = fmaf(pv[g], v, o[g][tt]);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Compressed segment body.
+// ------------------------------------------------------------------------------------------
+struct TileMeta {
+  uint64_t kb, vb;  // this lane's key / value tile bitmaps (0 past the block end)
+  uint32_t ko, vo;  // their offsets
+};
+
+template <int T>
+__device__ __forceinline__ TileMeta load_meta(const AttnArgs& a, int64_t kt0, int64_t vt0, int b0,
+                                              int nb, uint32_t lane) {
+  TileMeta m = {0ull, 0ull, 0u, 0u};
+  if ((int)(lane / T) < nb) {
+    const int64_t ti = (int64_t)b0 * T + lane;
+    m.kb = a.K.bitmaps[kt0 + ti];
+    m.ko = a.K.offsets[kt0 + ti];
+    m.vb = a.V.bitmaps[vt0 + ti];
+    m.vo = a.V.offsets[vt0 + ti];
+  }
+  return m;
+}
+
+// Packed-value runs of one block: [kstart, kstart + kn) and [vstart, vstart + vn).
+struct Runs {
+  uint32_t kstart, kn, vstart, vn;
+};
+
+template <int T>
+__device__ __forceinline__ Runs runs_of(const TileMeta& m, int nb) {
+  Runs r;
+  r.kstart = __builtin_amdgcn_readfirstlane(m.ko);
+  r.vstart = __builtin_amdgcn_readfirstlane(m.vo);
+  const int last = nb * T - 1;
+  r.kn = __builtin_amdgcn_readlane(m.ko + pad8((uint32_t)__popcll(m.kb)), last) - r.kstart;
+  r.vn = __builtin_amdgcn_readlane(m.vo + pad8((uint32_t)__popcll(m.vb)), last) - r.vstart;
+  return r;
+}
+
+// 512 fp16 values (one 16-byte load per lane) per staging chunk.
+template <int STAGE>
+__device__ __forceinline__ void stage_issue(u32x4 (&r)[STAGE], const uint16_t* kv, const uint16_t* vv,
+                                            const uint16_t* safe, const Runs& rn, uint32_t lane) {
+  // Every chunk is loaded unconditionally (no divergent writes to r); lanes past
+  // the end of their run read 16 harmless bytes at `safe` and never commit them.
+  const uint32_t nck = (rn.kn + 511) / 512;
+#pragma unroll
+  for (int c = 0; c < STAGE; ++c) {
+    const bool is_k = (uint32_t)c < nck;
+    const uint32_t off = 512u * (is_k ? (uint32_t)c : (uint32_t)c - nck) + 8u * lane;
+    const uint32_t n = is_k ? rn.kn : rn.vn;
+    const uint16_t* src = (is_k ? kv + rn.kstart : vv + rn.vstart) + off;
+    r[c] = *reinterpret_cast<const u32x4*>(off < n ? src : safe);
+  }
+}
+
+template <int STAGE>
+__device__ __forceinline__ void stage_commit(const u32x4 (&r)[STAGE], uint16_t* kst, uint16_t* vst,
+                                             const Runs& rn, uint32_t lane) {
+  const uint32_t nck = (rn.kn + 511) / 512;
+#pragma unroll
+  for (int c = 0; c < STAGE; ++c) {
+    const bool is_k = (uint32_t)c < nck;
+    const uint32_t off = 512u * (is_k ? (uint32_t)c : (uint32_t)c - nck) + 8u * lane;
+    const uint32_t n = is_k ? rn.kn : rn.vn;
+    uint16_t* dst = is_k ? kst : vst;
+    if (off < n) *reinterpret_cast<u32x4*>(dst + off) = r[c];
+  }
+  // 64 zero values after each run: a bit walk may read up to 63 values past its tile.
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  if (lane < 8) *reinterpret_cast<u32x4*>(kst + rn.kn + 8 * lane) = z;
+  else if (lane < 16) *reinterpret_cast<u32x4*>(vst + rn.vn + 8 * (lane - 8)) = z;
+}
+
+// Key half-tile walk: acc[g] += q[g][channel] * value over the set bits of `bits`.
+template <int G>
+__device__ __forceinline__ void key_walk(uint32_t bits, uint32_t vaddr, uint32_t qaddr, float (&acc)[G]) {
+  while (ballot(bits != 0u)) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t c = ffbl(bits);
+      bits &= bits - 1u;
+      const uint32_t qa = qaddr + c * (2u * G);
+      const float v = (float)lds_load<_Float16>(vaddr + 2u * u);
+      if constexpr (G == 1) {
+        acc[0] = fmaf((float)lds_load<_Float16>(qa), v, acc[0]);
+      } else if constexpr (G == 2) {
+        const half2_t qq = lds_load<half2_t>(qa);
+        acc[0] = fmaf((float)qq.x, v, acc[0]);
+        acc[1] = fmaf((float)qq.y, v, acc[1]);
+      } else {
+#pragma unroll
+        for (int g4 = 0; g4 < G; g4 += 4) {
+          const u32x2 qw = lds_load<u32x2>(qa + 2u * g4);
+          const half2_t q01 = as_h2(qw.x);
+          const half2_t q23 = as_h2(qw.y);
+          acc[g4 + 0] = fmaf((float)q01.x, v, acc[g4 + 0]);
+          acc[g4 + 1] = fmaf((float)q01.y, v, acc[g4 + 1]);
+          acc[g4 + 2] = fmaf((float)q23.x, v, acc[g4 + 2]);
+          acc[g4 + 3] = fmaf((float)q23.y, v, acc[g4 + 3]);
+        }
+      }
+    }
+    vaddr += 8u;
+  }
+}
+
+// Value half-tile walk: scatter the packed values into the expanded tile.
+__device__ __forceinline__ void value_walk(uint32_t bits, uint32_t vaddr, uint32_t daddr) {
+  while (ballot(bits != 0u)) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t c = ffbl(bits);
+      bits &= bits - 1u;
+      lds_store<uint16_t>(daddr + c * 4u, lds_load<uint16_t>(vaddr + 2u * u));
+    }
+    vaddr += 8u;
+  }
+}
+
+// LDS layout of the compressed body (byte offsets).
+struct SparseLds {
+  uint32_t qtab, ps, dense, kst, vst, total;
+};
+
+__host__ __device__ inline SparseLds sparse_lds_layout(int T, int G, int kmaxK, int kmaxV) {
+  const int NB = kWave / T;
+  SparseLds L;
+  uint32_t o = 0;
+  L.qtab = o;  o += ((T * kSlots * G * 2) + 15) & ~15;          // [t][slot][g] fp16
+  L.ps = o;    o += ((NB / 2) * G * 4 + 15) & ~15;              // [pair][g] half2
+  L.dense = o; o += (NB / 2) * T * kSlots * 4;                  // [pair][t][slot][2] fp16
+  L.kst = o;   o += ((NB * kmaxK + 64) * 2 + 15) & ~15;
+  L.vst = o;   o += ((NB * kmaxV + 64) * 2 + 15) & ~15;
+  L.total = o;
+  return L;
+}
+
+template <int T, int G, int STAGE>
+__device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, unsigned char* smem,
+                                            float (&m_run)[G], float (&l_run)[G],
+                                            float (&o)[G][T]) {
+  constexpr int d = kTile * T;
+  constexpr int NB = kWave / T;
+  const SparseLds L = sparse_lds_layout(T, G, a.kmaxK, a.kmaxV);
+  const uint32_t base = lds_addr(smem);
+  uint16_t* kst = reinterpret_cast<uint16_t*>(smem + L.kst);
+  uint16_t* vst = reinterpret_cast<uint16_t*>(smem + L.vst);
+  const uint32_t lane = lane_id();
+  const uint32_t j = lane / T, t = lane % T;
+
+  // q table with zero scratch slots: [t][slot][g].
+  {
+    const uint16_t* qsrc = a.q + (int64_t)bh * G * d;
+    uint16_t* qt = reinterpret_cast<uint16_t*>(smem + L.qtab);
+    for (int i = lane; i < T * kSlots * G; i += kWave) {
+      const int g = i % G, slot = (i / G) % kSlots, tt = i / (G * kSlots);
+      const int c = slot < 33 ? slot - 1 : slot - 2;
+      qt[i] = (slot == 0 || slot == 33) ? (uint16_t)0 : qsrc[g * d + kTile * tt + c];
+    }
   }
 
-  if (seg < a.n_sparse_segs) {
-    const int j0 = seg * a.sparse_seg_tokens;
-    const int j1 = min(j0 + a.sparse_seg_tokens, a.n_s);
-    const int64_t kt0 = (int64_t)bh * a.K.cap_tokens * T;
-    const int64_t vt0 = (int64_t)bh * a.V.cap_tokens * T;
-    const uint16_t* kv = a.K.values + (int64_t)bh * a.K.val_stride;
-    const uint16_t* vv = a.V.values + (int64_t)bh * a.V.val_stride;
-    for (int b0 = j0; b0 < j1; b0 += NB) {
-      const int nb = min(NB, j1 - b0);
-      const bool valid = (int)j < nb;
-      const int64_t ti = (int64_t)(b0 + (int)j) * T + t;
-      const uint64_t kb = valid ? a.K.bitmaps[kt0 + ti] : 0ull;
-      const uint32_t ko = valid ? a.K.offsets[kt0 + ti] : 0u;
-      const uint64_t vb = valid ? a.V.bitmaps[vt0 + ti] : 0ull;
-      const uint32_t vo = valid ? a.V.offsets[vt0 + ti] : 0u;
-      // The block's packed values are the contiguous runs [kstart, kend), [vstart, vend).
-      const uint32_t kstart = __builtin_amdgcn_readfirstlane(ko);
-      const uint32_t vstart = __builtin_amdgcn_readfirstlane(vo);
-      const uint32_t kend = __builtin_amdgcn_readlane(ko + pad8((uint32_t)__popcll(kb)), nb * T - 1);
-      const uint32_t vend = __builtin_amdgcn_readlane(vo + pad8((uint32_t)__popcll(vb)), nb * T - 1);
-      {
-        const uint4* src = reinterpret_cast<const uint4*>(kv + kstart);
-        uint4* dst = reinterpret_cast<uint4*>(kst);
-        const int n16 = (int)(kend - kstart) / 8;
-        for (int i = lane; i < n16; i += kWave) dst[i] = src[i];
-      }
-      {
-        const uint4* src = reinterpret_cast<const uint4*>(vv + vstart);
-        uint4* dst = reinterpret_cast<uint4*>(vst);
-        const int n16 = (int)(vend - vstart) / 8;
-        for (int i = lane; i < n16; i += kWave) dst[i] = src[i];
-      }
-      {
-        uint4* dz = reinterpret_cast<uint4*>(vdense);
-        for (int i = lane; i < NB * d / 8; i += kWave) dz[i] = make_uint4(0, 0, 0, 0);
-      }
-      __syncthreads();
+  const int j0 = seg * a.sparse_seg_tokens;
+  const int j1 = min(j0 + a.sparse_seg_tokens, a.n_s);
+  const int64_t kt0 = (int64_t)bh * a.K.cap_tokens * T;
+  const int64_t vt0 = (int64_t)bh * a.V.cap_tokens * T;
+  const uint16_t* kv = a.K.values + (int64_t)bh * a.K.val_stride;
+  const uint16_t* vv = a.V.values + (int64_t)bh * a.V.val_stride;
 
-      // Scores: lane (j, t) dots the kept entries of its key tile with q.
-      float acc[G];
-#pragma unroll
-      for (int g = 0; g < G; ++g) acc[g] = 0.f;
-      uint32_t pos = ko - kstart;
-#pragma unroll
-      for (int w = 0; w < 2; ++w) {
-        uint32_t bits = w ? (uint32_t)(kb >> 32) : (uint32_t)kb;
-        const uint32_t cb = kTile * t + 32 * w;
-        while (bits) {
-          const uint32_t c = cb + first_set_and_clear(bits);
-          const float kvf = half_bits_to_float(kst[pos++]);
-#pragma unroll
-          for (int g = 0; g < G; ++g) acc[g] = fmaf(half_bits_to_float(qs[g * d + c]), kvf, acc[g]);
-        }
-      }
-      softmax_update<T, G>(acc, valid, t, j, a.scale_log2, m_run, l_run, o, ps);
+  // Prologue: block 0 staged in LDS, metadata of block 1 in flight.
+  int nb = min(NB, j1 - j0);
+  TileMeta cur = load_meta<T>(a, kt0, vt0, j0, nb, lane);
+  Runs rcur = runs_of<T>(cur, nb);
+  u32x4 stg[STAGE];
+  stage_issue<STAGE>(stg, kv, vv, a.K.values, rcur, lane);
+  int nb_next = min(NB, j1 - (j0 + NB));
+  TileMeta nxt = {0ull, 0ull, 0u, 0u};
+  if (nb_next > 0) nxt = load_meta<T>(a, kt0, vt0, j0 + NB, nb_next, lane);
+  stage_commit<STAGE>(stg, kst, vst, rcur, lane);
 
-      // Expand the value tile into the dense block, channel-interleaved [j][c*T + t].
-      pos = vo - vstart;
-#pragma unroll
-      for (int w = 0; w < 2; ++w) {
-        uint32_t bits = w ? (uint32_t)(vb >> 32) : (uint32_t)vb;
-        const uint32_t cb = 32 * w;
-        while (bits) {
-          const uint32_t c = cb + first_set_and_clear(bits);
-          vdense[j * d + c * T + t] = vst[pos++];
-        }
-      }
-      __syncthreads();
+  // Per-lane constant addresses.
+  const uint32_t q_w0 = base + L.qtab + (uint32_t)((t * kSlots + 1) * G * 2);
+  const uint32_t q_w1 = q_w0 + 33u * G * 2;
+  const uint32_t d_w0 = base + L.dense + (uint32_t)((((j >> 1) * T + t) * kSlots + 1) * 4 + (j & 1) * 2);
+  const uint32_t d_w1 = d_w0 + 33u * 4;
+  const uint32_t pv_slot = lane < 32 ? 1 + lane : 2 + lane;  // PV: lane = channel of each tile
 
-      // p.V: lane = channel, channels lane + 64*tt.
-      for (int jj = 0; jj < nb; ++jj) {
-        float pv[G];
-#pragma unroll
-        for (int g = 0; g < G; ++g) pv[g] = ps[jj * G + g];
-#pragma unroll
-        for (int tt = 0; tt < T; ++tt) {
-          const float v = half_bits_to_float(vdense[jj * d + lane * T + tt]);
-#pragma unroll
-          for (int g = 0; g < G; ++g) o[g][tt] = fmaf(pv[g], v, o[g][tt]);
-        }
-      }
-      __syncthreads();
+  for (int b0 = j0; b0 < j1; b0 += NB) {
+    // Clear the expanded value tile.
+    {
+      uint4* dz = reinterpret_cast<uint4*>(smem + L.dense);
+      for (int i = lane; i < (NB / 2) * T * kSlots * 4 / 16; i += kWave) dz[i] = make_uint4(0, 0, 0, 0);
     }
-  } else {
-    // Dense segment: the local window (or a range of a dense cache).
-    const int dseg = seg - a.n_sparse_segs;
-    const int j0 = dseg * a.dense_seg_tokens;
-    const int j1 = min(j0 + a.dense_seg_tokens, a.n_dense);
-    const uint16_t* kd = a.kd + (int64_t)bh * a.n_dense * d;
-    const uint16_t* vd = a.vd + (int64_t)bh * a.n_dense * d;
-    for (int b0 = j0; b0 < j1; b0 += NB) {
-      const int nb = min(NB, j1 - b0);
-      const bool valid = (int)j < nb;
-      float acc[G];
+    __syncthreads();
+
+    // Software pipeline: fetch the next block's values and the metadata after it.
+    const bool has_next = nb_next > 0;
+    Runs rnext = {0u, 0u, 0u, 0u};
+    TileMeta nxt2 = {0ull, 0ull, 0u, 0u};
+    const int nb_next2 = min(NB, j1 - (b0 + 2 * NB));
+    if (has_next) rnext = runs_of<T>(nxt, nb_next);
+    stage_issue<STAGE>(stg, kv, vv, a.K.values, rnext, lane);
+    if (nb_next2 > 0) nxt2 = load_meta<T>(a, kt0, vt0, b0 + 2 * NB, nb_next2, lane);
+
+    // Scores.
+    float acc[G];
 #pragma unroll
-      for (int g = 0; g < G; ++g) acc[g] = 0.f;
-      if (valid) {
-        const uint4* kr = reinterpret_cast<const uint4*>(kd + (int64_t)(b0 + (int)j) * d + kTile * t);
-#pragma unroll
-        for (int i = 0; i < kTile / 8; ++i) {
-          const uint4 u = kr[i];
-          const half2_t k2[4] = {__builtin_bit_cast(half2_t, u.x), __builtin_bit_cast(half2_t, u.y),
-                                 __builtin_bit_cast(half2_t, u.z), __builtin_bit_cast(half2_t, u.w)};
-#pragma unroll
-          for (int g = 0; g < G; ++g) {
-            const uint4 qq = *reinterpret_cast<const uint4*>(qs + g * d + kTile * t + 8 * i);
-            acc[g] = __builtin_amdgcn_fdot2(k2[0], __builtin_bit_cast(half2_t, qq.x), acc[g], false);
-            acc[g] = __builtin_amdgcn_fdot2(k2[1], __builtin_bit_cast(half2_t, qq.y), acc[g], false);
-            acc[g] = __builtin_amdgcn_fdot2(k2[2], __builtin_bit_cast(half2_t, qq.z), acc[g], false);
-            acc[g] = __builtin_amdgcn_fdot2(k2[3], __builtin_bit_cast(half2_t, qq.w), acc[g], false);
-          }
-        }
-      }
-      softmax_update<T, G>(acc, valid, t, j, a.scale_log2, m_run, l_run, o, ps);
-      __syncthreads();
-      for (int jj = 0; jj < nb; ++jj) {
-        float pv[G];
-#pragma unroll
-        for (int g = 0; g < G; ++g) pv[g] = ps[jj * G + g];
-        const uint16_t* vr = vd + (int64_t)(b0 + jj) * d;
-#pragma unroll
-        for (int tt = 0; tt < T; ++tt) {
-          const float v = half_bits_to_float(vr[lane + kTile * tt]);
-#pragma unroll
-          for (int g = 0; g < G; ++g) o[g][tt] = fmaf(pv[g], v, o[g][tt]);
-        }
-      }
-      __syncthreads();
+    for (int g = 0; g < G; ++g) acc[g] = 0.f;
+    {
+      const uint32_t w0 = (uint32_t)cur.kb, w1 = (uint32_t)(cur.kb >> 32);
+      const uint32_t va = base + L.kst + ((int)j < nb ? 2u * (cur.ko - rcur.kstart) : 0u);
+      key_walk<G>(w0, va, q_w0, acc);
+      key_walk<G>(w1, va + 2u * (uint32_t)__popc(w0), q_w1, acc);
     }
+    const bool valid = (int)j < nb;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float sc = valid ? tile_sum<T>(acc[g]) * a.scale_log2 : -INFINITY;
+      const float mnew = fmaxf(m_run[g], wave_max_u(sc));
+      const float alpha = __builtin_amdgcn_exp2f(m_run[g] - mnew);
+      const _Float16 ph = valid ? (_Float16)__builtin_amdgcn_exp2f(sc - mnew) : (_Float16)0.f;
+      l_run[g] = l_run[g] * alpha + wave_sum_u(t == 0 ? (float)ph : 0.f);
+      m_run[g] = mnew;
+#pragma unroll
+      for (int tt = 0; tt < T; ++tt) o[g][tt] *= alpha;
+      if (t == 0) lds_store<_Float16>(base + L.ps + ((j >> 1) * G + g) * 4 + (j & 1) * 2, ph);
+    }
+
+    // Expand the value tiles.
+    {
+      const uint32_t w0 = (uint32_t)cur.vb, w1 = (uint32_t)(cur.vb >> 32);
+      const uint32_t va = base + L.vst + ((int)j < nb ? 2u * (cur.vo - rcur.vstart) : 0u);
+      value_walk(w0, va, d_w0);
+      value_walk(w1, va + 2u * (uint32_t)__popc(w0), d_w1);
+    }
+    __syncthreads();
+
+    // p.V over token pairs: lane = channel `lane` of every tile.
+    for (int pr = 0; pr < (nb + 1) / 2; ++pr) {
+      half2_t p2[G];
+      if constexpr (G == 1) {
+        p2[0] = lds_load<half2_t>(base + L.ps + pr * 4);
+      } else if constexpr (G == 2) {
+        const u32x2 w = lds_load<u32x2>(base + L.ps + pr * 8);
+        p2[0] = as_h2(w.x);
+        p2[1] = as_h2(w.y);
+      } else {
+#pragma unroll
+        for (int g4 = 0; g4 < G; g4 += 4) {
+          const u32x4 w = lds_load<u32x4>(base + L.ps + (pr * G + g4) * 4);
+          p2[g4 + 0] = as_h2(w.x);
+          p2[g4 + 1] = as_h2(w.y);
+          p2[g4 + 2] = as_h2(w.z);
+          p2[g4 + 3] = as_h2(w.w);
+        }
+      }
+#pragma unroll
+      for (int tt = 0; tt < T; ++tt) {
+        const half2_t v2 = lds_load<half2_t>(base + L.dense + ((pr * T + tt) * kSlots + pv_slot) * 4);
+#pragma unroll
+        for (int g = 0; g < G; ++g) o[g][tt] = __builtin_amdgcn_fdot2(v2, p2[g], o[g][tt], false);
+      }
+    }
+    __syncthreads();
+
+    if (has_next) {
+      stage_commit<STAGE>(stg, kst, vst, rnext, lane);
+      cur = nxt;
+      rcur = rnext;
+      nxt = nxt2;
+    }
+    nb = nb_next;
+    nb_next = nb_next2;
   }
+}
 
+template <int T, int G>
+__device__ __forceinline__ void write_partial(const AttnArgs& a, int seg, int bh, const float (&m_run)[G],
+                                              const float (&l_run)[G], const float (&o)[G][T]) {
+  constexpr int d = kTile * T;
+  const uint32_t lane = lane_id();
   const int64_t row0 = (int64_t)seg * a.BHq + (int64_t)bh * G;
 #pragma unroll
   for (int g = 0; g < G; ++g) {
@@ -235,6 +474,42 @@ __global__ __launch_bounds__(64) void k_attn_partial(AttnArgs a) {
 #pragma unroll
     for (int tt = 0; tt < T; ++tt) a.ws_o[(row0 + g) * d + lane + kTile * tt] = o[g][tt];
   }
+}
+
+template <int T, int G>
+__device__ __forceinline__ void init_state(float (&m_run)[G], float (&l_run)[G], float (&o)[G][T]) {
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m_run[g] = -INFINITY;
+    l_run[g] = 0.f;
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) o[g][tt] = 0.f;
+  }
+}
+
+// Sparse call: grid (n_sparse_segs + n_dense_segs, BHkv); compressed segments first.
+template <int T, int G, int STAGE>
+__global__ __launch_bounds__(64) void k_sparse_attn(AttnArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int seg = blockIdx.x, bh = blockIdx.y;
+  float m_run[G], l_run[G], o[G][T];
+  init_state<T, G>(m_run, l_run, o);
+  if (seg < a.n_sparse_segs)
+    sparse_body<T, G, STAGE>(a, seg, bh, smem, m_run, l_run, o);
+  else
+    dense_body<T, G>(a, seg - a.n_sparse_segs, bh, smem, m_run, l_run, o);
+  write_partial<T, G>(a, seg, bh, m_run, l_run, o);
+}
+
+// Dense baseline: grid (n_dense_segs, BHkv).
+template <int T, int G>
+__global__ __launch_bounds__(64) void k_dense_attn(AttnArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int seg = blockIdx.x, bh = blockIdx.y;
+  float m_run[G], l_run[G], o[G][T];
+  init_state<T, G>(m_run, l_run, o);
+  dense_body<T, G>(a, seg, bh, smem, m_run, l_run, o);
+  write_partial<T, G>(a, seg, bh, m_run, l_run, o);
 }
 
 // grid (BHq), one wave: log-sum-exp merge of the segments, fp16 output (RNE).
@@ -264,19 +539,54 @@ __global__ __launch_bounds__(64) void k_merge(const float2* __restrict__ ws_ml,
     out[(int64_t)r * d + lane + kTile * tt] = __builtin_bit_cast(uint16_t, (_Float16)(acc[tt] * inv));
 }
 
-static size_t partial_lds_bytes(int T, int G, int kmaxK, int kmaxV) {
+// ------------------------------------------------------------------------------------------
+// Host-side launch.
+// ------------------------------------------------------------------------------------------
+static size_t dense_lds_bytes(int T, int G) {
   const int d = kTile * T, NB = kWave / T;
-  size_t b = (size_t)G * d * 2 + (size_t)NB * G * 4 + (size_t)NB * d * 2;
-  b += (size_t)((NB * kmaxK + 7) & ~7) * 2 + (size_t)NB * kmaxV * 2;
-  return (b + 15) & ~size_t(15);
+  return (size_t)G * d * 2 + (size_t)NB * G * 4;
+}
+
+static int token_max_elems_dev(int d, int k) {
+  const int T = d / kTile;
+  const int nonempty = k < T ? k : T;
+  const int m = (k + (kPad - 1) * nonempty) / kPad * kPad;
+  return m < d ? m : d;
+}
+
+template <int T, int G, int STAGE>
+static hipError_t sparse_launch(const AttnShape& sh, const AttnArgs& a, hipStream_t s) {
+  const SparseLds L = sparse_lds_layout(T, G, a.kmaxK, a.kmaxV);
+  size_t lds = L.total;
+  if (sh.n_dense_segs > 0 && dense_lds_bytes(T, G) > lds) lds = dense_lds_bytes(T, G);
+  hipLaunchKernelGGL((k_sparse_attn<T, G, STAGE>), dim3(sh.n_sparse_segs + sh.n_dense_segs, sh.BHkv),
+                     dim3(kWave), lds, s, a);
+  return hipGetLastError();
+}
+
+template <int T, int G>
+static hipError_t sparse_stage(const AttnShape& sh, const AttnArgs& a, hipStream_t s) {
+  const int NB = kWave / T;
+  const int chunks = (NB * a.kmaxK + 511) / 512 + (NB * a.kmaxV + 511) / 512;
+  if (chunks <= 4) return sparse_launch<T, G, 4>(sh, a, s);
+  if (chunks <= 8) return sparse_launch<T, G, 8>(sh, a, s);
+  return sparse_launch<T, G, 16>(sh, a, s);
 }
 
 template <int T, int G>
 static hipError_t attention_TG(const AttnShape& sh, const AttnArgs& a, uint16_t* out, hipStream_t s) {
   const int n_seg = sh.n_sparse_segs + sh.n_dense_segs;
-  const size_t lds = partial_lds_bytes(T, G, a.kmaxK, a.kmaxV);
-  hipLaunchKernelGGL((k_attn_partial<T, G>), dim3(n_seg, sh.BHkv), dim3(kWave), lds, s, a);
-  hipError_t e = hipGetLastError();
+  hipError_t e;
+  if (sh.n_sparse_segs > 0) {
+    e = sparse_stage<T, G>(sh, a, s);
+  } else if (sh.n_s == 0 && sh.n_dense_segs > 0 && a.K.bitmaps != nullptr) {
+    // Sparse call with an empty compressed cache: only the window segment.
+    e = sparse_launch<T, G, 4>(sh, a, s);
+  } else {
+    hipLaunchKernelGGL((k_dense_attn<T, G>), dim3(sh.n_dense_segs, sh.BHkv), dim3(kWave),
+                       dense_lds_bytes(T, G), s, a);
+    e = hipGetLastError();
+  }
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_merge<T>, dim3(a.BHq), dim3(kWave), 0, s, a.ws_ml, a.ws_o, n_seg, a.BHq, out);
   return hipGetLastError();
@@ -291,13 +601,6 @@ static hipError_t attention_T(const AttnShape& sh, const AttnArgs& a, uint16_t* 
     case 8: return attention_TG<T, 8>(sh, a, out, s);
     default: return hipErrorInvalidValue;
   }
-}
-
-static int token_max_elems_dev(int d, int k) {
-  const int T = d / kTile;
-  const int nonempty = k < T ? k : T;
-  const int m = (k + (kPad - 1) * nonempty) / kPad * kPad;
-  return m < d ? m : d;
 }
 
 hipError_t launch_attention(const AttnShape& sh, const uint16_t* q, const SparseSide& K,
@@ -320,8 +623,8 @@ hipError_t launch_attention(const AttnShape& sh, const uint16_t* q, const Sparse
   a.ws_ml = reinterpret_cast<float2*>(ws_ml);
   a.ws_o = ws_o;
   a.BHq = sh.BHkv * sh.G;
-  a.kmaxK = sh.n_sparse_segs > 0 ? token_max_elems_dev(d, K.n_keep) : 0;
-  a.kmaxV = sh.n_sparse_segs > 0 ? token_max_elems_dev(d, V.n_keep) : 0;
+  a.kmaxK = K.bitmaps != nullptr ? token_max_elems_dev(d, K.n_keep) : 0;
+  a.kmaxV = V.bitmaps != nullptr ? token_max_elems_dev(d, V.n_keep) : 0;
   switch (sh.T) {
     case 1: return attention_T<1>(sh, a, out, s);
     case 2: return attention_T<2>(sh, a, out, s);
