@@ -44,7 +44,24 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-streams", type=int, default=48)
     ap.add_argument("--cpu-threads", type=int, default=0, help="0: min(16, cpu count)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device copy three times (scales HBM byte counters)")
     return ap.parse_args()
+
+
+def copy_calibration() -> None:
+    """A plain device-to-device copy of known size: what FETCH_SIZE / WRITE_SIZE read
+    for it gives the factor that turns those counters into bytes."""
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_per_copy": n, "copies": 3}), flush=True)
 
 
 def attn_alg_bytes(w, k_len_total: int, v_len_total: int, n_s: int) -> int:
@@ -56,6 +73,20 @@ def attn_alg_bytes(w, k_len_total: int, v_len_total: int, n_s: int) -> int:
     window = 2 * 2 * w.B * w.Hkv * w.n_tail * w.d
     qo = 2 * 2 * w.B * w.Hq * w.d
     return meta + vals + window + qo
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None
+    when there is none or the kernel source changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}.traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    if hashlib.sha256(src).hexdigest()[:16] != rec["source_sha256_prefix"]:
+        return None
+    return rec["fetch_bytes"] + rec["write_bytes"]
 
 
 def cpu_baseline(w, K, V, KL, VL, q, sample: int, threads: int) -> dict:
@@ -97,9 +128,12 @@ def cpu_baseline(w, K, V, KL, VL, q, sample: int, threads: int) -> dict:
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build measures one GPU only; the (batch, kv-head) "
-                                   "streams shard without communication (see the design notes)",
+        print(json.dumps({"error": "one GPU only: every (batch, kv-head) stream is independent, "
+                                   "so N GPUs would each run this benchmark on their own share",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import numpy as np
@@ -232,7 +266,8 @@ def main():
                       "kv_tokens_per_s": w.B * w.Hkv * (n_s_end + w.n_tail) / attn_s,
                       "alg_bytes": alg_bytes, "gb_s": attn_gbs},
         "roofline": {"bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": attn_gbs / HBM_PEAK_GBS, "traffic": None},
+                     "frac": attn_gbs / HBM_PEAK_GBS,
+                     "traffic": measured_traffic("k_sparse_attn", w.name)},
         "dense_baseline": {"us": t_dense * 1e6, "tokens_per_s": w.B / t_dense,
                            "gb_s": dense_bytes / t_dense / 1e9},
         "speedup_vs_dense": t_dense / attn_s,

@@ -12,8 +12,7 @@
  * streams.  Floating point is done in IEEE double.  The fp16 inputs are decoded
  * from their bit patterns by the binary16 definition (no compiler half type).
  *
- * Readings of the paper taken where it is silent (listed with reasons in the
- * design notes of the repository):
+ * Readings of the paper taken where it is silent:
  *   R1 pruning unit = one token of one head (d channels)           (Sec. 2)
  *   R2 kept count   = d - floor(s*d + 1/2), clamped to [0, d]
  *   R3 ranking      = larger |x| first; equal |x| -> lower channel first
