@@ -14,10 +14,11 @@
 //     loads while the current block is computed, then written to LDS;
 //   * lane (j, t) owns tile t of token j and walks the set bits of each
 //     32-bit half of its bitmap with v_ffbl, reading its packed values in
-//     order. A lane with no bits left gets the index -1, which points at a
-//     zero slot of the q table (its product is 0) and at a scratch slot of the
-//     expanded value tile, so the walk has no per-element branch; it runs in
-//     groups of 4 while any lane has bits left;
+//     order, 8 at a time with one 16-byte LDS load. A lane with no bits left
+//     gets the index -1, which points at a zero slot of the q table (its
+//     product is 0) and at a scratch slot of the expanded value tile, so the
+//     walk has no per-element branch; it runs in groups of 8 while any lane
+//     has bits left;
 //   * p.V runs with one lane per channel over the expanded value tile, two
 //     tokens at a time with v_dot2 (fp16 probabilities, fp32 accumulation).
 #include "mf_device.h"
@@ -36,6 +37,9 @@ __device__ __forceinline__ half2_t as_h2(uint32_t w) { return __builtin_bit_cast
 // Per tile and per 32-channel half, one scratch slot precedes the channels:
 // [s][ch 0..31][s][ch 32..63] -- slot of channel c is 1 + c + (c >= 32).
 constexpr int kSlots = 66;
+
+// Zero fp16 values staged after each packed run (a multiple of 8).
+constexpr uint32_t kMargin = 80;
 
 struct AttnArgs {
   const uint16_t* q;
@@ -254,59 +258,123 @@ __device__ __forceinline__ void stage_commit(const u32x4 (&r)[STAGE], uint16_t* 
     uint16_t* dst = is_k ? kst : vst;
     if (off < n) *reinterpret_cast<u32x4*>(dst + off) = r[c];
   }
-  // 64 zero values after each run: a bit walk may read up to 63 values past its tile.
+  // kMargin zero values after each run: the walks read whole groups of 8 up to
+  // 72 values past the start of a tile (at most 4 groups of the lower half and
+  // 5 of the upper half, which starts at most 32 values in), and the products of
+  // those values with the zero q slot must stay 0.
   const u32x4 z = {0u, 0u, 0u, 0u};
-  if (lane < 8) *reinterpret_cast<u32x4*>(kst + rn.kn + 8 * lane) = z;
-  else if (lane < 16) *reinterpret_cast<u32x4*>(vst + rn.vn + 8 * (lane - 8)) = z;
+  constexpr uint32_t kz = kMargin / 8;
+  if (lane < kz) *reinterpret_cast<u32x4*>(kst + rn.kn + 8 * lane) = z;
+  else if (lane < 2 * kz) *reinterpret_cast<u32x4*>(vst + rn.vn + 8 * (lane - kz)) = z;
 }
 
-// Key half-tile walk: acc[g] += q[g][channel] * value over the set bits of `bits`.
-template <int G>
-__device__ __forceinline__ void key_walk(uint32_t bits, uint32_t vaddr, uint32_t qaddr, float (&acc)[G]) {
-  while (ballot(bits != 0u)) {
+// The packed values of a tile start 16-byte aligned in LDS (tiles are padded to
+// 8 values), so the walks read them 8 at a time with one 16-byte LDS load and
+// pair slot u of the group with the next set bit of the 32-bit half word x.
+// Channel -1 (no bit left) addresses the zero slot of the q table and the
+// scratch slot of the expanded tile, so the walk has no per-element branch.
+//
+// The values of the upper half start at rank s = popcount(low half), which is
+// aligned only when s % 8 == 0. Its first group is read from the aligned
+// position below and its first s % 8 slots (values of the lower half, already
+// consumed) are phantom: they take channel -1 and consume no bit. Every later
+// group is aligned again.
+__device__ __forceinline__ _Float16 group_value(const u32x4& w, int u) {
+  const half2_t h = as_h2(w[u >> 1]);
+  return (u & 1) ? h.y : h.x;
+}
+
+template <bool PEEL>
+__device__ __forceinline__ uint32_t next_channel(uint32_t& x, int u, uint32_t m) {
+  if constexpr (PEEL) {
+    const uint32_t f = ffbl(x);  // evaluated unconditionally: no branch around the asm
+    const bool real = (uint32_t)u >= m;
+    x &= x - (real ? 1u : 0u);
+    return real ? f : 0xffffffffu;
+  } else {
+    const uint32_t c = ffbl(x);
+    x &= x - 1u;
+    return c;
+  }
+}
+
+// acc[g] += q[g][channel] * value over one group of 8 packed key values.
+template <int G, bool PEEL>
+__device__ __forceinline__ void key_group(uint32_t& x, uint32_t va, uint32_t qaddr, uint32_t m,
+                                          float (&acc)[G]) {
+  const u32x4 w = lds_load<u32x4>(va);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const uint32_t c = ffbl(bits);
-      bits &= bits - 1u;
-      const uint32_t qa = qaddr + c * (2u * G);
-      const float v = (float)lds_load<_Float16>(vaddr + 2u * u);
-      if constexpr (G == 1) {
-        acc[0] = fmaf((float)lds_load<_Float16>(qa), v, acc[0]);
-      } else if constexpr (G == 2) {
-        const half2_t qq = lds_load<half2_t>(qa);
-        acc[0] = fmaf((float)qq.x, v, acc[0]);
-        acc[1] = fmaf((float)qq.y, v, acc[1]);
-      } else {
+  for (int u = 0; u < 8; ++u) {
+    const uint32_t c = next_channel<PEEL>(x, u, m);
+    const uint32_t qa = qaddr + c * (2u * G);
+    const float v = (float)group_value(w, u);
+    if constexpr (G == 1) {
+      acc[0] = fmaf((float)lds_load<_Float16>(qa), v, acc[0]);
+    } else if constexpr (G == 2) {
+      const half2_t qq = lds_load<half2_t>(qa);
+      acc[0] = fmaf((float)qq.x, v, acc[0]);
+      acc[1] = fmaf((float)qq.y, v, acc[1]);
+    } else {
 #pragma unroll
-        for (int g4 = 0; g4 < G; g4 += 4) {
-          const u32x2 qw = lds_load<u32x2>(qa + 2u * g4);
-          const half2_t q01 = as_h2(qw.x);
-          const half2_t q23 = as_h2(qw.y);
-          acc[g4 + 0] = fmaf((float)q01.x, v, acc[g4 + 0]);
-          acc[g4 + 1] = fmaf((float)q01.y, v, acc[g4 + 1]);
-          acc[g4 + 2] = fmaf((float)q23.x, v, acc[g4 + 2]);
-          acc[g4 + 3] = fmaf((float)q23.y, v, acc[g4 + 3]);
-        }
+      for (int g4 = 0; g4 < G; g4 += 4) {
+        const u32x2 qw = lds_load<u32x2>(qa + 2u * g4);
+        const half2_t q01 = as_h2(qw.x);
+        const half2_t q23 = as_h2(qw.y);
+        acc[g4 + 0] = fmaf((float)q01.x, v, acc[g4 + 0]);
+        acc[g4 + 1] = fmaf((float)q01.y, v, acc[g4 + 1]);
+        acc[g4 + 2] = fmaf((float)q23.x, v, acc[g4 + 2]);
+        acc[g4 + 3] = fmaf((float)q23.y, v, acc[g4 + 3]);
       }
     }
-    vaddr += 8u;
   }
 }
 
-// Value half-tile walk: scatter the packed values into the expanded tile.
-__device__ __forceinline__ void value_walk(uint32_t bits, uint32_t vaddr, uint32_t daddr) {
-  while (ballot(bits != 0u)) {
+// Scatter one group of 8 packed values into the expanded value tile.
+template <bool PEEL>
+__device__ __forceinline__ void value_group(uint32_t& x, uint32_t va, uint32_t daddr, uint32_t m) {
+  const u32x4 w = lds_load<u32x4>(va);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const uint32_t c = ffbl(bits);
-      bits &= bits - 1u;
-      lds_store<uint16_t>(daddr + c * 4u, lds_load<uint16_t>(vaddr + 2u * u));
-    }
-    vaddr += 8u;
+  for (int u = 0; u < 8; ++u) {
+    const uint32_t c = next_channel<PEEL>(x, u, m);
+    lds_store<_Float16>(daddr + c * 4u, group_value(w, u));
   }
 }
 
-// LDS layout of the compressed body (byte offsets).
+// Scores of one tile: q . k over its 64-bit bitmap `bm`, values at LDS byte address `va`.
+template <int G>
+__device__ __forceinline__ void key_walk(uint64_t bm, uint32_t va, uint32_t q_w0, uint32_t q_w1,
+                                         float (&acc)[G]) {
+  uint32_t x = (uint32_t)bm;
+  const uint32_t s = (uint32_t)__popc(x);
+  for (uint32_t a = va; ballot(x != 0u); a += 16u) key_group<G, false>(x, a, q_w0, 0u, acc);
+  x = (uint32_t)(bm >> 32);
+  const uint32_t m = s & 7u;
+  uint32_t a = va + 2u * (s - m);
+  if (ballot(x != 0u)) {
+    key_group<G, true>(x, a, q_w1, m, acc);
+    for (a += 16u; ballot(x != 0u); a += 16u) key_group<G, false>(x, a, q_w1, 0u, acc);
+  }
+}
+
+// Expansion of one value tile into the dense tile.
+__device__ __forceinline__ void value_walk(uint64_t bm, uint32_t va, uint32_t d_w0, uint32_t d_w1) {
+  uint32_t x = (uint32_t)bm;
+  const uint32_t s = (uint32_t)__popc(x);
+  for (uint32_t a = va; ballot(x != 0u); a += 16u) value_group<false>(x, a, d_w0, 0u);
+  x = (uint32_t)(bm >> 32);
+  const uint32_t m = s & 7u;
+  uint32_t a = va + 2u * (s - m);
+  if (ballot(x != 0u)) {
+    value_group<true>(x, a, d_w1, m);
+    for (a += 16u; ballot(x != 0u); a += 16u) value_group<false>(x, a, d_w1, 0u);
+  }
+}
+
+// LDS layout of the compressed body (byte offsets). The expanded value tile
+// shares its bytes with the staged keys: it is cleared after the key walk of a
+// block and read by p.V before the next block's keys are committed. A
+// workgroup is one wave, whose LDS operations execute in program order, so the
+// phases need no barrier.
 struct SparseLds {
   uint32_t qtab, ps, dense, kst, vst, total;
 };
@@ -317,9 +385,12 @@ __host__ __device__ inline SparseLds sparse_lds_layout(int T, int G, int kmaxK, 
   uint32_t o = 0;
   L.qtab = o;  o += ((T * kSlots * G * 2) + 15) & ~15;          // [t][slot][g] fp16
   L.ps = o;    o += ((NB / 2) * G * 4 + 15) & ~15;              // [pair][g] half2
-  L.dense = o; o += (NB / 2) * T * kSlots * 4;                  // [pair][t][slot][2] fp16
-  L.kst = o;   o += ((NB * kmaxK + 64) * 2 + 15) & ~15;
-  L.vst = o;   o += ((NB * kmaxV + 64) * 2 + 15) & ~15;
+  L.vst = o;   o += ((NB * kmaxV + kMargin) * 2 + 15) & ~15;
+  const uint32_t kst_bytes = ((NB * kmaxK + kMargin) * 2 + 15) & ~15;
+  const uint32_t dense_bytes = (NB / 2) * T * kSlots * 4;      // [pair][t][slot][2] fp16
+  L.kst = o;
+  L.dense = o;
+  o += kst_bytes > dense_bytes ? kst_bytes : dense_bytes;
   L.total = o;
   return L;
 }
@@ -374,13 +445,6 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   const uint32_t pv_slot = lane < 32 ? 1 + lane : 2 + lane;  // PV: lane = channel of each tile
 
   for (int b0 = j0; b0 < j1; b0 += NB) {
-    // Clear the expanded value tile.
-    {
-      uint4* dz = reinterpret_cast<uint4*>(smem + L.dense);
-      for (int i = lane; i < (NB / 2) * T * kSlots * 4 / 16; i += kWave) dz[i] = make_uint4(0, 0, 0, 0);
-    }
-    __syncthreads();
-
     // Software pipeline: fetch the next block's values and the metadata after it.
     const bool has_next = nb_next > 0;
     Runs rnext = {0u, 0u, 0u, 0u};
@@ -395,10 +459,8 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g] = 0.f;
     {
-      const uint32_t w0 = (uint32_t)cur.kb, w1 = (uint32_t)(cur.kb >> 32);
       const uint32_t va = base + L.kst + ((int)j < nb ? 2u * (cur.ko - rcur.kstart) : 0u);
-      key_walk<G>(w0, va, q_w0, acc);
-      key_walk<G>(w1, va + 2u * (uint32_t)__popc(w0), q_w1, acc);
+      key_walk<G>(cur.kb, va, q_w0, q_w1, acc);
     }
     const bool valid = (int)j < nb;
 #pragma unroll
@@ -414,42 +476,59 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
       if (t == 0) lds_store<_Float16>(base + L.ps + ((j >> 1) * G + g) * 4 + (j & 1) * 2, ph);
     }
 
+    // Clear the expanded value tile (it overwrites the staged keys, read above).
+    {
+      constexpr int n16 = (NB / 2) * T * kSlots * 4 / 16;
+      const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int i = 0; i < (n16 + kWave - 1) / kWave; ++i)
+        if (i * kWave + (int)lane < n16) lds_store<u32x4>(base + L.dense + 16u * (i * kWave + lane), z);
+    }
+
     // Expand the value tiles.
     {
-      const uint32_t w0 = (uint32_t)cur.vb, w1 = (uint32_t)(cur.vb >> 32);
       const uint32_t va = base + L.vst + ((int)j < nb ? 2u * (cur.vo - rcur.vstart) : 0u);
-      value_walk(w0, va, d_w0);
-      value_walk(w1, va + 2u * (uint32_t)__popc(w0), d_w1);
+      value_walk(cur.vb, va, d_w0, d_w1);
     }
-    __syncthreads();
 
-    // p.V over token pairs: lane = channel `lane` of every tile.
-    for (int pr = 0; pr < (nb + 1) / 2; ++pr) {
-      half2_t p2[G];
-      if constexpr (G == 1) {
-        p2[0] = lds_load<half2_t>(base + L.ps + pr * 4);
-      } else if constexpr (G == 2) {
-        const u32x2 w = lds_load<u32x2>(base + L.ps + pr * 8);
-        p2[0] = as_h2(w.x);
-        p2[1] = as_h2(w.y);
-      } else {
+    // p.V over every token pair of the block (tokens past its end have p = 0
+    // and zero values), unrolled so the LDS loads of a batch are in flight
+    // together: lane = channel `lane` of every tile.
+    constexpr int NP = NB / 2;
+    constexpr int PB = G >= 8 ? 4 : 8;
+#pragma unroll 1
+    for (int pb = 0; pb < NP; pb += PB) {
+      half2_t p2[PB][G], v2[PB][T];
 #pragma unroll
-        for (int g4 = 0; g4 < G; g4 += 4) {
-          const u32x4 w = lds_load<u32x4>(base + L.ps + (pr * G + g4) * 4);
-          p2[g4 + 0] = as_h2(w.x);
-          p2[g4 + 1] = as_h2(w.y);
-          p2[g4 + 2] = as_h2(w.z);
-          p2[g4 + 3] = as_h2(w.w);
+      for (int i = 0; i < PB; ++i) {
+        const int pr = pb + i;
+        if constexpr (G == 1) {
+          p2[i][0] = lds_load<half2_t>(base + L.ps + pr * 4);
+        } else if constexpr (G == 2) {
+          const u32x2 w = lds_load<u32x2>(base + L.ps + pr * 8);
+          p2[i][0] = as_h2(w.x);
+          p2[i][1] = as_h2(w.y);
+        } else {
+#pragma unroll
+          for (int g4 = 0; g4 < G; g4 += 4) {
+            const u32x4 w = lds_load<u32x4>(base + L.ps + (pr * G + g4) * 4);
+            p2[i][g4 + 0] = as_h2(w.x);
+            p2[i][g4 + 1] = as_h2(w.y);
+            p2[i][g4 + 2] = as_h2(w.z);
+            p2[i][g4 + 3] = as_h2(w.w);
+          }
         }
+#pragma unroll
+        for (int tt = 0; tt < T; ++tt)
+          v2[i][tt] = lds_load<half2_t>(base + L.dense + ((pr * T + tt) * kSlots + pv_slot) * 4);
       }
 #pragma unroll
-      for (int tt = 0; tt < T; ++tt) {
-        const half2_t v2 = lds_load<half2_t>(base + L.dense + ((pr * T + tt) * kSlots + pv_slot) * 4);
+      for (int i = 0; i < PB; ++i)
 #pragma unroll
-        for (int g = 0; g < G; ++g) o[g][tt] = __builtin_amdgcn_fdot2(v2, p2[g], o[g][tt], false);
-      }
+        for (int tt = 0; tt < T; ++tt)
+#pragma unroll
+          for (int g = 0; g < G; ++g) o[g][tt] = __builtin_amdgcn_fdot2(v2[i][tt], p2[i][g], o[g][tt], false);
     }
-    __syncthreads();
 
     if (has_next) {
       stage_commit<STAGE>(stg, kst, vst, rnext, lane);
