@@ -129,8 +129,8 @@ int mustafar_ccache_init(mustafar_ccache_t* c, void* bitmaps, void* offsets, voi
 
 size_t mustafar_compress_workspace_bytes(int B, int H, int n_new) {
   if (B < 1 || H < 1 || n_new < 1) return 0;
-  const int64_t n_chunks = (n_new + mf::kCompressChunk - 1) / mf::kCompressChunk;
-  return (size_t)((int64_t)B * H * (n_chunks + 1) * sizeof(uint32_t));
+  const int64_t n_chunks = (n_new + mf::kMinCompressChunk - 1) / mf::kMinCompressChunk;
+  return (size_t)((int64_t)B * H * n_chunks * sizeof(uint64_t) + 16);
 }
 
 int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void* ws,
@@ -140,7 +140,7 @@ int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void
   if (n_new < 1 || !aligned(x, 16)) return MUSTAFAR_EINVAL;
   if ((int64_t)c->n_tokens + n_new > c->cap_tokens) return MUSTAFAR_ECAPACITY;
   const size_t need = mustafar_compress_workspace_bytes(c->B, c->H, n_new);
-  if (!aligned(ws, 4) || ws_bytes < need) return MUSTAFAR_EWORKSPACE;
+  if (!aligned(ws, 8) || ws_bytes < need) return MUSTAFAR_EWORKSPACE;
   const hipError_t e = mf::launch_compress(view_of(c), (const uint16_t*)x, n_new, c->n_tokens,
                                            (uint32_t*)ws, (hipStream_t)stream);
   st = status_of(e);

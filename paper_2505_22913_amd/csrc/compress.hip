@@ -1,23 +1,29 @@
 // Per-token magnitude pruning and bitmap compression on gfx950.
 //
-// One wavefront handles one token: lane i holds channel 64t+i of every tile t,
-// so the keep-mask of a tile is exactly one 64-bit ballot (Sec. 3 tiles are
-// 1x64 and the wavefront is 64 lanes wide). Selection of the n_keep largest
-// magnitudes (Sec. 2, per-token magnitude pruning) is a most-significant-bit
-// first radix select on the 15-bit fp16 magnitude with ballot+popcount counts,
-// then ties at the threshold go to the lowest channels via mbcnt ranks. The
-// packed position of a kept value inside its tile is mbcnt(bitmap) -- the
-// number of kept lanes below it -- so the scatter is one masked store per tile.
+// One wavefront handles one token at a time: lane i holds channel 64t+i of
+// every tile t, so the keep-mask of a tile is exactly one 64-bit ballot (Sec. 3
+// tiles are 1x64 and the wavefront is 64 lanes wide). Selection of the n_keep
+// largest magnitudes (Sec. 2, per-token magnitude pruning) is a
+// most-significant-bit first radix select on the 15-bit fp16 magnitude with
+// ballot+popcount counts, then ties at the threshold go to the lowest channels
+// via mbcnt ranks. The packed position of a kept value inside its tile is
+// mbcnt(bitmap) -- the number of kept lanes below it -- so a tile is packed by
+// one masked 2-byte store.
 //
 // A stream's per-tile offsets are an exclusive prefix sum of the padded tile
-// counts (Sec. 4.3 pads to 8). Bulk compression therefore runs in two launches:
-// k_select writes the bitmaps and per-chunk padded totals, k_pack scans the
-// totals, writes offsets and scatters the values (re-reading the dense tokens).
-// k_append handles the one-token-per-stream case of a decode step in one launch.
+// counts (Sec. 4.3 pads to 8), so bulk compression is a single-pass scan with
+// decoupled look-back: each workgroup takes a ticket (tickets order the chunks
+// of a stream), stages its chunk of dense tokens in LDS with 16-byte loads,
+// selects and packs every token in place, publishes its chunk total, reads the
+// totals or prefixes of the chunks before it, and writes its packed run with
+// 16-byte stores. k_append handles the one-token-per-stream case of a decode
+// step.
 #include "mf_device.h"
 #include "mf_launch.h"
 
 namespace mf {
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // Keep-mask of one token. mag[t] is the fp16 magnitude (bits & 0x7fff) of this
 // lane's channel in tile t. Sets bm[t] (wave-uniform) so that exactly k bits
@@ -88,124 +94,181 @@ __device__ __forceinline__ void load_token(const uint16_t* __restrict__ src, uin
   for (int t = 0; t < T; ++t) xv[t] = src[kTile * t + lane];
 }
 
-// grid (n_chunks, BH), 256 threads: wave w handles tokens [64w, 64w+64) of the chunk.
-template <int T>
-__global__ __launch_bounds__(256) void k_select(const uint16_t* __restrict__ x, int n_new, int k,
-                                                uint64_t* __restrict__ bitmaps, int cap_tokens,
-                                                int tok0, uint32_t* __restrict__ chunk_tot,
-                                                uint32_t* __restrict__ base_out,
-                                                const uint32_t* __restrict__ stream_len,
-                                                int n_chunks) {
-  constexpr int d = kTile * T;
-  const int chunk = blockIdx.x, bh = blockIdx.y;
-  const uint32_t lane = lane_id();
-  const int wave = threadIdx.x / kWave;
-  const int j_begin = chunk * kCompressChunk + wave * kWave;
-  const int j_end = min(j_begin + kWave, n_new);
-  const uint16_t* xs = x + (int64_t)bh * n_new * d;
-  uint64_t* bms = bitmaps + ((int64_t)bh * cap_tokens + tok0) * T;
+// Look-back flag of one chunk: status in bits 63:62, a 32-bit count below.
+constexpr uint64_t kFlagAgg = 1ull << 62;     // the chunk's own total is known
+constexpr uint64_t kFlagPrefix = 2ull << 62;  // the stream offset after the chunk is known
+constexpr uint32_t kSpinLimit = 1u << 20;     // polls before a chunk gives up (never reached)
+constexpr uint32_t kBadBase = 0xffffffffu;
 
-  uint32_t total = 0;
-  uint16_t cur[T], nxt[T];
-  if (j_begin < j_end) load_token<T>(xs + (int64_t)j_begin * d, lane, cur);
-  for (int j = j_begin; j < j_end; ++j) {
-    if (j + 1 < j_end) load_token<T>(xs + (int64_t)(j + 1) * d, lane, nxt);
-    uint32_t mag[T];
-#pragma unroll
-    for (int t = 0; t < T; ++t) mag[t] = cur[t] & 0x7fffu;
-    uint64_t bm[T];
-    select_token<T>(mag, k, bm);
-    uint64_t mine = bm[0];
-#pragma unroll
-    for (int t = 1; t < T; ++t) mine = (lane == (uint32_t)t) ? bm[t] : mine;
-    if (lane < (uint32_t)T) bms[(int64_t)j * T + lane] = mine;
-#pragma unroll
-    for (int t = 0; t < T; ++t) total += pad8((uint32_t)__popcll(bm[t]));
-#pragma unroll
-    for (int t = 0; t < T; ++t) cur[t] = nxt[t];
-  }
-  __shared__ uint32_t part[kCompressChunk / kWave];
-  if (lane == 0) part[wave] = total;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t s = 0;
-    for (int w = 0; w < kCompressChunk / kWave; ++w) s += part[w];
-    chunk_tot[(int64_t)bh * n_chunks + chunk] = s;
-    if (chunk == 0) base_out[bh] = tok0 > 0 ? stream_len[bh] : 0u;
-  }
+__global__ void k_clear(uint32_t* __restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
 }
 
-// grid (n_chunks, BH), 256 threads. Thread i first owns token i of the chunk
-// for the offset scan; then wave w packs tokens [64w, 64w+64).
+// The flag words are the only data workgroups exchange (the count travels in
+// the same 64-bit word as the status, and no workgroup reads what another one
+// writes to the cache), so relaxed device-scope atomics suffice: acquire and
+// release would write back and invalidate the whole L2 of the XCD on every poll.
+//
+// Offset in the stream at which chunk `chunk` starts, computed by one whole
+// wave. The chunk's total is published first; then the wave reads the flags of
+// the 64 chunks before it at once and adds, from the nearest one back, the
+// totals up to and including the first known prefix, moving 64 chunks further
+// back while none is found. Chunks with lower tickets are already running and
+// publish their totals without waiting, so every poll is eventually answered;
+// the poll count is bounded anyway.
+__device__ uint32_t look_back(uint64_t* __restrict__ fl, int chunk, uint32_t total,
+                              uint32_t first_base, uint32_t lane) {
+  if (chunk == 0) {
+    if (lane == 0)
+      __hip_atomic_store(fl, kFlagPrefix | (uint64_t)(first_base + total), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    return first_base;
+  }
+  if (lane == 0)
+    __hip_atomic_store(fl + chunk, kFlagAgg | (uint64_t)total, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  uint32_t acc = 0, polls = 0;
+  for (int top = chunk - 1;;) {
+    const int p = top - (int)lane;
+    // Positions before chunk 0 read as a known prefix of 0.
+    const uint64_t f = p >= 0 ? __hip_atomic_load(fl + p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                              : kFlagPrefix;
+    const uint32_t st = (uint32_t)(f >> 62);
+    const uint64_t pref = ballot(st == 2u);
+    const uint64_t none = ballot(st == 0u);
+    const uint32_t first = pref ? (uint32_t)__builtin_ctzll(pref) : 64u;  // nearest prefix
+    const uint64_t upto = first >= 63u ? ~0ull : ((2ull << first) - 1ull);
+    if (none & upto) {  // a chunk between here and that prefix has not published yet
+      if (++polls > kSpinLimit) return kBadBase;
+      __builtin_amdgcn_s_sleep(1);
+      continue;
+    }
+    uint32_t v = lane <= first ? (uint32_t)f : 0u;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += (uint32_t)__shfl_xor((int)v, o, kWave);
+    acc += v;
+    if (first < 64u) break;
+    top -= kWave;
+  }
+  if (lane == 0)
+    __hip_atomic_store(fl + chunk, kFlagPrefix | (uint64_t)(acc + total), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  return acc;
+}
+
+// 1-D grid of BH * n_chunks workgroups of 4 waves; a chunk is 4 * 64/T tokens of
+// one stream, each wave owning 64/T of them (4096 fp16 values, 8 KiB of LDS).
 template <int T>
-__global__ __launch_bounds__(256) void k_pack(const uint16_t* __restrict__ x, int n_new,
-                                              const uint64_t* __restrict__ bitmaps,
-                                              uint32_t* __restrict__ offsets,
-                                              uint16_t* __restrict__ values,
-                                              uint32_t* __restrict__ stream_len, int cap_tokens,
-                                              int tok0, int64_t val_stride,
-                                              const uint32_t* __restrict__ chunk_tot,
-                                              const uint32_t* __restrict__ base_in, int n_chunks) {
+__global__ __launch_bounds__(256) void k_compress(const uint16_t* __restrict__ x, int n_new, int k,
+                                                  uint64_t* __restrict__ bitmaps,
+                                                  uint32_t* __restrict__ offsets,
+                                                  uint16_t* __restrict__ values,
+                                                  uint32_t* __restrict__ stream_len, int cap_tokens,
+                                                  int tok0, int64_t val_stride,
+                                                  uint64_t* __restrict__ flags,
+                                                  uint32_t* __restrict__ ticket_ctr, int n_chunks) {
   constexpr int d = kTile * T;
-  constexpr int kWaves = kCompressChunk / kWave;
-  const int chunk = blockIdx.x, bh = blockIdx.y;
+  constexpr int kTPW = kWave / T;            // tokens per wave
+  constexpr int kCH = 4 * kTPW;              // tokens per chunk
+  constexpr int kRegion = kTPW * d;          // fp16 values per wave region
+  __shared__ __align__(16) uint16_t s_x[4][kRegion];  // dense tokens, packed in place
+  __shared__ uint64_t s_bm[4][kTPW * T];
+  __shared__ uint32_t s_loc[4][kTPW * T];    // tile offsets relative to the wave's run
+  __shared__ uint32_t s_wtot[4];
+  __shared__ uint32_t s_ticket, s_base;
+
   const int tid = threadIdx.x;
   const uint32_t lane = lane_id();
   const int wave = tid / kWave;
-  __shared__ uint32_t red[kWaves];
-  __shared__ uint32_t start_of[kCompressChunk];
-  __shared__ uint64_t bm_of[kCompressChunk][T];
-
-  // Offset of this chunk inside the stream: base + totals of the earlier chunks.
-  uint32_t s = 0;
-  for (int i = tid; i < chunk; i += kCompressChunk) s += chunk_tot[(int64_t)bh * n_chunks + i];
-  s = (uint32_t)wave_sum_i((int)s);
-  if (lane == 0) red[wave] = s;
+  if (tid == 0) s_ticket = atomicAdd(ticket_ctr, 1u);
   __syncthreads();
-  uint32_t chunk_base = base_in[bh];
-  for (int w = 0; w < kWaves; ++w) chunk_base += red[w];
-  __syncthreads();
+  const int ticket = (int)s_ticket;
+  const int bh = ticket / n_chunks, chunk = ticket % n_chunks;
+  const int j0 = chunk * kCH + wave * kTPW;
+  const int nt = max(0, min(kTPW, n_new - j0));
 
-  // Padded length of each token of the chunk and their exclusive scan.
-  const int jt = chunk * kCompressChunk + tid;
-  const uint64_t* bms = bitmaps + ((int64_t)bh * cap_tokens + tok0) * T;
-  uint32_t len = 0;
+  // Stage the wave's tokens: 16-byte coalesced loads, 8 per lane. Every load
+  // is issued (lanes past the wave's tokens re-read its first 16 bytes) so the
+  // staging registers are written unconditionally.
+  if (nt > 0) {
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(x + ((int64_t)bh * n_new + j0) * d);
+    u32x4_t* dst = reinterpret_cast<u32x4_t*>(s_x[wave]);
+    const int n16 = nt * d / 8;
+    u32x4_t r[kRegion / 8 / kWave];
 #pragma unroll
-  for (int t = 0; t < T; ++t) {
-    const uint64_t b = (jt < n_new) ? bms[(int64_t)jt * T + t] : 0ull;
-    bm_of[tid][t] = b;
-    len += pad8((uint32_t)__popcll(b));
-  }
-  uint32_t incl = len;
+    for (int i = 0; i < kRegion / 8 / kWave; ++i) {
+      const int c = i * kWave + (int)lane;
+      r[i] = src[c < n16 ? c : 0];
+    }
 #pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t v = __shfl_up(incl, o, kWave);
-    if (lane >= (uint32_t)o) incl += v;
+    for (int i = 0; i < kRegion / 8 / kWave; ++i) {
+      const int c = i * kWave + (int)lane;
+      if (c < n16) dst[c] = r[i];
+    }
   }
-  if (lane == kWave - 1) red[wave] = incl;
-  __syncthreads();
-  uint32_t before = 0;
-  for (int w = 0; w < wave; ++w) before += red[w];
-  start_of[tid] = chunk_base + before + incl - len;
-  if (tid == kCompressChunk - 1 && chunk == n_chunks - 1) stream_len[bh] = chunk_base + before + incl;
-  __syncthreads();
 
-  const uint16_t* xs = x + (int64_t)bh * n_new * d;
-  uint16_t* vals = values + (int64_t)bh * val_stride;
-  uint32_t* offs = offsets + ((int64_t)bh * cap_tokens + tok0) * T;
-  const int j_begin = chunk * kCompressChunk + wave * kWave;
-  const int j_end = min(j_begin + kWave, n_new);
-  uint16_t cur[T], nxt[T];
-  if (j_begin < j_end) load_token<T>(xs + (int64_t)j_begin * d, lane, cur);
-  for (int j = j_begin; j < j_end; ++j) {
-    if (j + 1 < j_end) load_token<T>(xs + (int64_t)(j + 1) * d, lane, nxt);
-    const int jl = j - chunk * kCompressChunk;
+  // Select and pack token by token (a wave's LDS operations run in order, so a
+  // token's packed values may overwrite its own dense values once read; they
+  // never reach later tokens because a token packs into at most d values).
+  uint16_t* reg = s_x[wave];
+  uint32_t run = 0;
+  for (int i = 0; i < nt; ++i) {
+    uint16_t xv[T];
+    uint32_t mag[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      xv[t] = reg[i * d + kTile * t + lane];
+      mag[t] = xv[t] & 0x7fffu;
+    }
     uint64_t bm[T];
+    select_token<T>(mag, k, bm);
+    uint32_t pos = run;
 #pragma unroll
-    for (int t = 0; t < T; ++t) bm[t] = bm_of[jl][t];
-    pack_token<T>(cur, bm, start_of[jl], vals, offs + (int64_t)j * T, lane);
-#pragma unroll
-    for (int t = 0; t < T; ++t) cur[t] = nxt[t];
+    for (int t = 0; t < T; ++t) {
+      const uint32_t cnt = (uint32_t)__popcll(bm[t]);
+      const uint32_t below = mbcnt(bm[t], 0u);
+      const bool kept = (bm[t] >> lane) & 1ull;
+      const uint32_t pad_slot = cnt + (lane - below);  // k-th dropped lane fills pad slot k
+      if (kept) reg[pos + below] = xv[t];
+      else if (pad_slot < pad8(cnt)) reg[pos + pad_slot] = 0;
+      if (lane == (uint32_t)t) {
+        s_bm[wave][i * T + t] = bm[t];
+        s_loc[wave][i * T + t] = pos;
+      }
+      pos += pad8(cnt);
+    }
+    run = pos;
+  }
+  if (lane == 0) s_wtot[wave] = run;
+  __syncthreads();
+
+  if (wave == 0) {
+    const uint32_t total = s_wtot[0] + s_wtot[1] + s_wtot[2] + s_wtot[3];
+    const uint32_t first = (chunk == 0 && tok0 > 0) ? stream_len[bh] : 0u;
+    const uint32_t base = look_back(flags + (int64_t)bh * n_chunks, chunk, total, first, lane);
+    if (lane == 0) {
+      s_base = base;
+      if (chunk == n_chunks - 1) stream_len[bh] = base == kBadBase ? kBadBase : base + total;
+    }
+  }
+  __syncthreads();
+  if (s_base == kBadBase) return;  // look-back gave up: nothing is written
+  uint32_t wbase = s_base;
+  for (int w = 0; w < wave; ++w) wbase += s_wtot[w];
+
+  // Packed run (a multiple of 8 values, 16-byte aligned in the stream).
+  {
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(reg);
+    u32x4_t* dst = reinterpret_cast<u32x4_t*>(values + (int64_t)bh * val_stride + wbase);
+    for (uint32_t c = lane; c < run / 8; c += kWave) dst[c] = src[c];
+  }
+  // Bitmaps and offsets of the wave's tiles (tile index = token * T + t).
+  const int64_t tile0 = ((int64_t)bh * cap_tokens + tok0 + j0) * T;
+  if ((int)lane < nt * T) {
+    bitmaps[tile0 + lane] = s_bm[wave][lane];
+    offsets[tile0 + lane] = wbase + s_loc[wave][lane];
   }
 }
 
@@ -242,16 +305,18 @@ __global__ __launch_bounds__(256) void k_append(const uint16_t* __restrict__ x, 
 template <int T>
 static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, int tok0,
                              uint32_t* ws, hipStream_t s) {
-  const int n_chunks = (n_new + kCompressChunk - 1) / kCompressChunk;
-  uint32_t* chunk_tot = ws;
-  uint32_t* base = ws + (int64_t)c.BH * n_chunks;
-  dim3 grid(n_chunks, c.BH);
-  hipLaunchKernelGGL(k_select<T>, grid, dim3(256), 0, s, x, n_new, c.n_keep, c.bitmaps,
-                     c.cap_tokens, tok0, chunk_tot, base, c.stream_len, n_chunks);
+  const int n_chunks = (n_new + compress_chunk_tokens(T) - 1) / compress_chunk_tokens(T);
+  const int64_t n_wg = (int64_t)c.BH * n_chunks;
+  uint64_t* flags = reinterpret_cast<uint64_t*>(ws);
+  uint32_t* ticket = reinterpret_cast<uint32_t*>(flags + n_wg);
+  const int64_t words = 2 * n_wg + 1;
+  const int clear_blocks = (int)((words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024);
+  hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, words);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_pack<T>, grid, dim3(256), 0, s, x, n_new, c.bitmaps, c.offsets, c.values,
-                     c.stream_len, c.cap_tokens, tok0, c.val_stride, chunk_tot, base, n_chunks);
+  hipLaunchKernelGGL(k_compress<T>, dim3((uint32_t)n_wg), dim3(256), 0, s, x, n_new, c.n_keep,
+                     c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
+                     flags, ticket, n_chunks);
   return hipGetLastError();
 }
 

@@ -6,8 +6,10 @@
 
 namespace mf {
 
-// Tokens per workgroup of the two-launch compression (4 waves x 64 tokens).
-constexpr int kCompressChunk = 256;
+// Tokens per workgroup of the bulk compression: 4 waves of 64/T tokens each.
+constexpr int compress_chunk_tokens(int T) { return 4 * (64 / T); }
+// Smallest chunk over the supported head sizes (T = 4), for workspace sizing.
+constexpr int kMinCompressChunk = 64;
 
 struct CacheView {
   uint64_t* bitmaps;
@@ -22,7 +24,8 @@ struct CacheView {
 };
 
 // Compress n_new tokens per stream (x: [BH][n_new][64T] fp16) after tok0 tokens.
-// ws: u32 [BH][n_chunks] chunk totals followed by u32 [BH] stream bases.
+// ws: u64 look-back flags [BH][n_chunks] followed by a u32 ticket counter; it is
+// cleared by the call itself.
 hipError_t launch_compress(const CacheView& c, const uint16_t* x, int n_new, int tok0, uint32_t* ws,
                            hipStream_t s);
 // Compress one token per stream (x: [BH][64T]) as token tok0.

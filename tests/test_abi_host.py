@@ -117,7 +117,9 @@ def test_ccache_init_validates(lib):
 def test_compress_and_append_reject_before_launch(lib):
     c, _ = _fake_cache(B=2, H=4, cap=100)
     ws_need = lib.mustafar_compress_workspace_bytes(2, 4, 50)
-    assert ws_need == 2 * 4 * (1 + 1) * 4
+    # one 8-byte scan flag per stream and 64-token chunk, plus a 16-byte ticket counter
+    assert ws_need == 2 * 4 * 1 * 8 + 16
+    assert lib.mustafar_compress_workspace_bytes(1, 1, 65) == 2 * 8 + 16
     x = 0x500000
     assert lib.mustafar_prune_compress(ctypes.byref(c), x, 0, 0x600000, ws_need, None) == mf.EINVAL
     assert lib.mustafar_prune_compress(ctypes.byref(c), x + 2, 50, 0x600000, ws_need,
@@ -128,6 +130,8 @@ def test_compress_and_append_reject_before_launch(lib):
                                        None) == mf.EWORKSPACE
     assert lib.mustafar_prune_compress(ctypes.byref(c), x, 50, None, ws_need,
                                        None) == mf.EWORKSPACE
+    assert lib.mustafar_prune_compress(ctypes.byref(c), x, 50, 0x600004, ws_need,
+                                       None) == mf.EWORKSPACE                # not 8-byte aligned
     c.n_tokens = 100
     assert lib.mustafar_append(ctypes.byref(c), x, None) == mf.ECAPACITY
     assert lib.mustafar_prune_compress(ctypes.byref(c), x, 1, 0x600000, 10 ** 6,

@@ -69,6 +69,22 @@ def test_compress_ties_zeros_and_subnormals(d, s):
     compare_format(got, oracle.compress(x, s), 130, all_pairs(2, 2))
 
 
+@pytest.mark.parametrize("d", [64, 128, 256])
+def test_compress_many_chunks_shared_workspace(d):
+    # Tens of chunks per stream (long look-back chains) and one workspace reused
+    # by consecutive calls: the call must clear its scan flags itself.
+    import torch
+    announce(f"compress many chunks d={d}")
+    B, H, N = 2, 3, 5000
+    K, V = synth.make_kv(B, H, N, d, seed=300 + d)
+    ws = torch.empty(mf.mustafar_compress_workspace_bytes(B, H, N), dtype=torch.uint8,
+                     device="cuda")
+    for x, s in ((K, 0.5), (V, 0.7), (K, 0.0), (V, 1.0)):
+        cache = mf.CompressedCache(B, H, d, s, N)
+        mf.mustafar_prune_compress(cache, to_dev(x), ws=ws)
+        compare_format(read_cache(cache), oracle.compress(x, s), N, all_pairs(B, H))
+
+
 def test_compress_in_pieces_and_append_equal_compress_all():
     announce("compress pieces + append")
     B, H, d = 2, 4, 128
