@@ -591,31 +591,69 @@ __global__ __launch_bounds__(64) void k_dense_attn(AttnArgs a) {
   write_partial<T, G>(a, seg, bh, m_run, l_run, o);
 }
 
-// grid (BHq), one wave: log-sum-exp merge of the segments, fp16 output (RNE).
+// grid (BHq), 4 waves: log-sum-exp merge of the segments, fp16 output (RNE).
+// The 256 threads first reduce the segments' maxima and weighted sums; then
+// wave w accumulates the weighted partial outputs of segments w, w+4, ...
+// (lane = channel, four segments' loads in flight) and LDS adds the waves.
+constexpr int kMergeWaves = 4;
+
+__device__ __forceinline__ float block_reduce(float v, bool is_max, float* red) {
+  v = is_max ? wave_max_u(v) : wave_sum_u(v);
+  const int wave = threadIdx.x / kWave;
+  if (lane_id() == 0) red[wave] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int w = 1; w < kMergeWaves; ++w) r = is_max ? fmaxf(r, red[w]) : r + red[w];
+  __syncthreads();
+  return r;
+}
+
 template <int T>
-__global__ __launch_bounds__(64) void k_merge(const float2* __restrict__ ws_ml,
-                                              const float* __restrict__ ws_o, int n_seg, int BHq,
-                                              uint16_t* __restrict__ out) {
+__global__ __launch_bounds__(kMergeWaves * kWave) void k_merge(const float2* __restrict__ ws_ml,
+                                                              const float* __restrict__ ws_o,
+                                                              int n_seg, int BHq,
+                                                              uint16_t* __restrict__ out) {
   constexpr int d = kTile * T;
+  __shared__ float red[kMergeWaves];
+  __shared__ float part[kMergeWaves][d];
   const int r = blockIdx.x;
+  const int tid = threadIdx.x, wave = tid / kWave;
   const uint32_t lane = lane_id();
   float M = -INFINITY;
-  for (int s = 0; s < n_seg; ++s) M = fmaxf(M, ws_ml[(int64_t)s * BHq + r].x);
-  float L = 0.f, acc[T];
+  for (int s = tid; s < n_seg; s += kMergeWaves * kWave) M = fmaxf(M, ws_ml[(int64_t)s * BHq + r].x);
+  M = block_reduce(M, true, red);
+  float L = 0.f;
+  for (int s = tid; s < n_seg; s += kMergeWaves * kWave) {
+    const float2 ml = ws_ml[(int64_t)s * BHq + r];
+    L = fmaf(ml.y, ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - M), L);
+  }
+  L = block_reduce(L, false, red);
+
+  float acc[T];
 #pragma unroll
   for (int tt = 0; tt < T; ++tt) acc[tt] = 0.f;
-  for (int s = 0; s < n_seg; ++s) {
+#pragma unroll 4
+  for (int s = wave; s < n_seg; s += kMergeWaves) {
     const float2 ml = ws_ml[(int64_t)s * BHq + r];
-    const float w = __builtin_amdgcn_exp2f(ml.x - M);
-    L = fmaf(ml.y, w, L);
+    const float w = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - M);
+    const float* o = ws_o + ((int64_t)s * BHq + r) * d + lane;
 #pragma unroll
-    for (int tt = 0; tt < T; ++tt)
-      acc[tt] = fmaf(ws_o[((int64_t)s * BHq + r) * d + lane + kTile * tt], w, acc[tt]);
+    for (int tt = 0; tt < T; ++tt) acc[tt] = fmaf(o[kTile * tt], w, acc[tt]);
   }
-  const float inv = 1.f / L;
 #pragma unroll
-  for (int tt = 0; tt < T; ++tt)
-    out[(int64_t)r * d + lane + kTile * tt] = __builtin_bit_cast(uint16_t, (_Float16)(acc[tt] * inv));
+  for (int tt = 0; tt < T; ++tt) part[wave][lane + kTile * tt] = acc[tt];
+  __syncthreads();
+  if (wave == 0) {
+    const float inv = 1.f / L;
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+      float v = part[0][lane + kTile * tt];
+#pragma unroll
+      for (int w = 1; w < kMergeWaves; ++w) v += part[w][lane + kTile * tt];
+      out[(int64_t)r * d + lane + kTile * tt] = __builtin_bit_cast(uint16_t, (_Float16)(v * inv));
+    }
+  }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -667,7 +705,8 @@ static hipError_t attention_TG(const AttnShape& sh, const AttnArgs& a, uint16_t*
     e = hipGetLastError();
   }
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_merge<T>, dim3(a.BHq), dim3(kWave), 0, s, a.ws_ml, a.ws_o, n_seg, a.BHq, out);
+  hipLaunchKernelGGL(k_merge<T>, dim3(a.BHq), dim3(kMergeWaves * kWave), 0, s, a.ws_ml, a.ws_o, n_seg,
+                     a.BHq, out);
   return hipGetLastError();
 }
 
