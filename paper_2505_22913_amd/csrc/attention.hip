@@ -96,6 +96,21 @@ __device__ __forceinline__ float wave_sum_u(float v) {
   return readlane_f(v, 0) + readlane_f(v, 32);
 }
 
+// Maximum over all 64 lanes of a non-negative int, returned wave-uniform.
+template <int CTRL>
+__device__ __forceinline__ int dppi(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+
+__device__ __forceinline__ int wave_max_int(int v) {
+  v = max(v, dppi<0xB1>(v));
+  v = max(v, dppi<0x4E>(v));
+  v = max(v, dppi<0x124>(v));
+  v = max(v, dppi<0x128>(v));
+  v = max(v, __builtin_amdgcn_ds_swizzle(v, 0x401F));
+  return max(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 32));
+}
+
 // Sum over the T lanes (adjacent, T in {1,2,4}) that hold the tiles of one token.
 template <int T>
 __device__ __forceinline__ float tile_sum(float v) {
@@ -298,45 +313,128 @@ __device__ __forceinline__ uint32_t next_channel(uint32_t& x, int u, uint32_t m)
   }
 }
 
-// acc[g] += q[g][channel] * value over one group of 8 packed key values.
+// The walks are software-pipelined: a group is split into an issue step (its
+// 16-byte value load, its channels and, for keys, its q loads) and a consume
+// step (the products, or the scatter into the expanded tile), and the loop
+// issues group g+1 before consuming group g, so each group's LDS round trip
+// overlaps the previous group's arithmetic. Two register sets alternate.
+template <int G> struct QVal { u32x2 v[G / 4]; };  // q of G heads at one channel (G >= 4)
+template <> struct QVal<1> { _Float16 v; };
+template <> struct QVal<2> { half2_t v; };
+
+template <int G>
+struct KeyGroup {
+  u32x4 w;
+  QVal<G> q[8];
+};
+
 template <int G, bool PEEL>
-__device__ __forceinline__ void key_group(uint32_t& x, uint32_t va, uint32_t qaddr, uint32_t m,
-                                          float (&acc)[G]) {
-  const u32x4 w = lds_load<u32x4>(va);
+__device__ __forceinline__ void key_issue(uint32_t& x, uint32_t va, uint32_t qaddr, uint32_t m,
+                                          KeyGroup<G>& k) {
+  k.w = lds_load<u32x4>(va);
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
-    const uint32_t c = next_channel<PEEL>(x, u, m);
-    const uint32_t qa = qaddr + c * (2u * G);
-    const float v = (float)group_value(w, u);
+    const uint32_t qa = qaddr + next_channel<PEEL>(x, u, m) * (2u * G);
     if constexpr (G == 1) {
-      acc[0] = fmaf((float)lds_load<_Float16>(qa), v, acc[0]);
+      k.q[u].v = lds_load<_Float16>(qa);
     } else if constexpr (G == 2) {
-      const half2_t qq = lds_load<half2_t>(qa);
-      acc[0] = fmaf((float)qq.x, v, acc[0]);
-      acc[1] = fmaf((float)qq.y, v, acc[1]);
+      k.q[u].v = lds_load<half2_t>(qa);
     } else {
 #pragma unroll
-      for (int g4 = 0; g4 < G; g4 += 4) {
-        const u32x2 qw = lds_load<u32x2>(qa + 2u * g4);
-        const half2_t q01 = as_h2(qw.x);
-        const half2_t q23 = as_h2(qw.y);
-        acc[g4 + 0] = fmaf((float)q01.x, v, acc[g4 + 0]);
-        acc[g4 + 1] = fmaf((float)q01.y, v, acc[g4 + 1]);
-        acc[g4 + 2] = fmaf((float)q23.x, v, acc[g4 + 2]);
-        acc[g4 + 3] = fmaf((float)q23.y, v, acc[g4 + 3]);
+      for (int g4 = 0; g4 < G / 4; ++g4) k.q[u].v[g4] = lds_load<u32x2>(qa + 8u * g4);
+    }
+  }
+}
+
+template <int G>
+__device__ __forceinline__ void key_consume(const KeyGroup<G>& k, float (&acc)[G]) {
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const float v = (float)group_value(k.w, u);
+    if constexpr (G == 1) {
+      acc[0] = fmaf((float)k.q[u].v, v, acc[0]);
+    } else if constexpr (G == 2) {
+      acc[0] = fmaf((float)k.q[u].v.x, v, acc[0]);
+      acc[1] = fmaf((float)k.q[u].v.y, v, acc[1]);
+    } else {
+#pragma unroll
+      for (int g4 = 0; g4 < G / 4; ++g4) {
+        const half2_t q01 = as_h2(k.q[u].v[g4].x);
+        const half2_t q23 = as_h2(k.q[u].v[g4].y);
+        acc[4 * g4 + 0] = fmaf((float)q01.x, v, acc[4 * g4 + 0]);
+        acc[4 * g4 + 1] = fmaf((float)q01.y, v, acc[4 * g4 + 1]);
+        acc[4 * g4 + 2] = fmaf((float)q23.x, v, acc[4 * g4 + 2]);
+        acc[4 * g4 + 3] = fmaf((float)q23.y, v, acc[4 * g4 + 3]);
       }
     }
   }
 }
 
-// Scatter one group of 8 packed values into the expanded value tile.
+// One 32-channel half of a key tile: n groups of 8 from byte address a (n is the
+// busiest lane's count, so the loop is uniform and every iteration issues the
+// next group before consuming the current one); the first group has m phantom
+// slots when PEEL.
+template <int G, bool PEEL>
+__device__ __forceinline__ void key_half(uint32_t x, uint32_t a, uint32_t qaddr, uint32_t m,
+                                         float (&acc)[G]) {
+  const int n = wave_max_int((int)(m + (uint32_t)__popc(x) + 7u) >> 3);
+  if (n == 0) return;
+  KeyGroup<G> k0, k1;
+  key_issue<G, PEEL>(x, a, qaddr, m, k0);
+  int g = 1;
+  for (; g + 1 < n; g += 2) {
+    key_issue<G, false>(x, a + 16u * g, qaddr, 0u, k1);
+    key_consume<G>(k0, acc);
+    key_issue<G, false>(x, a + 16u * (g + 1), qaddr, 0u, k0);
+    key_consume<G>(k1, acc);
+  }
+  if (g < n) {
+    key_issue<G, false>(x, a + 16u * g, qaddr, 0u, k1);
+    key_consume<G>(k0, acc);
+    key_consume<G>(k1, acc);
+  } else {
+    key_consume<G>(k0, acc);
+  }
+}
+
+struct ValueGroup {
+  u32x4 w;
+  uint32_t c[8];
+};
+
 template <bool PEEL>
-__device__ __forceinline__ void value_group(uint32_t& x, uint32_t va, uint32_t daddr, uint32_t m) {
-  const u32x4 w = lds_load<u32x4>(va);
+__device__ __forceinline__ void value_issue(uint32_t& x, uint32_t va, uint32_t m, ValueGroup& g) {
+  g.w = lds_load<u32x4>(va);
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const uint32_t c = next_channel<PEEL>(x, u, m);
-    lds_store<_Float16>(daddr + c * 4u, group_value(w, u));
+  for (int u = 0; u < 8; ++u) g.c[u] = next_channel<PEEL>(x, u, m);
+}
+
+__device__ __forceinline__ void value_consume(const ValueGroup& g, uint32_t daddr) {
+#pragma unroll
+  for (int u = 0; u < 8; ++u) lds_store<_Float16>(daddr + g.c[u] * 4u, group_value(g.w, u));
+}
+
+// One 32-channel half of a value tile, scattered into the expanded tile
+// (pipelined like key_half).
+template <bool PEEL>
+__device__ __forceinline__ void value_half(uint32_t x, uint32_t a, uint32_t daddr, uint32_t m) {
+  const int n = wave_max_int((int)(m + (uint32_t)__popc(x) + 7u) >> 3);
+  if (n == 0) return;
+  ValueGroup g0, g1;
+  value_issue<PEEL>(x, a, m, g0);
+  int g = 1;
+  for (; g + 1 < n; g += 2) {
+    value_issue<false>(x, a + 16u * g, 0u, g1);
+    value_consume(g0, daddr);
+    value_issue<false>(x, a + 16u * (g + 1), 0u, g0);
+    value_consume(g1, daddr);
+  }
+  if (g < n) {
+    value_issue<false>(x, a + 16u * g, 0u, g1);
+    value_consume(g0, daddr);
+    value_consume(g1, daddr);
+  } else {
+    value_consume(g0, daddr);
   }
 }
 
@@ -344,30 +442,16 @@ __device__ __forceinline__ void value_group(uint32_t& x, uint32_t va, uint32_t d
 template <int G>
 __device__ __forceinline__ void key_walk(uint64_t bm, uint32_t va, uint32_t q_w0, uint32_t q_w1,
                                          float (&acc)[G]) {
-  uint32_t x = (uint32_t)bm;
-  const uint32_t s = (uint32_t)__popc(x);
-  for (uint32_t a = va; ballot(x != 0u); a += 16u) key_group<G, false>(x, a, q_w0, 0u, acc);
-  x = (uint32_t)(bm >> 32);
-  const uint32_t m = s & 7u;
-  uint32_t a = va + 2u * (s - m);
-  if (ballot(x != 0u)) {
-    key_group<G, true>(x, a, q_w1, m, acc);
-    for (a += 16u; ballot(x != 0u); a += 16u) key_group<G, false>(x, a, q_w1, 0u, acc);
-  }
+  const uint32_t lo = (uint32_t)bm, s = (uint32_t)__popc(lo), m = s & 7u;
+  key_half<G, false>(lo, va, q_w0, 0u, acc);
+  key_half<G, true>((uint32_t)(bm >> 32), va + 2u * (s - m), q_w1, m, acc);
 }
 
 // Expansion of one value tile into the dense tile.
 __device__ __forceinline__ void value_walk(uint64_t bm, uint32_t va, uint32_t d_w0, uint32_t d_w1) {
-  uint32_t x = (uint32_t)bm;
-  const uint32_t s = (uint32_t)__popc(x);
-  for (uint32_t a = va; ballot(x != 0u); a += 16u) value_group<false>(x, a, d_w0, 0u);
-  x = (uint32_t)(bm >> 32);
-  const uint32_t m = s & 7u;
-  uint32_t a = va + 2u * (s - m);
-  if (ballot(x != 0u)) {
-    value_group<true>(x, a, d_w1, m);
-    for (a += 16u; ballot(x != 0u); a += 16u) value_group<false>(x, a, d_w1, 0u);
-  }
+  const uint32_t lo = (uint32_t)bm, s = (uint32_t)__popc(lo), m = s & 7u;
+  value_half<false>(lo, va, d_w0, 0u);
+  value_half<true>((uint32_t)(bm >> 32), va + 2u * (s - m), d_w1, m);
 }
 
 // LDS layout of the compressed body (byte offsets). The expanded value tile
@@ -495,7 +579,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
     // and zero values), unrolled so the LDS loads of a batch are in flight
     // together: lane = channel `lane` of every tile.
     constexpr int NP = NB / 2;
-    constexpr int PB = G >= 8 ? 4 : 8;
+    constexpr int PB = G >= 4 ? 4 : 8;
 #pragma unroll 1
     for (int pb = 0; pb < NP; pb += PB) {
       half2_t p2[PB][G], v2[PB][T];
@@ -686,7 +770,9 @@ static hipError_t sparse_stage(const AttnShape& sh, const AttnArgs& a, hipStream
   const int NB = kWave / T;
   const int chunks = (NB * a.kmaxK + 511) / 512 + (NB * a.kmaxV + 511) / 512;
   if (chunks <= 4) return sparse_launch<T, G, 4>(sh, a, s);
+  if (chunks <= 6) return sparse_launch<T, G, 6>(sh, a, s);
   if (chunks <= 8) return sparse_launch<T, G, 8>(sh, a, s);
+  if (chunks <= 12) return sparse_launch<T, G, 12>(sh, a, s);
   return sparse_launch<T, G, 16>(sh, a, s);
 }
 
