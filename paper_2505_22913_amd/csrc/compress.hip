@@ -25,6 +25,16 @@ namespace mf {
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
+template <typename V>
+__device__ __forceinline__ V lds_ld(uint32_t byte_addr) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) V*>(byte_addr);
+}
+
+template <typename V>
+__device__ __forceinline__ void lds_st(uint32_t byte_addr, V v) {
+  *reinterpret_cast<__attribute__((address_space(3))) V*>(byte_addr) = v;
+}
+
 // Keep-mask of one token. mag[t] is the fp16 magnitude (bits & 0x7fff) of this
 // lane's channel in tile t. Sets bm[t] (wave-uniform) so that exactly k bits
 // are set over the T tiles: the k largest magnitudes, ties to lower channels.
@@ -158,117 +168,243 @@ __device__ uint32_t look_back(uint64_t* __restrict__ fl, int chunk, uint32_t tot
   return acc;
 }
 
-// 1-D grid of BH * n_chunks workgroups of 4 waves; a chunk is 4 * 64/T tokens of
-// one stream, each wave owning 64/T of them (4096 fp16 values, 8 KiB of LDS).
-template <int T>
-__global__ __launch_bounds__(256) void k_compress(const uint16_t* __restrict__ x, int n_new, int k,
-                                                  uint64_t* __restrict__ bitmaps,
-                                                  uint32_t* __restrict__ offsets,
-                                                  uint16_t* __restrict__ values,
-                                                  uint32_t* __restrict__ stream_len, int cap_tokens,
-                                                  int tok0, int64_t val_stride,
-                                                  uint64_t* __restrict__ flags,
-                                                  uint32_t* __restrict__ ticket_ctr, int n_chunks) {
-  constexpr int d = kTile * T;
-  constexpr int kTPW = kWave / T;            // tokens per wave
-  constexpr int kCH = 4 * kTPW;              // tokens per chunk
-  constexpr int kRegion = kTPW * d;          // fp16 values per wave region
-  __shared__ __align__(16) uint16_t s_x[4][kRegion];  // dense tokens, packed in place
-  __shared__ uint64_t s_bm[4][kTPW * T];
-  __shared__ uint32_t s_loc[4][kTPW * T];    // tile offsets relative to the wave's run
-  __shared__ uint32_t s_wtot[4];
-  __shared__ uint32_t s_ticket, s_base;
-
-  const int tid = threadIdx.x;
-  const uint32_t lane = lane_id();
-  const int wave = tid / kWave;
-  if (tid == 0) s_ticket = atomicAdd(ticket_ctr, 1u);
-  __syncthreads();
-  const int ticket = (int)s_ticket;
-  const int bh = ticket / n_chunks, chunk = ticket % n_chunks;
-  const int j0 = chunk * kCH + wave * kTPW;
-  const int nt = max(0, min(kTPW, n_new - j0));
-
-  // Stage the wave's tokens: 16-byte coalesced loads, 8 per lane. Every load
-  // is issued (lanes past the wave's tokens re-read its first 16 bytes) so the
-  // staging registers are written unconditionally.
-  if (nt > 0) {
-    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(x + ((int64_t)bh * n_new + j0) * d);
-    u32x4_t* dst = reinterpret_cast<u32x4_t*>(s_x[wave]);
-    const int n16 = nt * d / 8;
-    u32x4_t r[kRegion / 8 / kWave];
+// Top-k selection with one lane per token, bit-sliced. A lane holds the 15-bit
+// magnitudes of its token (of its half of the token when d = 256), two per
+// 32-bit register. A 16x16 bit transpose of each group of 16 registers (the low
+// and high halves are two independent matrices) turns them into bit planes:
+// word b of a group has bit r = bit b of key 2r and bit 16+r = bit b of key
+// 2r+1 of the group's 32 keys. The k largest keys are then found most
+// significant bit first on whole plane words: `cand` holds the keys that still
+// tie with the threshold prefix and `above` those already known to be larger;
+// a plane's ones in `cand` either all stay candidates (if, with `above`, they
+// reach k) or all move to `above`. At the end the threshold ties (`cand`) are
+// taken lowest channel first up to k. This is the same selection as the radix
+// search on the magnitude, with a per-plane cost instead of a per-key one.
+__device__ __forceinline__ void transpose16x2(uint32_t* x) {
+  constexpr uint32_t kMask[4] = {0x00ff00ffu, 0x0f0f0f0fu, 0x33333333u, 0x55555555u};
 #pragma unroll
-    for (int i = 0; i < kRegion / 8 / kWave; ++i) {
+  for (int l = 0; l < 4; ++l) {
+    const int s = 8 >> l;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if (i & s) continue;
+      const uint32_t t = ((x[i] >> s) ^ x[i + s]) & kMask[l];
+      x[i + s] ^= t;
+      x[i] ^= t << s;
+    }
+  }
+}
+
+// Bit r of the low half to bit 2r, bit r of the high half to bit 2r+1.
+__device__ __forceinline__ uint32_t interleave_halves(uint32_t x) {
+  constexpr uint32_t kMask[4] = {0x0000ff00u, 0x00f000f0u, 0x0c0c0c0cu, 0x22222222u};
+#pragma unroll
+  for (int l = 0; l < 4; ++l) {
+    const int s = 8 >> l;
+    const uint32_t t = ((x >> s) ^ x) & kMask[l];
+    x ^= t ^ (t << s);
+  }
+  return x;
+}
+
+// The lowest n set bits of w (n >= 0).
+__device__ __forceinline__ uint32_t lowest_bits(uint32_t w, int n) {
+  if (n >= (int)__popc(w)) return w;
+  if (n <= 0) return 0u;
+  uint32_t p = 0;  // largest p with popcount(w below bit p) < n
+#pragma unroll
+  for (int s = 16; s >= 1; s >>= 1)
+    if ((int)__popc(w & ((1u << (p + s)) - 1u)) < n) p += s;
+  return w & (p >= 31u ? 0xffffffffu : ((2u << p) - 1u));
+}
+
+// One wave per workgroup; a chunk is 64 tokens (32 when d = 256) of one stream.
+template <int T>
+__global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__ x, int n_new, int k,
+                                                    uint64_t* __restrict__ bitmaps,
+                                                    uint32_t* __restrict__ offsets,
+                                                    uint16_t* __restrict__ values,
+                                                    uint32_t* __restrict__ stream_len,
+                                                    int cap_tokens, int tok0, int64_t val_stride,
+                                                    uint64_t* __restrict__ flags,
+                                                    uint32_t* __restrict__ ticket_ctr, int n_chunks) {
+  constexpr int d = kTile * T;
+  constexpr int LPT = T >= 4 ? 2 : 1;      // lanes per token in the threshold search
+  constexpr int TPW = kWave / LPT;          // tokens per chunk
+  constexpr int CPL = d / LPT;              // channels per lane
+  constexpr int NR = CPL / 2;               // packed registers per lane
+  constexpr int ROW = d * 2 + 16;           // LDS bytes per token row (pad: conflict-free row reads)
+  constexpr int P16 = d / 8;                // 16-byte pieces per row
+  __shared__ __align__(16) unsigned char s_rows[TPW * ROW];  // dense rows, then the packed run
+
+  const uint32_t lane = lane_id();
+  uint32_t tk = 0;
+  if (lane == 0) tk = atomicAdd(ticket_ctr, 1u);
+  const int ticket = __builtin_amdgcn_readfirstlane((int)tk);
+  const int bh = ticket / n_chunks, chunk = ticket % n_chunks;
+  const int j0 = chunk * TPW;
+  const int nt = min(TPW, n_new - j0);      // >= 1
+  const uint32_t base_lds = (uint32_t)(uintptr_t)s_rows;
+
+  // Stage the chunk's dense rows: 16-byte coalesced loads (every load issued;
+  // lanes past the chunk re-read its first piece and store nothing).
+  {
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(x + ((int64_t)bh * n_new + j0) * d);
+    const int n16 = nt * P16;
+    constexpr int kIt = TPW * P16 / kWave;
+    u32x4_t r[kIt];
+#pragma unroll
+    for (int i = 0; i < kIt; ++i) {
       const int c = i * kWave + (int)lane;
       r[i] = src[c < n16 ? c : 0];
     }
 #pragma unroll
-    for (int i = 0; i < kRegion / 8 / kWave; ++i) {
+    for (int i = 0; i < kIt; ++i) {
       const int c = i * kWave + (int)lane;
-      if (c < n16) dst[c] = r[i];
+      if (c < n16) *reinterpret_cast<u32x4_t*>(s_rows + (c / P16) * ROW + (c % P16) * 16) = r[i];
     }
   }
 
-  // Select and pack token by token (a wave's LDS operations run in order, so a
-  // token's packed values may overwrite its own dense values once read; they
-  // never reach later tokens because a token packs into at most d values).
-  uint16_t* reg = s_x[wave];
-  uint32_t run = 0;
+  // Keep-mask of this lane's token (lanes past the chunk select on a copy of
+  // the last row and store nothing): NW words of 32 channels, channel order.
+  constexpr int NW = NR / 16;
+  uint32_t keep[NW];
+  {
+    const int jt = min((int)lane / LPT, nt - 1);
+    const unsigned char* row = s_rows + jt * ROW + ((int)lane % LPT) * CPL * 2;
+    uint32_t pl[NR];
+#pragma unroll
+    for (int i = 0; i < NR / 4; ++i) {
+      const u32x4_t w = *reinterpret_cast<const u32x4_t*>(row + 16 * i);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pl[4 * i + e] = w[e] & 0x7fff7fffu;
+    }
+#pragma unroll
+    for (int g = 0; g < NW; ++g) transpose16x2(pl + 16 * g);   // pl[16g + b] = plane b of group g
+    uint32_t cand[NW], above[NW];
+#pragma unroll
+    for (int g = 0; g < NW; ++g) {
+      cand[g] = 0xffffffffu;
+      above[g] = 0u;
+    }
+    int n_above = 0;
+#pragma unroll
+    for (int b = 14; b >= 0; --b) {
+      uint32_t ones[NW];
+      int c1 = 0;
+#pragma unroll
+      for (int g = 0; g < NW; ++g) {
+        ones[g] = cand[g] & pl[16 * g + b];
+        c1 += __popc(ones[g]);
+      }
+      if constexpr (LPT == 2) c1 += __builtin_amdgcn_mov_dpp(c1, 0xB1, 0xF, 0xF, false);
+      const bool take = n_above + c1 >= k;
+#pragma unroll
+      for (int g = 0; g < NW; ++g) {
+        above[g] = take ? above[g] : (above[g] | ones[g]);
+        cand[g] = take ? ones[g] : (cand[g] & ~pl[16 * g + b]);
+      }
+      n_above += take ? 0 : c1;
+    }
+    // Ties at the threshold: the lowest channels first, up to k (across the two
+    // lanes of a d = 256 token, the lower half of the channels first).
+    int need = k - n_above, n_cand = 0;
+#pragma unroll
+    for (int g = 0; g < NW; ++g) {
+      above[g] = interleave_halves(above[g]);
+      cand[g] = interleave_halves(cand[g]);
+      n_cand += __popc(cand[g]);
+    }
+    if constexpr (LPT == 2) {
+      const int lower = __builtin_amdgcn_mov_dpp(n_cand, 0xB1, 0xF, 0xF, false);
+      if (lane & 1u) need -= lower;
+    }
+    if (ballot(need < n_cand)) {
+#pragma unroll
+      for (int g = 0; g < NW; ++g) {
+        const int c = __popc(cand[g]);
+        cand[g] = lowest_bits(cand[g], need);
+        need -= c;
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < NW; ++g) keep[g] = above[g] | cand[g];
+  }
+
+  // Tile offsets relative to the chunk's run: the padded tile counts of this
+  // lane, scanned over the lanes (token-major, so for d = 256 the lower half
+  // of a token comes first).
+  constexpr int TPL = T / LPT;               // tiles per lane
+  uint32_t tile_pos[TPL];
+  uint32_t lane_len = 0;
+#pragma unroll
+  for (int t = 0; t < TPL; ++t) {
+    tile_pos[t] = lane_len;
+    lane_len += pad8((uint32_t)(__popc(keep[2 * t]) + __popc(keep[2 * t + 1])));
+  }
+  if ((int)lane >= nt * LPT) lane_len = 0;   // lanes past the chunk hold no token
+  uint32_t incl = lane_len;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t v = (uint32_t)__shfl_up((int)incl, o, kWave);
+    if ((int)lane >= o) incl += v;
+  }
+  const uint32_t lane_off = incl - lane_len;
+  const uint32_t run = (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
+
+  // Packing, one token at a time with lane = channel (tile bitmaps and offsets
+  // read from the selecting lanes). The packed run is written over the rows in
+  // place: a token packs into at most d values, so it never reaches the next
+  // token's row.
+  uint16_t xn[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) xn[t] = lds_ld<uint16_t>(base_lds + (kTile * t + lane) * 2);
   for (int i = 0; i < nt; ++i) {
     uint16_t xv[T];
-    uint32_t mag[T];
 #pragma unroll
     for (int t = 0; t < T; ++t) {
-      xv[t] = reg[i * d + kTile * t + lane];
-      mag[t] = xv[t] & 0x7fffu;
+      xv[t] = xn[t];
+      if (i + 1 < nt) xn[t] = lds_ld<uint16_t>(base_lds + (i + 1) * ROW + (kTile * t + lane) * 2);
     }
-    uint64_t bm[T];
-    select_token<T>(mag, k, bm);
-    uint32_t pos = run;
+    uint32_t pos = (uint32_t)__builtin_amdgcn_readlane((int)lane_off, i * LPT);
 #pragma unroll
     for (int t = 0; t < T; ++t) {
-      const uint32_t cnt = (uint32_t)__popcll(bm[t]);
-      const uint32_t below = mbcnt(bm[t], 0u);
-      const bool kept = (bm[t] >> lane) & 1ull;
-      const uint32_t pad_slot = cnt + (lane - below);  // k-th dropped lane fills pad slot k
-      if (kept) reg[pos + below] = xv[t];
-      else if (pad_slot < pad8(cnt)) reg[pos + pad_slot] = 0;
-      if (lane == (uint32_t)t) {
-        s_bm[wave][i * T + t] = bm[t];
-        s_loc[wave][i * T + t] = pos;
-      }
+      const int src = i * LPT + t / TPL;         // lane holding tile t of token i
+      const int w0 = 2 * (t % TPL);              // its word pair
+      const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)keep[w0], src);
+      const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)keep[w0 + 1], src);
+      const uint64_t bm = (uint64_t)lo | ((uint64_t)hi << 32);
+      if (LPT == 2 && t == TPL)
+        pos = (uint32_t)__builtin_amdgcn_readlane((int)lane_off, i * LPT + 1);
+      const uint32_t cnt = (uint32_t)__popcll(bm);
+      const uint32_t below = mbcnt(bm, 0u);
+      const bool kept = (bm >> lane) & 1ull;
+      const uint32_t slot = kept ? below : cnt + (lane - below);  // dropped lane r fills pad slot r
+      if (kept || slot < pad8(cnt))
+        lds_st<uint16_t>(base_lds + (pos + slot) * 2, kept ? xv[t] : (uint16_t)0);
       pos += pad8(cnt);
     }
-    run = pos;
   }
-  if (lane == 0) s_wtot[wave] = run;
-  __syncthreads();
 
-  if (wave == 0) {
-    const uint32_t total = s_wtot[0] + s_wtot[1] + s_wtot[2] + s_wtot[3];
-    const uint32_t first = (chunk == 0 && tok0 > 0) ? stream_len[bh] : 0u;
-    const uint32_t base = look_back(flags + (int64_t)bh * n_chunks, chunk, total, first, lane);
-    if (lane == 0) {
-      s_base = base;
-      if (chunk == n_chunks - 1) stream_len[bh] = base == kBadBase ? kBadBase : base + total;
-    }
-  }
-  __syncthreads();
-  if (s_base == kBadBase) return;  // look-back gave up: nothing is written
-  uint32_t wbase = s_base;
-  for (int w = 0; w < wave; ++w) wbase += s_wtot[w];
+  const uint32_t first = (chunk == 0 && tok0 > 0) ? stream_len[bh] : 0u;
+  const uint32_t base = look_back(flags + (int64_t)bh * n_chunks, chunk, run, first, lane);
+  if (lane == 0 && chunk == n_chunks - 1) stream_len[bh] = base == kBadBase ? kBadBase : base + run;
+  if (base == kBadBase) return;  // look-back gave up: nothing is written
 
   // Packed run (a multiple of 8 values, 16-byte aligned in the stream).
   {
-    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(reg);
-    u32x4_t* dst = reinterpret_cast<u32x4_t*>(values + (int64_t)bh * val_stride + wbase);
-    for (uint32_t c = lane; c < run / 8; c += kWave) dst[c] = src[c];
+    u32x4_t* dst = reinterpret_cast<u32x4_t*>(values + (int64_t)bh * val_stride + base);
+    for (uint32_t c = lane; c < run / 8; c += kWave)
+      dst[c] = *reinterpret_cast<const u32x4_t*>(s_rows + 16 * c);
   }
-  // Bitmaps and offsets of the wave's tiles (tile index = token * T + t).
-  const int64_t tile0 = ((int64_t)bh * cap_tokens + tok0 + j0) * T;
-  if ((int)lane < nt * T) {
-    bitmaps[tile0 + lane] = s_bm[wave][lane];
-    offsets[tile0 + lane] = wbase + s_loc[wave][lane];
+  // Bitmaps and offsets of this lane's tiles (tile index = token * T + t).
+  if ((int)lane < nt * LPT) {
+    const int64_t tile0 = ((int64_t)bh * cap_tokens + tok0 + j0) * T + (int)lane * TPL;
+#pragma unroll
+    for (int t = 0; t < TPL; ++t) {
+      bitmaps[tile0 + t] = (uint64_t)keep[2 * t] | ((uint64_t)keep[2 * t + 1] << 32);
+      offsets[tile0 + t] = base + lane_off + tile_pos[t];
+    }
   }
 }
 
@@ -314,7 +450,7 @@ static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, i
   hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, words);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_compress<T>, dim3((uint32_t)n_wg), dim3(256), 0, s, x, n_new, c.n_keep,
+  hipLaunchKernelGGL(k_compress<T>, dim3((uint32_t)n_wg), dim3(kWave), 0, s, x, n_new, c.n_keep,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
                      flags, ticket, n_chunks);
   return hipGetLastError();

@@ -6,10 +6,11 @@
 
 namespace mf {
 
-// Tokens per workgroup of the bulk compression: 4 waves of 64/T tokens each.
-constexpr int compress_chunk_tokens(int T) { return 4 * (64 / T); }
+// Tokens per one-wave workgroup of the bulk compression (one lane per token,
+// two lanes per token when d = 256).
+constexpr int compress_chunk_tokens(int T) { return T >= 4 ? 32 : 64; }
 // Smallest chunk over the supported head sizes (T = 4), for workspace sizing.
-constexpr int kMinCompressChunk = 64;
+constexpr int kMinCompressChunk = 32;
 
 struct CacheView {
   uint64_t* bitmaps;
