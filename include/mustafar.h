@@ -167,6 +167,14 @@ int mustafar_dense_decode_attn(const void* q, int B, int Hq, int Hkv, const void
 /* Static message for a status code. */
 const char* mustafar_strerror(int status);
 
+/* MEASUREMENT HELPER (not a step of the method). Streams `bytes` of device
+ * memory at `src` through 16-byte loads and writes one 32-bit checksum per
+ * workgroup to `sink` (device, at least mustafar_stream_read_sink_bytes()):
+ * the HBM read ceiling the decode kernels are measured against. `src` must be
+ * 16-byte aligned and `bytes` a multiple of 16. Errors: EINVAL. */
+size_t mustafar_stream_read_sink_bytes(void);
+int mustafar_stream_read(const void* src, size_t bytes, void* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -68,6 +68,9 @@ _SIGS = {
                                                   ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                                   ctypes.c_size_t, ctypes.c_void_p]),
     "mustafar_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+    "mustafar_stream_read_sink_bytes": (ctypes.c_size_t, []),
+    "mustafar_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                            ctypes.c_void_p]),
 }
 
 
@@ -237,3 +240,14 @@ def mustafar_dense_decode_attn(q, k, v, scale: float = 0.0, out=None, n_splits: 
         _dptr(q), B, Hq, Hkv, _dptr(k), _dptr(v), N, d, float(scale), _dptr(out), int(n_splits),
         _dptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
     return out
+
+
+def mustafar_stream_read(buf, sink=None, stream=None):
+    """Measurement helper: stream the bytes of device tensor `buf` through 16-byte loads."""
+    import torch
+    if sink is None:
+        sink = torch.empty(lib().mustafar_stream_read_sink_bytes(), dtype=torch.uint8,
+                           device=buf.device)
+    _check("mustafar_stream_read", lib().mustafar_stream_read(
+        _dptr(buf), buf.numel() * buf.element_size(), _dptr(sink), _stream(stream)))
+    return sink

@@ -12,7 +12,7 @@ namespace {
 constexpr int kTile = MUSTAFAR_TILE;
 constexpr int kPad = MUSTAFAR_PAD;
 constexpr int kMaxGrid = 65535;            // grid.y limit for the stream index
-constexpr int kTargetWaves = 16384;        // decode: ~5 rounds of ~13 resident waves on 256 CUs
+constexpr int kTargetWaves = 32768;        // decode: ~10 rounds of ~13 resident waves on 256 CUs
 constexpr int kMinSegTokens = 128;         // decode: smallest useful segment
 constexpr int kSegAlign = 64;              // segments are whole 64-token blocks
 

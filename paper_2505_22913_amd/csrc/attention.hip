@@ -161,10 +161,10 @@ __device__ __forceinline__ void dense_body(const AttnArgs& a, int dseg, int bh, 
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g] = 0.f;
     if (valid) {
-      const uint4* kr = reinterpret_cast<const uint4*>(kd + (int64_t)(b0 + (int)j) * d + kTile * t);
+      const u32x4* kr = reinterpret_cast<const u32x4*>(kd + (int64_t)(b0 + (int)j) * d + kTile * t);
 #pragma unroll
       for (int i = 0; i < kTile / 8; ++i) {
-        const uint4 u = kr[i];
+        const u32x4 u = kr[i];
         const half2_t k2[4] = {as_h2(u.x), as_h2(u.y),
                                as_h2(u.z), as_h2(u.w)};
 #pragma unroll
@@ -220,10 +220,10 @@ __device__ __forceinline__ TileMeta load_meta(const AttnArgs& a, int64_t kt0, in
   TileMeta m = {0ull, 0ull, 0u, 0u};
   if ((int)(lane / T) < nb) {
     const int64_t ti = (int64_t)b0 * T + lane;
-    m.kb = a.K.bitmaps[kt0 + ti];
-    m.ko = a.K.offsets[kt0 + ti];
-    m.vb = a.V.bitmaps[vt0 + ti];
-    m.vo = a.V.offsets[vt0 + ti];
+    m.kb = __builtin_nontemporal_load(&a.K.bitmaps[kt0 + ti]);
+    m.ko = __builtin_nontemporal_load(&a.K.offsets[kt0 + ti]);
+    m.vb = __builtin_nontemporal_load(&a.V.bitmaps[vt0 + ti]);
+    m.vo = __builtin_nontemporal_load(&a.V.offsets[vt0 + ti]);
   }
   return m;
 }
@@ -244,7 +244,9 @@ __device__ __forceinline__ Runs runs_of(const TileMeta& m, int nb) {
   return r;
 }
 
-// 512 fp16 values (one 16-byte load per lane) per staging chunk.
+// 512 fp16 values (one 16-byte load per lane) per staging chunk. The
+// compressed streams are read once per call, so every HBM read of the
+// compressed path is non-temporal (measured faster on gfx950 than cached loads).
 template <int STAGE>
 __device__ __forceinline__ void stage_issue(u32x4 (&r)[STAGE], const uint16_t* kv, const uint16_t* vv,
                                             const uint16_t* safe, const Runs& rn, uint32_t lane) {
@@ -257,7 +259,7 @@ __device__ __forceinline__ void stage_issue(u32x4 (&r)[STAGE], const uint16_t* k
     const uint32_t off = 512u * (is_k ? (uint32_t)c : (uint32_t)c - nck) + 8u * lane;
     const uint32_t n = is_k ? rn.kn : rn.vn;
     const uint16_t* src = (is_k ? kv + rn.kstart : vv + rn.vstart) + off;
-    r[c] = *reinterpret_cast<const u32x4*>(off < n ? src : safe);
+    r[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(off < n ? src : safe));
   }
 }
 

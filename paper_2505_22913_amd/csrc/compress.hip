@@ -246,8 +246,8 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
   const int nt = min(TPW, n_new - j0);      // >= 1
   const uint32_t base_lds = (uint32_t)(uintptr_t)s_rows;
 
-  // Stage the chunk's dense rows: 16-byte coalesced loads (every load issued;
-  // lanes past the chunk re-read its first piece and store nothing).
+  // Stage the chunk's dense rows: 16-byte coalesced non-temporal loads (every
+  // load issued; lanes past the chunk re-read its first piece and store nothing).
   {
     const u32x4_t* src = reinterpret_cast<const u32x4_t*>(x + ((int64_t)bh * n_new + j0) * d);
     const int n16 = nt * P16;
@@ -256,7 +256,7 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
 #pragma unroll
     for (int i = 0; i < kIt; ++i) {
       const int c = i * kWave + (int)lane;
-      r[i] = src[c < n16 ? c : 0];
+      r[i] = __builtin_nontemporal_load(&src[c < n16 ? c : 0]);
     }
 #pragma unroll
     for (int i = 0; i < kIt; ++i) {
@@ -395,7 +395,7 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
   {
     u32x4_t* dst = reinterpret_cast<u32x4_t*>(values + (int64_t)bh * val_stride + base);
     for (uint32_t c = lane; c < run / 8; c += kWave)
-      dst[c] = *reinterpret_cast<const u32x4_t*>(s_rows + 16 * c);
+      __builtin_nontemporal_store(*reinterpret_cast<const u32x4_t*>(s_rows + 16 * c), &dst[c]);
   }
   // Bitmaps and offsets of this lane's tiles (tile index = token * T + t).
   if ((int)lane < nt * LPT) {

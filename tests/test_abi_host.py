@@ -182,3 +182,11 @@ def test_strerror_covers_every_status(lib):
     for code in (mf.OK, mf.EINVAL, mf.ECAPACITY, mf.EWORKSPACE, mf.ELAUNCH, mf.EUNSUPPORTED):
         assert mf.strerror(code) not in ("", "unknown status")
     assert mf.strerror(-99) == "unknown status"
+
+
+def test_stream_read_helper_rejects_bad_arguments(lib):
+    assert lib.mustafar_stream_read_sink_bytes() > 0
+    assert lib.mustafar_stream_read(0x100008, 64, 0x200000, None) == mf.EINVAL   # src not 16-aligned
+    assert lib.mustafar_stream_read(0x100000, 24, 0x200000, None) == mf.EINVAL   # bytes % 16
+    assert lib.mustafar_stream_read(None, 64, 0x200000, None) == mf.EINVAL
+    assert lib.mustafar_stream_read(0x100000, 64, None, None) == mf.EINVAL

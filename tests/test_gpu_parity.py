@@ -208,3 +208,15 @@ def test_decode_loop_append_then_attend():
         if step < steps:
             mf.mustafar_append(Kc, to_dev(np.ascontiguousarray(K[:, :, ns])))
             mf.mustafar_append(Vc, to_dev(np.ascontiguousarray(V[:, :, ns])))
+
+
+def test_stream_read_checksum():
+    # The read-ceiling helper must really read every byte: the XOR of the
+    # per-workgroup checksums equals the XOR of all 32-bit words.
+    import torch
+    announce("stream read checksum")
+    rng = np.random.default_rng(3)
+    words = rng.integers(0, 2 ** 32, size=(1 << 20) + 12, dtype=np.uint64).astype(np.uint32)
+    buf = torch.from_numpy(words.view(np.int32)).cuda()
+    sink = mf.mustafar_stream_read(buf).cpu().numpy().view(np.uint32)
+    assert int(np.bitwise_xor.reduce(sink)) == int(np.bitwise_xor.reduce(words))
