@@ -19,7 +19,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libmustafar.so")
-SOURCES = ["api.hip", "compress.hip", "attention.hip", "measure.hip"]
+SOURCES = ["api.hip", "compress.hip", "attention.hip", "attention_mfma.hip", "measure.hip"]
 ARCH = "gfx950"
 
 

@@ -172,9 +172,13 @@ int mustafar_attn_default_splits(int B, int Hkv, int n_tokens) {
 size_t mustafar_attn_workspace_bytes(int B, int Hq, int Hkv, int d, int n_tokens, int n_splits) {
   if (B < 1 || Hq < 1 || Hkv < 1 || d < 1 || n_tokens < 0) return 0;
   if (n_splits <= 0) n_splits = mustafar_attn_default_splits(B, Hkv, n_tokens);
-  // Segments actually launched never exceed n_splits over the tokens plus one window segment.
+  // Segments actually launched never exceed n_splits over the tokens plus one window
+  // segment; a two-level merge adds its first-level parts.
   const int64_t n_seg = (int64_t)n_splits + 1;
-  return (size_t)(n_seg * B * Hq * (int64_t)(d + 2) * (int64_t)sizeof(float));
+  const int64_t BHq = (int64_t)B * Hq;
+  const int64_t parts = mf::merge_parts(n_seg, BHq);
+  const int64_t rows = n_seg + (parts > 1 ? parts : 0);
+  return (size_t)(rows * BHq * (int64_t)(d + 2) * (int64_t)sizeof(float));
 }
 
 static int decode_common(const void* q, int B, int Hq, int Hkv, int d, int n_s, int n_dense,

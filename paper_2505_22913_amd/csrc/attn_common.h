@@ -1,0 +1,387 @@
+// Device helpers shared by the decode-attention kernels (attention.hip: the
+// bit-walk kernel for G = 1, attention_mfma.hip: the MFMA kernel for G >= 2):
+// types, wave reductions, LDS access, the staging of compressed blocks, the
+// bit-walk primitives, the dense (window) segment body and the partial-result
+// writes of the split-K scheme.
+#pragma once
+
+#include "mf_device.h"
+#include "mf_launch.h"
+
+namespace mf {
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Reinterpret 32 bits as two fp16. Takes the word BY VALUE: __builtin_bit_cast
+// applied directly to an ext-vector element (w.y) reinterprets element 0.
+__device__ __forceinline__ half2_t as_h2(uint32_t w) { return __builtin_bit_cast(half2_t, w); }
+
+// Per tile and per 32-channel half, one scratch slot precedes the channels:
+// [s][ch 0..31][s][ch 32..63] -- slot of channel c is 1 + c + (c >= 32).
+constexpr int kSlots = 66;
+
+// Zero fp16 values staged after each packed run (a multiple of 8).
+constexpr uint32_t kMargin = 80;
+
+struct AttnArgs {
+  const uint16_t* q;
+  SparseSide K, V;
+  const uint16_t* kd;  // dense keys   [BHkv][n_dense][d]
+  const uint16_t* vd;  // dense values [BHkv][n_dense][d]
+  int n_s, n_dense;
+  int n_sparse_segs, sparse_seg_tokens;
+  int n_dense_segs, dense_seg_tokens;
+  float scale_log2;
+  float2* ws_ml;
+  float* ws_o;
+  int BHq;
+  int kmaxK, kmaxV;  // worst-case fp16 elements per token of each cache
+};
+
+__device__ __forceinline__ uint32_t ffbl(uint32_t x) {  // 0xffffffff when x == 0
+  uint32_t r;
+  asm("v_ffbl_b32 %0, %1" : "=v"(r) : "v"(x));
+  return r;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ float swz_xor16(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
+}
+
+__device__ __forceinline__ float readlane_f(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+
+// Max / sum over all 64 lanes, returned wave-uniform: DPP within 16-lane rows,
+// a swizzle across row pairs, then the two 32-lane halves.
+__device__ __forceinline__ float wave_max_u(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp<0x124>(v));  // row_ror:4
+  v = fmaxf(v, dpp<0x128>(v));  // row_ror:8
+  v = fmaxf(v, swz_xor16(v));
+  return fmaxf(readlane_f(v, 0), readlane_f(v, 32));
+}
+
+__device__ __forceinline__ float wave_sum_u(float v) {
+  v += dpp<0xB1>(v);
+  v += dpp<0x4E>(v);
+  v += dpp<0x124>(v);
+  v += dpp<0x128>(v);
+  v += swz_xor16(v);
+  return readlane_f(v, 0) + readlane_f(v, 32);
+}
+
+// Maximum over all 64 lanes of a non-negative int, returned wave-uniform.
+template <int CTRL>
+__device__ __forceinline__ int dppi(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+
+__device__ __forceinline__ int wave_max_int(int v) {
+  v = max(v, dppi<0xB1>(v));
+  v = max(v, dppi<0x4E>(v));
+  v = max(v, dppi<0x124>(v));
+  v = max(v, dppi<0x128>(v));
+  v = max(v, __builtin_amdgcn_ds_swizzle(v, 0x401F));
+  return max(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 32));
+}
+
+// Sum over the T lanes (adjacent, T in {1,2,4}) that hold the tiles of one token.
+template <int T>
+__device__ __forceinline__ float tile_sum(float v) {
+  if constexpr (T >= 2) v += dpp<0xB1>(v);
+  if constexpr (T >= 4) v += dpp<0x4E>(v);
+  return v;
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)p;
+}
+
+template <typename V>
+__device__ __forceinline__ V lds_load(uint32_t byte_addr) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) V*>(byte_addr);
+}
+
+template <typename V>
+__device__ __forceinline__ void lds_store(uint32_t byte_addr, V v) {
+  *reinterpret_cast<__attribute__((address_space(3))) V*>(byte_addr) = v;
+}
+
+// ------------------------------------------------------------------------------------------
+// Dense segment body: the local window of the sparse call, or a range of a dense cache.
+// ------------------------------------------------------------------------------------------
+template <int T, int G>
+__device__ __forceinline__ void dense_body(const AttnArgs& a, int dseg, int bh, unsigned char* smem,
+                                           float (&m_run)[G], float (&l_run)[G],
+                                           float (&o)[G][T]) {
+  constexpr int d = kTile * T;
+  constexpr int NB = kWave / T;
+  uint16_t* qs = reinterpret_cast<uint16_t*>(smem);           // [G][d]
+  float* ps = reinterpret_cast<float*>(smem + G * d * 2);     // [NB][G]
+  const uint32_t lane = lane_id();
+  const uint32_t j = lane / T, t = lane % T;
+  const uint16_t* qsrc = a.q + (int64_t)bh * G * d;
+  for (int i = lane; i < G * d; i += kWave) qs[i] = qsrc[i];
+  __syncthreads();
+
+  const int j0 = dseg * a.dense_seg_tokens;
+  const int j1 = min(j0 + a.dense_seg_tokens, a.n_dense);
+  const uint16_t* kd = a.kd + (int64_t)bh * a.n_dense * d;
+  const uint16_t* vd = a.vd + (int64_t)bh * a.n_dense * d;
+  for (int b0 = j0; b0 < j1; b0 += NB) {
+    const int nb = min(NB, j1 - b0);
+    const bool valid = (int)j < nb;
+    float acc[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[g] = 0.f;
+    if (valid) {
+      const u32x4* kr = reinterpret_cast<const u32x4*>(kd + (int64_t)(b0 + (int)j) * d + kTile * t);
+#pragma unroll
+      for (int i = 0; i < kTile / 8; ++i) {
+        const u32x4 u = kr[i];
+        const half2_t k2[4] = {as_h2(u.x), as_h2(u.y),
+                               as_h2(u.z), as_h2(u.w)};
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const uint4 qq = *reinterpret_cast<const uint4*>(qs + g * d + kTile * t + 8 * i);
+          acc[g] = __builtin_amdgcn_fdot2(k2[0], as_h2(qq.x), acc[g], false);
+          acc[g] = __builtin_amdgcn_fdot2(k2[1], as_h2(qq.y), acc[g], false);
+          acc[g] = __builtin_amdgcn_fdot2(k2[2], as_h2(qq.z), acc[g], false);
+          acc[g] = __builtin_amdgcn_fdot2(k2[3], as_h2(qq.w), acc[g], false);
+        }
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float sc = valid ? tile_sum<T>(acc[g]) * a.scale_log2 : -INFINITY;
+      const float mnew = fmaxf(m_run[g], wave_max_u(sc));
+      const float alpha = __builtin_amdgcn_exp2f(m_run[g] - mnew);
+      const float pj = valid ? __builtin_amdgcn_exp2f(sc - mnew) : 0.f;
+      l_run[g] = l_run[g] * alpha + wave_sum_u(t == 0 ? pj : 0.f);
+      m_run[g] = mnew;
+#pragma unroll
+      for (int tt = 0; tt < T; ++tt) o[g][tt] *= alpha;
+      if (t == 0 && valid) ps[j * G + g] = pj;
+    }
+    __syncthreads();
+    for (int jj = 0; jj < nb; ++jj) {
+      float pv[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) pv[g] = ps[jj * G + g];
+      const uint16_t* vr = vd + (int64_t)(b0 + jj) * d;
+#pragma unroll
+      for (int tt = 0; tt < T; ++tt) {
+        const float v = half_bits_to_float(vr[lane + kTile * tt]);
+#pragma unroll
+        for (int g = 0; g < G; ++g) o[g][tt] = fmaf(pv[g], v, o[g][tt]);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Compressed segment body.
+// ------------------------------------------------------------------------------------------
+struct TileMeta {
+  uint64_t kb, vb;  // this lane's key / value tile bitmaps (0 past the block end)
+  uint32_t ko, vo;  // their offsets
+};
+
+template <int T>
+__device__ __forceinline__ TileMeta load_meta(const AttnArgs& a, int64_t kt0, int64_t vt0, int b0,
+                                              int nb, uint32_t lane) {
+  TileMeta m = {0ull, 0ull, 0u, 0u};
+  if ((int)(lane / T) < nb) {
+    const int64_t ti = (int64_t)b0 * T + lane;
+    m.kb = __builtin_nontemporal_load(&a.K.bitmaps[kt0 + ti]);
+    m.ko = __builtin_nontemporal_load(&a.K.offsets[kt0 + ti]);
+    m.vb = __builtin_nontemporal_load(&a.V.bitmaps[vt0 + ti]);
+    m.vo = __builtin_nontemporal_load(&a.V.offsets[vt0 + ti]);
+  }
+  return m;
+}
+
+// Packed-value runs of one block: [kstart, kstart + kn) and [vstart, vstart + vn).
+struct Runs {
+  uint32_t kstart, kn, vstart, vn;
+};
+
+template <int T>
+__device__ __forceinline__ Runs runs_of(const TileMeta& m, int nb) {
+  Runs r;
+  r.kstart = __builtin_amdgcn_readfirstlane(m.ko);
+  r.vstart = __builtin_amdgcn_readfirstlane(m.vo);
+  const int last = nb * T - 1;
+  r.kn = __builtin_amdgcn_readlane(m.ko + pad8((uint32_t)__popcll(m.kb)), last) - r.kstart;
+  r.vn = __builtin_amdgcn_readlane(m.vo + pad8((uint32_t)__popcll(m.vb)), last) - r.vstart;
+  return r;
+}
+
+// 512 fp16 values (one 16-byte load per lane) per staging chunk. The
+// compressed streams are read once per call, so every HBM read of the
+// compressed path is non-temporal (measured faster on gfx950 than cached loads).
+template <int STAGE>
+__device__ __forceinline__ void stage_issue(u32x4 (&r)[STAGE], const uint16_t* kv, const uint16_t* vv,
+                                            const uint16_t* safe, const Runs& rn, uint32_t lane) {
+  // Every chunk is loaded unconditionally (no divergent writes to r); lanes past
+  // the end of their run read 16 harmless bytes at `safe` and never commit them.
+  const uint32_t nck = (rn.kn + 511) / 512;
+#pragma unroll
+  for (int c = 0; c < STAGE; ++c) {
+    const bool is_k = (uint32_t)c < nck;
+    const uint32_t off = 512u * (is_k ? (uint32_t)c : (uint32_t)c - nck) + 8u * lane;
+    const uint32_t n = is_k ? rn.kn : rn.vn;
+    const uint16_t* src = (is_k ? kv + rn.kstart : vv + rn.vstart) + off;
+    r[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(off < n ? src : safe));
+  }
+}
+
+template <int STAGE>
+__device__ __forceinline__ void stage_commit(const u32x4 (&r)[STAGE], uint16_t* kst, uint16_t* vst,
+                                             const Runs& rn, uint32_t lane) {
+  const uint32_t nck = (rn.kn + 511) / 512;
+#pragma unroll
+  for (int c = 0; c < STAGE; ++c) {
+    const bool is_k = (uint32_t)c < nck;
+    const uint32_t off = 512u * (is_k ? (uint32_t)c : (uint32_t)c - nck) + 8u * lane;
+    const uint32_t n = is_k ? rn.kn : rn.vn;
+    uint16_t* dst = is_k ? kst : vst;
+    if (off < n) *reinterpret_cast<u32x4*>(dst + off) = r[c];
+  }
+  // kMargin zero values after each run: the walks read whole groups of 8 up to
+  // 72 values past the start of a tile (at most 4 groups of the lower half and
+  // 5 of the upper half, which starts at most 32 values in), and the products of
+  // those values with the zero q slot must stay 0.
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  constexpr uint32_t kz = kMargin / 8;
+  if (lane < kz) *reinterpret_cast<u32x4*>(kst + rn.kn + 8 * lane) = z;
+  else if (lane < 2 * kz) *reinterpret_cast<u32x4*>(vst + rn.vn + 8 * (lane - kz)) = z;
+}
+
+// The packed values of a tile start 16-byte aligned in LDS (tiles are padded to
+// 8 values), so the walks read them 8 at a time with one 16-byte LDS load and
+// pair slot u of the group with the next set bit of the 32-bit half word x.
+// Channel -1 (no bit left) addresses the zero slot of the q table and the
+// scratch slot of the expanded tile, so the walk has no per-element branch.
+//
+// The values of the upper half start at rank s = popcount(low half), which is
+// aligned only when s % 8 == 0. Its first group is read from the aligned
+// position below and its first s % 8 slots (values of the lower half, already
+// consumed) are phantom: they take channel -1 and consume no bit. Every later
+// group is aligned again.
+__device__ __forceinline__ _Float16 group_value(const u32x4& w, int u) {
+  const half2_t h = as_h2(w[u >> 1]);
+  return (u & 1) ? h.y : h.x;
+}
+
+template <bool PEEL>
+__device__ __forceinline__ uint32_t next_channel(uint32_t& x, int u, uint32_t m) {
+  if constexpr (PEEL) {
+    const uint32_t f = ffbl(x);  // evaluated unconditionally: no branch around the asm
+    const bool real = (uint32_t)u >= m;
+    x &= x - (real ? 1u : 0u);
+    return real ? f : 0xffffffffu;
+  } else {
+    const uint32_t c = ffbl(x);
+    x &= x - 1u;
+    return c;
+  }
+}
+
+struct ValueGroup {
+  u32x4 w;
+  uint32_t c[8];
+};
+
+template <bool PEEL>
+__device__ __forceinline__ void value_issue(uint32_t& x, uint32_t va, uint32_t m, ValueGroup& g) {
+  g.w = lds_load<u32x4>(va);
+#pragma unroll
+  for (int u = 0; u < 8; ++u) g.c[u] = next_channel<PEEL>(x, u, m);
+}
+
+// Channel c of the expanded tile is at byte daddr + c * STRIDE.
+template <uint32_t STRIDE>
+__device__ __forceinline__ void value_consume(const ValueGroup& g, uint32_t daddr) {
+#pragma unroll
+  for (int u = 0; u < 8; ++u) lds_store<_Float16>(daddr + g.c[u] * STRIDE, group_value(g.w, u));
+}
+
+// One 32-channel half of a value tile, scattered into the expanded tile
+// (pipelined like key_half).
+template <bool PEEL, uint32_t STRIDE>
+__device__ __forceinline__ void value_half(uint32_t x, uint32_t a, uint32_t daddr, uint32_t m) {
+  const int n = wave_max_int((int)(m + (uint32_t)__popc(x) + 7u) >> 3);
+  if (n == 0) return;
+  ValueGroup g0, g1;
+  value_issue<PEEL>(x, a, m, g0);
+  int g = 1;
+  for (; g + 1 < n; g += 2) {
+    value_issue<false>(x, a + 16u * g, 0u, g1);
+    value_consume<STRIDE>(g0, daddr);
+    value_issue<false>(x, a + 16u * (g + 1), 0u, g0);
+    value_consume<STRIDE>(g1, daddr);
+  }
+  if (g < n) {
+    value_issue<false>(x, a + 16u * g, 0u, g1);
+    value_consume<STRIDE>(g0, daddr);
+    value_consume<STRIDE>(g1, daddr);
+  } else {
+    value_consume<STRIDE>(g0, daddr);
+  }
+}
+
+template <int T, int G>
+__device__ __forceinline__ void write_partial(const AttnArgs& a, int seg, int bh, const float (&m_run)[G],
+                                              const float (&l_run)[G], const float (&o)[G][T]) {
+  constexpr int d = kTile * T;
+  const uint32_t lane = lane_id();
+  const int64_t row0 = (int64_t)seg * a.BHq + (int64_t)bh * G;
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    if (lane == 0) a.ws_ml[row0 + g] = make_float2(m_run[g], l_run[g]);
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) a.ws_o[(row0 + g) * d + lane + kTile * tt] = o[g][tt];
+  }
+}
+
+template <int T, int G>
+__device__ __forceinline__ void init_state(float (&m_run)[G], float (&l_run)[G], float (&o)[G][T]) {
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m_run[g] = -INFINITY;
+    l_run[g] = 0.f;
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) o[g][tt] = 0.f;
+  }
+}
+
+inline size_t dense_lds_bytes(int T, int G) {
+  const int d = kTile * T, NB = kWave / T;
+  return (size_t)G * d * 2 + (size_t)NB * G * 4;
+}
+
+inline int token_max_elems_dev(int d, int k) {
+  const int T = d / kTile;
+  const int nonempty = k < T ? k : T;
+  const int m = (k + (kPad - 1) * nonempty) / kPad * kPad;
+  return m < d ? m : d;
+}
+
+// The MFMA kernel for grouped queries (attention_mfma.hip; G in {2, 4, 8}); the
+// sparse call uses it from kMfmaMinGroup query heads per kv-head on.
+constexpr int kMfmaMinGroup = 2;
+hipError_t launch_sparse_mfma(const AttnShape& sh, const AttnArgs& a, hipStream_t s);
+
+}  // namespace mf

@@ -52,8 +52,16 @@ struct AttnShape {
   float scale_log2;  // score scale times log2(e)
 };
 
+// Split-K merge in two levels when a single level would run on too few
+// workgroups (many segments, few query heads): the number of first-level parts
+// of 32 segments, or 1 for a single-level merge.
+inline int merge_parts(int64_t n_seg, int64_t BHq) {
+  return (n_seg > 64 && BHq < 256) ? (int)((n_seg + 31) / 32) : 1;
+}
+
 // Partial results of every segment into ws_ml [n_seg][BHq] (max, sum) and
-// ws_o [n_seg][BHq][d], then the merge into out [BHq][d] fp16.
+// ws_o [n_seg][BHq][d], then the merge into out [BHq][d] fp16 (a two-level merge
+// uses [parts][BHq] (max, sum) and [parts][BHq][d] after ws_o).
 hipError_t launch_attention(const AttnShape& sh, const uint16_t* q, const SparseSide& K,
                             const SparseSide& V, const uint16_t* kd, const uint16_t* vd,
                             float* ws_ml, float* ws_o, uint16_t* out, hipStream_t s);
