@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--splits", type=int, default=0, help="split-K segments (0: library default)")
     ap.add_argument("--seed", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-streams", type=int, default=48)
+    ap.add_argument("--cpu-sample-streams", type=int, default=256)
     ap.add_argument("--cpu-threads", type=int, default=0, help="0: min(16, cpu count)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy three times (scales HBM byte counters)")
