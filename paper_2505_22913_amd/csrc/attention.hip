@@ -30,99 +30,75 @@ namespace mf {
 // step (the products, or the scatter into the expanded tile), and the loop
 // issues group g+1 before consuming group g, so each group's LDS round trip
 // overlaps the previous group's arithmetic. Two register sets alternate.
-template <int G> struct QVal { u32x2 v[G / 4]; };  // q of G heads at one channel (G >= 4)
-template <> struct QVal<1> { _Float16 v; };
-template <> struct QVal<2> { half2_t v; };
-
-template <int G>
+//
+// Keys: slots pair up, so one v_dot2 (fp16 pairs, fp32 accumulation) takes two
+// products; the two q values of a pair are loaded into the halves of one register.
 struct KeyGroup {
   u32x4 w;
-  QVal<G> q[8];
+  half2_t q[4];
 };
 
-template <int G, bool PEEL>
+template <bool PEEL>
 __device__ __forceinline__ void key_issue(uint32_t& x, uint32_t va, uint32_t qaddr, uint32_t m,
-                                          KeyGroup<G>& k) {
+                                          KeyGroup& k) {
   k.w = lds_load<u32x4>(va);
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const uint32_t qa = qaddr + next_channel<PEEL>(x, u, m) * (2u * G);
-    if constexpr (G == 1) {
-      k.q[u].v = lds_load<_Float16>(qa);
-    } else if constexpr (G == 2) {
-      k.q[u].v = lds_load<half2_t>(qa);
-    } else {
-#pragma unroll
-      for (int g4 = 0; g4 < G / 4; ++g4) k.q[u].v[g4] = lds_load<u32x2>(qa + 8u * g4);
-    }
+  for (int u = 0; u < 8; u += 2) {
+    const uint32_t c0 = next_bit<PEEL>(x, u, m);
+    const uint32_t c1 = next_bit<PEEL>(x, u + 1, m);
+    half2_t q;
+    q.x = lds_load<_Float16>(qaddr + 2u * c0);
+    q.y = lds_load<_Float16>(qaddr + 2u * c1);
+    k.q[u / 2] = q;
   }
 }
 
-template <int G>
-__device__ __forceinline__ void key_consume(const KeyGroup<G>& k, float (&acc)[G]) {
-#pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const float v = (float)group_value(k.w, u);
-    if constexpr (G == 1) {
-      acc[0] = fmaf((float)k.q[u].v, v, acc[0]);
-    } else if constexpr (G == 2) {
-      acc[0] = fmaf((float)k.q[u].v.x, v, acc[0]);
-      acc[1] = fmaf((float)k.q[u].v.y, v, acc[1]);
-    } else {
-#pragma unroll
-      for (int g4 = 0; g4 < G / 4; ++g4) {
-        const half2_t q01 = as_h2(k.q[u].v[g4].x);
-        const half2_t q23 = as_h2(k.q[u].v[g4].y);
-        acc[4 * g4 + 0] = fmaf((float)q01.x, v, acc[4 * g4 + 0]);
-        acc[4 * g4 + 1] = fmaf((float)q01.y, v, acc[4 * g4 + 1]);
-        acc[4 * g4 + 2] = fmaf((float)q23.x, v, acc[4 * g4 + 2]);
-        acc[4 * g4 + 3] = fmaf((float)q23.y, v, acc[4 * g4 + 3]);
-      }
-    }
-  }
+__device__ __forceinline__ void key_consume(const KeyGroup& k, float& acc) {
+  acc = __builtin_amdgcn_fdot2(as_h2(k.w.x), k.q[0], acc, false);
+  acc = __builtin_amdgcn_fdot2(as_h2(k.w.y), k.q[1], acc, false);
+  acc = __builtin_amdgcn_fdot2(as_h2(k.w.z), k.q[2], acc, false);
+  acc = __builtin_amdgcn_fdot2(as_h2(k.w.w), k.q[3], acc, false);
 }
 
-// One 32-channel half of a key tile: n groups of 8 from byte address a (n is the
-// busiest lane's count, so the loop is uniform and every iteration issues the
-// next group before consuming the current one); the first group has m phantom
-// slots when PEEL.
-template <int G, bool PEEL>
-__device__ __forceinline__ void key_half(uint32_t x, uint32_t a, uint32_t qaddr, uint32_t m,
-                                         float (&acc)[G]) {
-  const int n = wave_max_int((int)(m + (uint32_t)__popc(x) + 7u) >> 3);
+// One 32-channel half of a key tile (bit 31 left out, see next_bit): n groups of
+// 8 from byte address a (n is the busiest lane's count, so the loop is uniform
+// and every iteration issues the next group before consuming the current one);
+// the first group has m phantom slots when PEEL.
+template <bool PEEL>
+__device__ __forceinline__ void key_half(int n, uint32_t x, uint32_t a, uint32_t qaddr, uint32_t m,
+                                         float& acc) {
   if (n == 0) return;
-  KeyGroup<G> k0, k1;
-  key_issue<G, PEEL>(x, a, qaddr, m, k0);
+  KeyGroup k0, k1;
+  key_issue<PEEL>(x, a, qaddr, m, k0);
   int g = 1;
   for (; g + 1 < n; g += 2) {
-    key_issue<G, false>(x, a + 16u * g, qaddr, 0u, k1);
-    key_consume<G>(k0, acc);
-    key_issue<G, false>(x, a + 16u * (g + 1), qaddr, 0u, k0);
-    key_consume<G>(k1, acc);
+    key_issue<false>(x, a + 16u * g, qaddr, 0u, k1);
+    key_consume(k0, acc);
+    key_issue<false>(x, a + 16u * (g + 1), qaddr, 0u, k0);
+    key_consume(k1, acc);
   }
   if (g < n) {
-    key_issue<G, false>(x, a + 16u * g, qaddr, 0u, k1);
-    key_consume<G>(k0, acc);
-    key_consume<G>(k1, acc);
+    key_issue<false>(x, a + 16u * g, qaddr, 0u, k1);
+    key_consume(k0, acc);
+    key_consume(k1, acc);
   } else {
-    key_consume<G>(k0, acc);
+    key_consume(k0, acc);
   }
 }
 
-// Scores of one tile: q . k over its 64-bit bitmap `bm`, values at LDS byte address `va`.
-template <int G>
-__device__ __forceinline__ void key_walk(uint64_t bm, uint32_t va, uint32_t q_w0, uint32_t q_w1,
-                                         float (&acc)[G]) {
-  const uint32_t lo = (uint32_t)bm, s = (uint32_t)__popc(lo), m = s & 7u;
-  key_half<G, false>(lo, va, q_w0, 0u, acc);
-  key_half<G, true>((uint32_t)(bm >> 32), va + 2u * (s - m), q_w1, m, acc);
-}
-
-// Expansion of one value tile into the dense tile.
-__device__ __forceinline__ void value_walk(uint64_t bm, uint32_t va, uint32_t d_w0, uint32_t d_w1) {
-  const uint32_t lo = (uint32_t)bm, s = (uint32_t)__popc(lo), m = s & 7u;
-  value_half<false, 4u>(lo, va, d_w0, 0u);
-  value_half<true, 4u>((uint32_t)(bm >> 32), va + 2u * (s - m), d_w1, m);
+// Scores of one tile: q . k over its 64-bit bitmap `bm`, values at LDS byte
+// address `va`. Channels 31 and 63 (bit 31 of each half) are added here from
+// their ranks s - 1 and c - 1; q31 and q63 are this tile's q at those channels.
+__device__ __forceinline__ void key_walk(int nlo, int nhi, uint64_t bm, uint32_t va, uint32_t q_w0,
+                                         uint32_t q_w1, _Float16 q31, _Float16 q63, float& acc) {
+  const uint32_t lo = (uint32_t)bm, hi = (uint32_t)(bm >> 32);
+  const uint32_t s = (uint32_t)__popc(lo), c = s + (uint32_t)__popc(hi), m = s & 7u;
+  const _Float16 v31 = lds_load<_Float16>(va + 2u * s - 2u);
+  const _Float16 v63 = lds_load<_Float16>(va + 2u * c - 2u);
+  key_half<false>(nlo, lo & kLow31, va, q_w0, 0u, acc);
+  key_half<true>(nhi, hi & kLow31, va + 2u * (s - m), q_w1, m, acc);
+  acc = fmaf((int)lo < 0 ? (float)q31 : 0.f, (float)v31, acc);
+  acc = fmaf((int)hi < 0 ? (float)q63 : 0.f, (float)v63, acc);
 }
 
 // LDS layout of the compressed body (byte offsets). The expanded value tile
@@ -134,14 +110,21 @@ struct SparseLds {
   uint32_t qtab, ps, dense, kst, vst, total;
 };
 
+// Bytes per tile of the q table. With one head the tiles sit 16 banks apart,
+// so the lanes of the two tiles of d = 128 read disjoint banks (but for the
+// scratch and boundary slots) in one key-walk load.
+__host__ __device__ constexpr uint32_t qtab_stride(int G) {
+  return G == 1 ? 192u : ((uint32_t)(kSlots * G * 2) + 15u) & ~15u;
+}
+
 __host__ __device__ inline SparseLds sparse_lds_layout(int T, int G, int kmaxK, int kmaxV) {
   const int NB = kWave / T;
   SparseLds L;
   uint32_t o = 0;
-  L.qtab = o;  o += ((T * kSlots * G * 2) + 15) & ~15;          // [t][slot][g] fp16
+  L.qtab = o;  o += T * qtab_stride(G);                          // [t][slot][g] fp16
   L.ps = o;    o += ((NB / 2) * G * 4 + 15) & ~15;              // [pair][g] half2
-  L.vst = o;   o += ((NB * kmaxV + kMargin) * 2 + 15) & ~15;
-  const uint32_t kst_bytes = ((NB * kmaxK + kMargin) * 2 + 15) & ~15;
+  L.vst = o;   o += (run_region_elems(NB * kmaxV) * 2 + 15) & ~15u;
+  const uint32_t kst_bytes = (run_region_elems(NB * kmaxK) * 2 + 15) & ~15u;
   const uint32_t dense_bytes = (NB / 2) * T * kSlots * 4;      // [pair][t][slot][2] fp16
   L.kst = o;
   L.dense = o;
@@ -158,19 +141,20 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   constexpr int NB = kWave / T;
   const SparseLds L = sparse_lds_layout(T, G, a.kmaxK, a.kmaxV);
   const uint32_t base = lds_addr(smem);
-  uint16_t* kst = reinterpret_cast<uint16_t*>(smem + L.kst);
-  uint16_t* vst = reinterpret_cast<uint16_t*>(smem + L.vst);
   const uint32_t lane = lane_id();
   const uint32_t j = lane / T, t = lane % T;
 
   // q table with zero scratch slots: [t][slot][g].
   {
     const uint16_t* qsrc = a.q + (int64_t)bh * G * d;
-    uint16_t* qt = reinterpret_cast<uint16_t*>(smem + L.qtab);
+    // Slot 0 and 33 are the scratch slots; channels 31 and 63 read zero in
+    // the walks (their products are added once per tile).
     for (int i = lane; i < T * kSlots * G; i += kWave) {
       const int g = i % G, slot = (i / G) % kSlots, tt = i / (G * kSlots);
       const int c = slot < 33 ? slot - 1 : slot - 2;
-      qt[i] = (slot == 0 || slot == 33) ? (uint16_t)0 : qsrc[g * d + kTile * tt + c];
+      const bool zero = slot == 0 || slot == 33 || c == 31 || c == 63;
+      uint16_t* qt = reinterpret_cast<uint16_t*>(smem + L.qtab + tt * qtab_stride(G));
+      qt[slot * G + g] = zero ? (uint16_t)0 : qsrc[g * d + kTile * tt + c];
     }
   }
 
@@ -186,18 +170,22 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   TileMeta cur = load_meta<T>(a, kt0, vt0, j0, nb, lane);
   Runs rcur = runs_of<T>(cur, nb);
   u32x4 stg[STAGE];
-  stage_issue<STAGE>(stg, kv, vv, a.K.values, rcur, lane);
+  stage_issue<STAGE>(stg, kv, vv, rcur, lane);
   int nb_next = min(NB, j1 - (j0 + NB));
   TileMeta nxt = {0ull, 0ull, 0u, 0u};
   if (nb_next > 0) nxt = load_meta<T>(a, kt0, vt0, j0 + NB, nb_next, lane);
-  stage_commit<STAGE>(stg, kst, vst, rcur, lane);
+  stage_commit<STAGE>(stg, base + L.kst, base + L.vst, rcur, lane);
 
   // Per-lane constant addresses.
-  const uint32_t q_w0 = base + L.qtab + (uint32_t)((t * kSlots + 1) * G * 2);
+  const uint32_t q_w0 = base + L.qtab + t * qtab_stride(G) + (uint32_t)(G * 2);
   const uint32_t q_w1 = q_w0 + 33u * G * 2;
+  const uint16_t* qrow = a.q + (int64_t)bh * G * d + kTile * t;
+  const _Float16 q31 = __builtin_bit_cast(_Float16, qrow[31]);
+  const _Float16 q63 = __builtin_bit_cast(_Float16, qrow[63]);
   const uint32_t d_w0 = base + L.dense + (uint32_t)((((j >> 1) * T + t) * kSlots + 1) * 4 + (j & 1) * 2);
   const uint32_t d_w1 = d_w0 + 33u * 4;
   const uint32_t pv_slot = lane < 32 ? 1 + lane : 2 + lane;  // PV: lane = channel of each tile
+  const uint32_t pv_addr = base + L.dense + pv_slot * 4u;
 
   for (int b0 = j0; b0 < j1; b0 += NB) {
     // Software pipeline: fetch the next block's values and the metadata after it.
@@ -206,16 +194,17 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
     TileMeta nxt2 = {0ull, 0ull, 0u, 0u};
     const int nb_next2 = min(NB, j1 - (b0 + 2 * NB));
     if (has_next) rnext = runs_of<T>(nxt, nb_next);
-    stage_issue<STAGE>(stg, kv, vv, a.K.values, rnext, lane);
+    stage_issue<STAGE>(stg, kv, vv, rnext, lane);
     if (nb_next2 > 0) nxt2 = load_meta<T>(a, kt0, vt0, b0 + 2 * NB, nb_next2, lane);
 
     // Scores.
+    const WalkCounts wc = walk_counts(cur.kb, cur.vb);
     float acc[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g] = 0.f;
     {
       const uint32_t va = base + L.kst + ((int)j < nb ? 2u * (cur.ko - rcur.kstart) : 0u);
-      key_walk<G>(cur.kb, va, q_w0, q_w1, acc);
+      key_walk(wc.klo, wc.khi, cur.kb, va, q_w0, q_w1, q31, q63, acc[0]);
     }
     const bool valid = (int)j < nb;
 #pragma unroll
@@ -243,7 +232,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
     // Expand the value tiles.
     {
       const uint32_t va = base + L.vst + ((int)j < nb ? 2u * (cur.vo - rcur.vstart) : 0u);
-      value_walk(cur.vb, va, d_w0, d_w1);
+      expand_tile<4u>(wc.vlo, wc.vhi, cur.vb, va, d_w0, d_w1);
     }
 
     // p.V over every token pair of the block (tokens past its end have p = 0
@@ -253,20 +242,22 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
     constexpr int PB = G >= 4 ? 4 : 8;
 #pragma unroll 1
     for (int pb = 0; pb < NP; pb += PB) {
+      // Byte addresses of this batch; the per-pair steps are immediate offsets.
+      const uint32_t pa = base + L.ps + (uint32_t)(pb * G * 4);
+      const uint32_t da = pv_addr + (uint32_t)(pb * T * kSlots * 4);
       half2_t p2[PB][G], v2[PB][T];
 #pragma unroll
       for (int i = 0; i < PB; ++i) {
-        const int pr = pb + i;
         if constexpr (G == 1) {
-          p2[i][0] = lds_load<half2_t>(base + L.ps + pr * 4);
+          p2[i][0] = lds_load<half2_t>(pa + i * 4);
         } else if constexpr (G == 2) {
-          const u32x2 w = lds_load<u32x2>(base + L.ps + pr * 8);
+          const u32x2 w = lds_load<u32x2>(pa + i * 8);
           p2[i][0] = as_h2(w.x);
           p2[i][1] = as_h2(w.y);
         } else {
 #pragma unroll
           for (int g4 = 0; g4 < G; g4 += 4) {
-            const u32x4 w = lds_load<u32x4>(base + L.ps + (pr * G + g4) * 4);
+            const u32x4 w = lds_load<u32x4>(pa + (i * G + g4) * 4);
             p2[i][g4 + 0] = as_h2(w.x);
             p2[i][g4 + 1] = as_h2(w.y);
             p2[i][g4 + 2] = as_h2(w.z);
@@ -275,7 +266,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
         }
 #pragma unroll
         for (int tt = 0; tt < T; ++tt)
-          v2[i][tt] = lds_load<half2_t>(base + L.dense + ((pr * T + tt) * kSlots + pv_slot) * 4);
+          v2[i][tt] = lds_load<half2_t>(da + (uint32_t)((i * T + tt) * kSlots * 4));
       }
 #pragma unroll
       for (int i = 0; i < PB; ++i)
@@ -286,7 +277,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
     }
 
     if (has_next) {
-      stage_commit<STAGE>(stg, kst, vst, rnext, lane);
+      stage_commit<STAGE>(stg, base + L.kst, base + L.vst, rnext, lane);
       cur = nxt;
       rcur = rnext;
       nxt = nxt2;
@@ -303,10 +294,14 @@ __global__ __launch_bounds__(64) void k_sparse_attn(AttnArgs a) {
   const int seg = blockIdx.x, bh = blockIdx.y;
   float m_run[G], l_run[G], o[G][T];
   init_state<T, G>(m_run, l_run, o);
-  if (seg < a.n_sparse_segs)
-    sparse_body<T, G, STAGE>(a, seg, bh, smem, m_run, l_run, o);
-  else
+  // With G >= 2 the compressed segments run on the MFMA kernel; this one then
+  // only serves the window of a call whose compressed cache is empty.
+  if constexpr (G == 1) {
+    if (seg < a.n_sparse_segs) sparse_body<T, G, STAGE>(a, seg, bh, smem, m_run, l_run, o);
+    else dense_body<T, G>(a, seg - a.n_sparse_segs, bh, smem, m_run, l_run, o);
+  } else {
     dense_body<T, G>(a, seg - a.n_sparse_segs, bh, smem, m_run, l_run, o);
+  }
   write_partial<T, G>(a, seg, bh, m_run, l_run, o);
 }
 
@@ -430,7 +425,8 @@ static hipError_t attention_TG(const AttnShape& sh, const AttnArgs& a, uint16_t*
   hipError_t e;
   if (sh.n_sparse_segs > 0) {
     // Grouped queries contract on the matrix cores (attention_mfma.hip).
-    e = G >= kMfmaMinGroup ? launch_sparse_mfma(sh, a, s) : sparse_stage<T, G>(sh, a, s);
+    if constexpr (G >= kMfmaMinGroup) e = launch_sparse_mfma(sh, a, s);
+    else e = sparse_stage<T, G>(sh, a, s);
   } else if (sh.n_s == 0 && sh.n_dense_segs > 0 && a.K.bitmaps != nullptr) {
     // Sparse call with an empty compressed cache: only the window segment.
     e = sparse_launch<T, G, 4>(sh, a, s);

@@ -53,10 +53,10 @@ __host__ __device__ inline MfmaLds mfma_lds_layout(int kmaxK, int kmaxV) {
   MfmaLds L;
   uint32_t o = 0;
   L.vst = o;
-  o += ((Geo::NB * kmaxV + kMargin) * 2 + 15) & ~15u;
+  o += (run_region_elems(Geo::NB * kmaxV) * 2 + 15) & ~15u;
   L.kst = o;
   L.vdt = o;
-  const uint32_t kst_bytes = ((Geo::NB * kmaxK + kMargin) * 2 + 15) & ~15u;
+  const uint32_t kst_bytes = (run_region_elems(Geo::NB * kmaxK) * 2 + 15) & ~15u;
   L.kd = o + kst_bytes;
   const uint32_t a = kst_bytes + Geo::NB * Geo::KD_ROW;
   const uint32_t b = T * kMSlots * Geo::VD_ROW;
@@ -78,8 +78,6 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
   constexpr int NB = Geo::NB, NG = Geo::NG, NC = Geo::NC;
   const MfmaLds L = mfma_lds_layout<T>(a.kmaxK, a.kmaxV);
   const uint32_t base = lds_addr(smem);
-  uint16_t* kst = reinterpret_cast<uint16_t*>(smem + L.kst);
-  uint16_t* vst = reinterpret_cast<uint16_t*>(smem + L.vst);
   const uint32_t lane = lane_id();
   const uint32_t j = lane / T, t = lane % T;       // walk layout: token j, tile t
   const uint32_t r16 = lane % 16, q4 = lane / 16;  // MFMA layout: column, row quad
@@ -110,11 +108,11 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
   TileMeta cur = load_meta<T>(a, kt0, vt0, j0, nb, lane);
   Runs rcur = runs_of<T>(cur, nb);
   u32x4 stg[STAGE];
-  stage_issue<STAGE>(stg, kv, vv, a.K.values, rcur, lane);
+  stage_issue<STAGE>(stg, kv, vv, rcur, lane);
   int nb_next = min(NB, j1 - (j0 + NB));
   TileMeta nxt = {0ull, 0ull, 0u, 0u};
   if (nb_next > 0) nxt = load_meta<T>(a, kt0, vt0, j0 + NB, nb_next, lane);
-  stage_commit<STAGE>(stg, kst, vst, rcur, lane);
+  stage_commit<STAGE>(stg, base + L.kst, base + L.vst, rcur, lane);
 
   // Walk destinations: channel c of half h of this lane's tile.
   const uint32_t kd_w0 = base + L.kd + j * Geo::KD_ROW + (t * kMSlots + 4u) * 2u;
@@ -128,16 +126,15 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
     TileMeta nxt2 = {0ull, 0ull, 0u, 0u};
     const int nb_next2 = min(NB, j1 - (b0 + 2 * NB));
     if (has_next) rnext = runs_of<T>(nxt, nb_next);
-    stage_issue<STAGE>(stg, kv, vv, a.K.values, rnext, lane);
+    stage_issue<STAGE>(stg, kv, vv, rnext, lane);
     if (nb_next2 > 0) nxt2 = load_meta<T>(a, kt0, vt0, b0 + 2 * NB, nb_next2, lane);
 
     // Expand the keys (tokens past the block end have empty bitmaps).
+    const WalkCounts wc = walk_counts(cur.kb, cur.vb);
     lds_zero(base + L.kd, NB * Geo::KD_ROW, lane);
     {
       const uint32_t va = base + L.kst + ((int)j < nb ? 2u * (cur.ko - rcur.kstart) : 0u);
-      const uint32_t lo = (uint32_t)cur.kb, s = (uint32_t)__popc(lo), m = s & 7u;
-      value_half<false, 2u>(lo, va, kd_w0, 0u);
-      value_half<true, 2u>((uint32_t)(cur.kb >> 32), va + 2u * (s - m), kd_w1, m);
+      expand_tile<2u>(wc.klo, wc.khi, cur.kb, va, kd_w0, kd_w1);
     }
 
     // Scores: S[group g][token 4 q4 + e][head r16].
@@ -191,9 +188,7 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
     lds_zero(base + L.vdt, T * kMSlots * Geo::VD_ROW, lane);
     {
       const uint32_t va = base + L.vst + ((int)j < nb ? 2u * (cur.vo - rcur.vstart) : 0u);
-      const uint32_t lo = (uint32_t)cur.vb, s = (uint32_t)__popc(lo), m = s & 7u;
-      value_half<false, Geo::VD_ROW>(lo, va, vd_w0, 0u);
-      value_half<true, Geo::VD_ROW>((uint32_t)(cur.vb >> 32), va + 2u * (s - m), vd_w1, m);
+      expand_tile<Geo::VD_ROW>(wc.vlo, wc.vhi, cur.vb, va, vd_w0, vd_w1);
     }
 
     // Rescale the accumulators: row 4 q4 + e of every O tile is head 4 q4 + e.
@@ -226,7 +221,7 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
     }
 
     if (has_next) {
-      stage_commit<STAGE>(stg, kst, vst, rnext, lane);
+      stage_commit<STAGE>(stg, base + L.kst, base + L.vst, rnext, lane);
       cur = nxt;
       rcur = rnext;
       nxt = nxt2;

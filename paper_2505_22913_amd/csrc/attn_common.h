@@ -80,21 +80,6 @@ __device__ __forceinline__ float wave_sum_u(float v) {
   return readlane_f(v, 0) + readlane_f(v, 32);
 }
 
-// Maximum over all 64 lanes of a non-negative int, returned wave-uniform.
-template <int CTRL>
-__device__ __forceinline__ int dppi(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
-}
-
-__device__ __forceinline__ int wave_max_int(int v) {
-  v = max(v, dppi<0xB1>(v));
-  v = max(v, dppi<0x4E>(v));
-  v = max(v, dppi<0x124>(v));
-  v = max(v, dppi<0x128>(v));
-  v = max(v, __builtin_amdgcn_ds_swizzle(v, 0x401F));
-  return max(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 32));
-}
-
 // Sum over the T lanes (adjacent, T in {1,2,4}) that hold the tiles of one token.
 template <int T>
 __device__ __forceinline__ float tile_sum(float v) {
@@ -228,52 +213,112 @@ __device__ __forceinline__ Runs runs_of(const TileMeta& m, int nb) {
   return r;
 }
 
-// 512 fp16 values (one 16-byte load per lane) per staging chunk. The
-// compressed streams are read once per call, so every HBM read of the
-// compressed path is non-temporal (measured faster on gfx950 than cached loads).
+// Staging chunks: 512 fp16 values, one 16-byte load per lane. A run of n
+// values needs ceil(n / 512) chunks; its LDS region holds whole chunks.
+constexpr uint32_t kChunk = 512;
+
+__host__ __device__ inline uint32_t run_region_elems(uint32_t max_run) {
+  const uint32_t whole = (max_run + kChunk - 1) / kChunk * kChunk;
+  const uint32_t need = max_run + kMargin;
+  return whole > need ? whole : need;
+}
+
+// Raw buffer descriptor (gfx9 word 3) over `elems` fp16 values at p: a load
+// past the end returns zeros and reads no memory.
+// The arguments are wave-uniform; readfirstlane states it, so the descriptor
+// stays in scalar registers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t run_rsrc(const uint16_t* p, uint32_t elems) {
+  const uint64_t a = (uint64_t)(uintptr_t)p;
+  const uint64_t u = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(a >> 32)) << 32) |
+                     (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  const int bytes = __builtin_amdgcn_readfirstlane((int)(elems * 2u));
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(u), (short)0, bytes, 0x00020000);
+}
+
+constexpr int kLoadNT = 2;  // non-temporal: the compressed streams are read once per call
+
+// Chunk c of the block's key run, then of its value run. Every chunk is loaded
+// (no divergent register writes); the descriptors bound each run, so the lanes
+// past its end get zeros.
 template <int STAGE>
 __device__ __forceinline__ void stage_issue(u32x4 (&r)[STAGE], const uint16_t* kv, const uint16_t* vv,
-                                            const uint16_t* safe, const Runs& rn, uint32_t lane) {
-  // Every chunk is loaded unconditionally (no divergent writes to r); lanes past
-  // the end of their run read 16 harmless bytes at `safe` and never commit them.
-  const uint32_t nck = (rn.kn + 511) / 512;
+                                            const Runs& rn, uint32_t lane) {
+  const uint32_t nck = (rn.kn + kChunk - 1) / kChunk;
 #pragma unroll
   for (int c = 0; c < STAGE; ++c) {
     const bool is_k = (uint32_t)c < nck;
-    const uint32_t off = 512u * (is_k ? (uint32_t)c : (uint32_t)c - nck) + 8u * lane;
+    const uint32_t first = kChunk * (is_k ? (uint32_t)c : (uint32_t)c - nck);
     const uint32_t n = is_k ? rn.kn : rn.vn;
-    const uint16_t* src = (is_k ? kv + rn.kstart : vv + rn.vstart) + off;
-    r[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(off < n ? src : safe));
+    const uint16_t* src = (is_k ? kv + rn.kstart : vv + rn.vstart) + first;
+    const uint32_t rest = (uint32_t)max((int)n - (int)first, 0);  // scalar max (no VALU saturation)
+    r[c] = __builtin_amdgcn_raw_buffer_load_b128(run_rsrc(src, rest), 16u * lane, 0, kLoadNT);
   }
 }
 
+// Whole chunks go to LDS (zeros past each run's end), then kMargin zeros after
+// each run: the walks read whole groups of 8 up to 72 values past the start of
+// a tile (at most 4 groups of the lower half and 5 of the upper half, which
+// starts at most 32 values in), and the products of those values with the zero
+// q slot must stay 0.
 template <int STAGE>
-__device__ __forceinline__ void stage_commit(const u32x4 (&r)[STAGE], uint16_t* kst, uint16_t* vst,
+__device__ __forceinline__ void stage_commit(const u32x4 (&r)[STAGE], uint32_t kst, uint32_t vst,
                                              const Runs& rn, uint32_t lane) {
-  const uint32_t nck = (rn.kn + 511) / 512;
+  const uint32_t nck = (rn.kn + kChunk - 1) / kChunk, nvc = (rn.vn + kChunk - 1) / kChunk;
 #pragma unroll
   for (int c = 0; c < STAGE; ++c) {
-    const bool is_k = (uint32_t)c < nck;
-    const uint32_t off = 512u * (is_k ? (uint32_t)c : (uint32_t)c - nck) + 8u * lane;
-    const uint32_t n = is_k ? rn.kn : rn.vn;
-    uint16_t* dst = is_k ? kst : vst;
-    if (off < n) *reinterpret_cast<u32x4*>(dst + off) = r[c];
+    if ((uint32_t)c < nck + nvc) {
+      const uint32_t dst = (uint32_t)c < nck ? kst + 2u * kChunk * c : vst + 2u * kChunk * (c - nck);
+      lds_store<u32x4>(dst + 16u * lane, r[c]);
+    }
   }
-  // kMargin zero values after each run: the walks read whole groups of 8 up to
-  // 72 values past the start of a tile (at most 4 groups of the lower half and
-  // 5 of the upper half, which starts at most 32 values in), and the products of
-  // those values with the zero q slot must stay 0.
   const u32x4 z = {0u, 0u, 0u, 0u};
   constexpr uint32_t kz = kMargin / 8;
-  if (lane < kz) *reinterpret_cast<u32x4*>(kst + rn.kn + 8 * lane) = z;
-  else if (lane < 2 * kz) *reinterpret_cast<u32x4*>(vst + rn.vn + 8 * (lane - kz)) = z;
+  if (lane < kz) lds_store<u32x4>(kst + 2u * rn.kn + 16u * lane, z);
+  else if (lane < 2 * kz) lds_store<u32x4>(vst + 2u * rn.vn + 16u * (lane - kz), z);
+}
+
+// Trip counts of the four walks of a block (key and value tiles, lower and
+// upper halves; groups of 8 slots, the upper half with its leading phantom
+// slots), each the maximum over the wave: one-hot in a byte per walk, one OR
+// reduction for all four.
+struct WalkCounts {
+  int klo, khi, vlo, vhi;
+};
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_or(uint32_t v) {
+  return v | (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+__device__ __forceinline__ uint32_t half_groups_onehot(uint64_t bm, int shift) {
+  const uint32_t s = (uint32_t)__popc((uint32_t)bm);
+  const uint32_t lo = (s + 7u) >> 3;
+  const uint32_t hi = ((s & 7u) + (uint32_t)__popc((uint32_t)(bm >> 32)) + 7u) >> 3;
+  return (1u << (lo + shift)) | (1u << (hi + shift + 8));
+}
+
+__device__ __forceinline__ WalkCounts walk_counts(uint64_t kb, uint64_t vb) {
+  uint32_t v = half_groups_onehot(kb, 0) | half_groups_onehot(vb, 16);
+  v = dpp_or<0xB1>(v);
+  v = dpp_or<0x4E>(v);
+  v = dpp_or<0x124>(v);
+  v = dpp_or<0x128>(v);
+  v |= (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x401F);
+  v = (uint32_t)__builtin_amdgcn_readlane((int)v, 0) | (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
+  WalkCounts w;
+  w.klo = 31 - __builtin_clz(v & 0xffu);
+  w.khi = 31 - __builtin_clz((v >> 8) & 0xffu);
+  w.vlo = 31 - __builtin_clz((v >> 16) & 0xffu);
+  w.vhi = 31 - __builtin_clz(v >> 24);
+  return w;
 }
 
 // The packed values of a tile start 16-byte aligned in LDS (tiles are padded to
 // 8 values), so the walks read them 8 at a time with one 16-byte LDS load and
 // pair slot u of the group with the next set bit of the 32-bit half word x.
-// Channel -1 (no bit left) addresses the zero slot of the q table and the
-// scratch slot of the expanded tile, so the walk has no per-element branch.
+// Channel -1 (all ones: no bit left) addresses the zero slot of the q table
+// and the scratch slot of the expanded tile, so the walk has no per-element
+// branch.
 //
 // The values of the upper half start at rank s = popcount(low half), which is
 // aligned only when s % 8 == 0. Its first group is read from the aligned
@@ -285,31 +330,10 @@ __device__ __forceinline__ _Float16 group_value(const u32x4& w, int u) {
   return (u & 1) ? h.y : h.x;
 }
 
-template <bool PEEL>
-__device__ __forceinline__ uint32_t next_channel(uint32_t& x, int u, uint32_t m) {
-  if constexpr (PEEL) {
-    const uint32_t f = ffbl(x);  // evaluated unconditionally: no branch around the asm
-    const bool real = (uint32_t)u >= m;
-    x &= x - (real ? 1u : 0u);
-    return real ? f : 0xffffffffu;
-  } else {
-    const uint32_t c = ffbl(x);
-    x &= x - 1u;
-    return c;
-  }
-}
-
 struct ValueGroup {
   u32x4 w;
   uint32_t c[8];
 };
-
-template <bool PEEL>
-__device__ __forceinline__ void value_issue(uint32_t& x, uint32_t va, uint32_t m, ValueGroup& g) {
-  g.w = lds_load<u32x4>(va);
-#pragma unroll
-  for (int u = 0; u < 8; ++u) g.c[u] = next_channel<PEEL>(x, u, m);
-}
 
 // Channel c of the expanded tile is at byte daddr + c * STRIDE.
 template <uint32_t STRIDE>
@@ -318,11 +342,40 @@ __device__ __forceinline__ void value_consume(const ValueGroup& g, uint32_t dadd
   for (int u = 0; u < 8; ++u) lds_store<_Float16>(daddr + g.c[u] * STRIDE, group_value(g.w, u));
 }
 
-// One 32-channel half of a value tile, scattered into the expanded tile
-// (pipelined like key_half).
+// Walks with a one-instruction bit clear, x += -1 << f (f = the lowest set
+// bit). Past the last set bit f alternates between -1 (all ones) and 31, so a
+// walk that runs on (the wave's busiest lane sets the trip count) sends its
+// surplus slots to the scratch slot and to channel 31 of its half. The walked
+// word therefore leaves bit 31 out: channel 31 of each half is handled once per
+// tile by the caller (for keys its q slot is zero, for values its expanded slot
+// is rewritten after the walk).
+constexpr uint32_t kLow31 = 0x7fffffffu;
+
+template <bool PEEL>
+__device__ __forceinline__ uint32_t next_bit(uint32_t& x, int u, uint32_t m) {
+  const uint32_t f = ffbl(x);
+  const uint32_t nx = x + (~0u << (f & 31u));
+  if constexpr (PEEL) {
+    const bool real = (uint32_t)u >= m;
+    x = real ? nx : x;
+    return real ? f : 0xffffffffu;
+  } else {
+    x = nx;
+    return f;
+  }
+}
+
+template <bool PEEL>
+__device__ __forceinline__ void value_issue(uint32_t& x, uint32_t va, uint32_t m, ValueGroup& g) {
+  g.w = lds_load<u32x4>(va);
+#pragma unroll
+  for (int u = 0; u < 8; ++u) g.c[u] = next_bit<PEEL>(x, u, m);
+}
+
+// One 32-channel half of a tile scattered into the expanded tile, pipelined
+// like the key walk: n groups (the wave's maximum), m phantom slots first when PEEL.
 template <bool PEEL, uint32_t STRIDE>
-__device__ __forceinline__ void value_half(uint32_t x, uint32_t a, uint32_t daddr, uint32_t m) {
-  const int n = wave_max_int((int)(m + (uint32_t)__popc(x) + 7u) >> 3);
+__device__ __forceinline__ void value_half(int n, uint32_t x, uint32_t a, uint32_t daddr, uint32_t m) {
   if (n == 0) return;
   ValueGroup g0, g1;
   value_issue<PEEL>(x, a, m, g0);
@@ -340,6 +393,23 @@ __device__ __forceinline__ void value_half(uint32_t x, uint32_t a, uint32_t dadd
   } else {
     value_consume<STRIDE>(g0, daddr);
   }
+}
+
+// Expansion of one tile (bitmap bm, packed values at LDS byte address va) into
+// an expanded tile whose channel c of half h is at byte d_h + c * STRIDE.
+// Channels 31 and 63 are written last (value, or zero when dropped), over the
+// walks' surplus writes; nlo and nhi are the wave's trip counts.
+template <uint32_t STRIDE>
+__device__ __forceinline__ void expand_tile(int nlo, int nhi, uint64_t bm, uint32_t va, uint32_t d_w0,
+                                            uint32_t d_w1) {
+  const uint32_t lo = (uint32_t)bm, hi = (uint32_t)(bm >> 32);
+  const uint32_t s = (uint32_t)__popc(lo), c = s + (uint32_t)__popc(hi), m = s & 7u;
+  const _Float16 v31 = lds_load<_Float16>(va + 2u * s - 2u);
+  const _Float16 v63 = lds_load<_Float16>(va + 2u * c - 2u);
+  value_half<false, STRIDE>(nlo, lo & kLow31, va, d_w0, 0u);
+  value_half<true, STRIDE>(nhi, hi & kLow31, va + 2u * (s - m), d_w1, m);
+  lds_store<_Float16>(d_w0 + STRIDE * 31u, (int)lo < 0 ? v31 : (_Float16)0.f);
+  lds_store<_Float16>(d_w1 + STRIDE * 31u, (int)hi < 0 ? v63 : (_Float16)0.f);
 }
 
 template <int T, int G>
