@@ -101,14 +101,23 @@ __device__ __forceinline__ void key_walk(int nlo, int nhi, uint64_t bm, uint32_t
   acc = fmaf((int)hi < 0 ? (float)q63 : 0.f, (float)v63, acc);
 }
 
-// LDS layout of the compressed body (byte offsets). The expanded value tile
-// shares its bytes with the staged keys: it is cleared after the key walk of a
-// block and read by p.V before the next block's keys are committed. A
-// workgroup is one wave, whose LDS operations execute in program order, so the
-// phases need no barrier.
+// LDS layout of the compressed body (byte offsets). Values are expanded one
+// 32-channel half at a time (both halves of every tile of the block), into a
+// channel-major half tile: row `slot` (0 = the scratch slot, 1 + c = channel c
+// of the half) holds dword t * NPT + p = tokens 2p, 2p+1 of tile t (NPT token
+// pairs per block), rows kPvRow dwords apart. The scatter's lanes write the
+// banks of their token pairs whatever their channel, and p.V reads four token
+// pairs of one channel with one 16-byte load, conflict-free across a row of
+// lanes (the row stride is 9 x 16 bytes). The half tile shares its bytes with
+// the staged keys: it is cleared after the key walk of a block and read by p.V
+// before the next block's keys are committed. A workgroup is one wave, whose
+// LDS operations execute in program order, so the phases need no barrier.
 struct SparseLds {
   uint32_t qtab, ps, dense, kst, vst, total;
 };
+
+constexpr int kHalfSlots = 33;
+constexpr uint32_t kPvRow = 36;  // dwords per half-tile row: 32 (T x NPT) + 4 pad
 
 // Bytes per tile of the q table. With one head the tiles sit 16 banks apart,
 // so the lanes of the two tiles of d = 128 read disjoint banks (but for the
@@ -117,44 +126,55 @@ __host__ __device__ constexpr uint32_t qtab_stride(int G) {
   return G == 1 ? 192u : ((uint32_t)(kSlots * G * 2) + 15u) & ~15u;
 }
 
-__host__ __device__ inline SparseLds sparse_lds_layout(int T, int G, int kmaxK, int kmaxV) {
+__host__ __device__ constexpr uint32_t half_tile_bytes(int) { return kHalfSlots * kPvRow * 4u; }
+
+__host__ __device__ inline SparseLds sparse_lds_layout(int T, int kmaxK, int kmaxV) {
   const int NB = kWave / T;
   SparseLds L;
   uint32_t o = 0;
-  L.qtab = o;  o += T * qtab_stride(G);                          // [t][slot][g] fp16
-  L.ps = o;    o += ((NB / 2) * G * 4 + 15) & ~15;              // [pair][g] half2
+  L.qtab = o;  o += T * qtab_stride(1);                          // [t][slot] fp16
+  L.ps = o;    o += ((NB / 2) * 4 + 15) & ~15;                   // [pair] half2
   L.vst = o;   o += (run_region_elems(NB * kmaxV) * 2 + 15) & ~15u;
   const uint32_t kst_bytes = (run_region_elems(NB * kmaxK) * 2 + 15) & ~15u;
-  const uint32_t dense_bytes = (NB / 2) * T * kSlots * 4;      // [pair][t][slot][2] fp16
   L.kst = o;
   L.dense = o;
-  o += kst_bytes > dense_bytes ? kst_bytes : dense_bytes;
+  o += kst_bytes > half_tile_bytes(T) ? kst_bytes : half_tile_bytes(T);
   L.total = o;
   return L;
 }
 
-template <int T, int G, int STAGE>
+// p.V work of a lane per half: (tile, channel-of-half) units. With T >= 2 the
+// 32 T units are spread over the 64 lanes (unit L + 64 k of lane L); with T = 1
+// lanes L and L + 32 share unit L % 32 and split the token pairs.
+template <int T>
+struct PvUnits {
+  static constexpr int UPL = T >= 2 ? T / 2 : 1;
+  static constexpr int NP = kWave / T / 2;                 // token pairs per block
+  static constexpr int NPL = T == 1 ? NP / 2 : NP;         // pairs per lane
+};
+
+// Compressed segment, one head per kv-head.
+template <int T, int STAGE>
 __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, unsigned char* smem,
-                                            float (&m_run)[G], float (&l_run)[G],
-                                            float (&o)[G][T]) {
+                                            float& m_run, float& l_run, float (&o)[T]) {
   constexpr int d = kTile * T;
   constexpr int NB = kWave / T;
-  const SparseLds L = sparse_lds_layout(T, G, a.kmaxK, a.kmaxV);
+  using PU = PvUnits<T>;
+  const SparseLds L = sparse_lds_layout(T, a.kmaxK, a.kmaxV);
   const uint32_t base = lds_addr(smem);
   const uint32_t lane = lane_id();
   const uint32_t j = lane / T, t = lane % T;
 
-  // q table with zero scratch slots: [t][slot][g].
+  // q table [t][slot]: slots 0 and 33 are the scratch slots; channels 31 and
+  // 63 read zero in the walks (their products are added once per tile).
   {
-    const uint16_t* qsrc = a.q + (int64_t)bh * G * d;
-    // Slot 0 and 33 are the scratch slots; channels 31 and 63 read zero in
-    // the walks (their products are added once per tile).
-    for (int i = lane; i < T * kSlots * G; i += kWave) {
-      const int g = i % G, slot = (i / G) % kSlots, tt = i / (G * kSlots);
+    const uint16_t* qsrc = a.q + (int64_t)bh * d;
+    for (int i = lane; i < T * kSlots; i += kWave) {
+      const int slot = i % kSlots, tt = i / kSlots;
       const int c = slot < 33 ? slot - 1 : slot - 2;
       const bool zero = slot == 0 || slot == 33 || c == 31 || c == 63;
-      uint16_t* qt = reinterpret_cast<uint16_t*>(smem + L.qtab + tt * qtab_stride(G));
-      qt[slot * G + g] = zero ? (uint16_t)0 : qsrc[g * d + kTile * tt + c];
+      uint16_t* qt = reinterpret_cast<uint16_t*>(smem + L.qtab + tt * qtab_stride(1));
+      qt[slot] = zero ? (uint16_t)0 : qsrc[kTile * tt + c];
     }
   }
 
@@ -176,16 +196,28 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   if (nb_next > 0) nxt = load_meta<T>(a, kt0, vt0, j0 + NB, nb_next, lane);
   stage_commit<STAGE>(stg, base + L.kst, base + L.vst, rcur, lane);
 
-  // Per-lane constant addresses.
-  const uint32_t q_w0 = base + L.qtab + t * qtab_stride(G) + (uint32_t)(G * 2);
-  const uint32_t q_w1 = q_w0 + 33u * G * 2;
-  const uint16_t* qrow = a.q + (int64_t)bh * G * d + kTile * t;
+  // Per-lane constant addresses: walks (token j, tile t) ...
+  const uint32_t q_w0 = base + L.qtab + t * qtab_stride(1) + 2u;
+  const uint32_t q_w1 = q_w0 + 33u * 2u;
+  const uint16_t* qrow = a.q + (int64_t)bh * d + kTile * t;
   const _Float16 q31 = __builtin_bit_cast(_Float16, qrow[31]);
   const _Float16 q63 = __builtin_bit_cast(_Float16, qrow[63]);
-  const uint32_t d_w0 = base + L.dense + (uint32_t)((((j >> 1) * T + t) * kSlots + 1) * 4 + (j & 1) * 2);
-  const uint32_t d_w1 = d_w0 + 33u * 4;
-  const uint32_t pv_slot = lane < 32 ? 1 + lane : 2 + lane;  // PV: lane = channel of each tile
-  const uint32_t pv_addr = base + L.dense + pv_slot * 4u;
+  constexpr uint32_t NPT = PU::NP;
+  constexpr uint32_t kRowB = kPvRow * 4u;  // expanded-tile stride per channel
+  const uint32_t d_w = base + L.dense + kRowB + (t * NPT + (j >> 1)) * 4u + (j & 1) * 2u;
+  // ... and p.V units (tile tu, channel lane % 32 of the half).
+  const uint32_t pv_pair0 = T == 1 ? (lane / 32u) * PU::NPL : 0u;
+  uint32_t pv_addr[PU::UPL];
+#pragma unroll
+  for (int k = 0; k < PU::UPL; ++k) {
+    const uint32_t tu = T == 1 ? 0u : lane / 32u + 2u * k;
+    pv_addr[k] = base + L.dense + ((1u + lane % 32u) * kPvRow + tu * NPT + pv_pair0) * 4u;
+  }
+  float oh[2][PU::UPL];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int k = 0; k < PU::UPL; ++k) oh[h][k] = 0.f;
 
   for (int b0 = j0; b0 < j1; b0 += NB) {
     // Software pipeline: fetch the next block's values and the metadata after it.
@@ -199,81 +231,72 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
 
     // Scores.
     const WalkCounts wc = walk_counts(cur.kb, cur.vb);
-    float acc[G];
-#pragma unroll
-    for (int g = 0; g < G; ++g) acc[g] = 0.f;
+    float acc = 0.f;
     {
       const uint32_t va = base + L.kst + ((int)j < nb ? 2u * (cur.ko - rcur.kstart) : 0u);
-      key_walk(wc.klo, wc.khi, cur.kb, va, q_w0, q_w1, q31, q63, acc[0]);
+      key_walk(wc.klo, wc.khi, cur.kb, va, q_w0, q_w1, q31, q63, acc);
     }
-    const bool valid = (int)j < nb;
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float sc = valid ? tile_sum<T>(acc[g]) * a.scale_log2 : -INFINITY;
-      const float mnew = fmaxf(m_run[g], wave_max_u(sc));
-      const float alpha = __builtin_amdgcn_exp2f(m_run[g] - mnew);
+    {
+      const bool valid = (int)j < nb;
+      const float sc = valid ? tile_sum<T>(acc) * a.scale_log2 : -INFINITY;
+      const float mnew = fmaxf(m_run, wave_max_u(sc));
+      const float alpha = __builtin_amdgcn_exp2f(m_run - mnew);
       const _Float16 ph = valid ? (_Float16)__builtin_amdgcn_exp2f(sc - mnew) : (_Float16)0.f;
-      l_run[g] = l_run[g] * alpha + wave_sum_u(t == 0 ? (float)ph : 0.f);
-      m_run[g] = mnew;
+      l_run = l_run * alpha + wave_sum_u(t == 0 ? (float)ph : 0.f);
+      m_run = mnew;
 #pragma unroll
-      for (int tt = 0; tt < T; ++tt) o[g][tt] *= alpha;
-      if (t == 0) lds_store<_Float16>(base + L.ps + ((j >> 1) * G + g) * 4 + (j & 1) * 2, ph);
-    }
-
-    // Clear the expanded value tile (it overwrites the staged keys, read above).
-    {
-      constexpr int n16 = (NB / 2) * T * kSlots * 4 / 16;
-      const u32x4 z = {0u, 0u, 0u, 0u};
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int i = 0; i < (n16 + kWave - 1) / kWave; ++i)
-        if (i * kWave + (int)lane < n16) lds_store<u32x4>(base + L.dense + 16u * (i * kWave + lane), z);
+        for (int k = 0; k < PU::UPL; ++k) oh[h][k] *= alpha;
+      if (t == 0) lds_store<_Float16>(base + L.ps + (j >> 1) * 4 + (j & 1) * 2, ph);
     }
 
-    // Expand the value tiles.
-    {
-      const uint32_t va = base + L.vst + ((int)j < nb ? 2u * (cur.vo - rcur.vstart) : 0u);
-      expand_tile<4u>(wc.vlo, wc.vhi, cur.vb, va, d_w0, d_w1);
-    }
-
-    // p.V over every token pair of the block (tokens past its end have p = 0
-    // and zero values), unrolled so the LDS loads of a batch are in flight
-    // together: lane = channel `lane` of every tile.
-    constexpr int NP = NB / 2;
-    constexpr int PB = G >= 4 ? 4 : 8;
+    // Values, one half of every tile at a time: clear the half tile (it
+    // overwrites the staged keys, read above), expand, p.V.
+    const uint32_t va = base + L.vst + ((int)j < nb ? 2u * (cur.vo - rcur.vstart) : 0u);
+    const uint32_t vlo = (uint32_t)cur.vb, vhi = (uint32_t)(cur.vb >> 32);
+    const uint32_t vs = (uint32_t)__popc(vlo), vm = vs & 7u;
+    const _Float16 v31 = lds_load<_Float16>(va + 2u * vs - 2u);
+    const _Float16 v63 = lds_load<_Float16>(va + 2u * (vs + (uint32_t)__popc(vhi)) - 2u);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      {
+        constexpr int n16 = (int)(half_tile_bytes(T) / 16);
+        const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int i = 0; i < (n16 + kWave - 1) / kWave; ++i)
+          if (i * kWave + (int)lane < n16) lds_store<u32x4>(base + L.dense + 16u * (i * kWave + lane), z);
+      }
+      if (h == 0) {
+        value_half<false, kRowB>(wc.vlo, vlo & kLow31, va, d_w, 0u);
+        lds_store<_Float16>(d_w + kRowB * 31u, (int)vlo < 0 ? v31 : (_Float16)0.f);
+      } else {
+        value_half<true, kRowB>(wc.vhi, vhi & kLow31, va + 2u * (vs - vm), d_w, vm);
+        lds_store<_Float16>(d_w + kRowB * 31u, (int)vhi < 0 ? v63 : (_Float16)0.f);
+      }
+      // p.V over the lane's token pairs (tokens past the block end have p = 0
+      // and zero values), four pairs per 16-byte load of p and of each unit.
+      constexpr int NQ = PU::NPL / 4;
+      constexpr int QB = NQ >= 2 ? 2 : 1;  // 16-byte loads in flight per unit
 #pragma unroll 1
-    for (int pb = 0; pb < NP; pb += PB) {
-      // Byte addresses of this batch; the per-pair steps are immediate offsets.
-      const uint32_t pa = base + L.ps + (uint32_t)(pb * G * 4);
-      const uint32_t da = pv_addr + (uint32_t)(pb * T * kSlots * 4);
-      half2_t p2[PB][G], v2[PB][T];
+      for (int q0 = 0; q0 < NQ; q0 += QB) {
+        u32x4 p4[QB], v4[QB][PU::UPL];
 #pragma unroll
-      for (int i = 0; i < PB; ++i) {
-        if constexpr (G == 1) {
-          p2[i][0] = lds_load<half2_t>(pa + i * 4);
-        } else if constexpr (G == 2) {
-          const u32x2 w = lds_load<u32x2>(pa + i * 8);
-          p2[i][0] = as_h2(w.x);
-          p2[i][1] = as_h2(w.y);
-        } else {
+        for (int q = 0; q < QB; ++q) {
+          p4[q] = lds_load<u32x4>(base + L.ps + (pv_pair0 + 4u * (q0 + q)) * 4u);
 #pragma unroll
-          for (int g4 = 0; g4 < G; g4 += 4) {
-            const u32x4 w = lds_load<u32x4>(pa + (i * G + g4) * 4);
-            p2[i][g4 + 0] = as_h2(w.x);
-            p2[i][g4 + 1] = as_h2(w.y);
-            p2[i][g4 + 2] = as_h2(w.z);
-            p2[i][g4 + 3] = as_h2(w.w);
-          }
+          for (int k = 0; k < PU::UPL; ++k) v4[q][k] = lds_load<u32x4>(pv_addr[k] + 16u * (q0 + q));
         }
 #pragma unroll
-        for (int tt = 0; tt < T; ++tt)
-          v2[i][tt] = lds_load<half2_t>(da + (uint32_t)((i * T + tt) * kSlots * 4));
+        for (int q = 0; q < QB; ++q)
+#pragma unroll
+          for (int k = 0; k < PU::UPL; ++k) {
+            oh[h][k] = __builtin_amdgcn_fdot2(as_h2(v4[q][k].x), as_h2(p4[q].x), oh[h][k], false);
+            oh[h][k] = __builtin_amdgcn_fdot2(as_h2(v4[q][k].y), as_h2(p4[q].y), oh[h][k], false);
+            oh[h][k] = __builtin_amdgcn_fdot2(as_h2(v4[q][k].z), as_h2(p4[q].z), oh[h][k], false);
+            oh[h][k] = __builtin_amdgcn_fdot2(as_h2(v4[q][k].w), as_h2(p4[q].w), oh[h][k], false);
+          }
       }
-#pragma unroll
-      for (int i = 0; i < PB; ++i)
-#pragma unroll
-        for (int tt = 0; tt < T; ++tt)
-#pragma unroll
-          for (int g = 0; g < G; ++g) o[g][tt] = __builtin_amdgcn_fdot2(v2[i][tt], p2[i][g], o[g][tt], false);
     }
 
     if (has_next) {
@@ -284,6 +307,24 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
     }
     nb = nb_next;
     nb_next = nb_next2;
+  }
+
+  // Back to the partial layout (lane = channel of each tile): channel lane of
+  // tile tt is unit tt * 32 + lane % 32 of half lane / 32.
+  const bool upper = lane >= 32u;
+#pragma unroll
+  for (int tt = 0; tt < T; ++tt) {
+    if constexpr (T == 1) {
+      const int c = (int)(lane % 32u);
+      const float a0 = __shfl(oh[0][0], c, kWave) + __shfl(oh[0][0], c + 32, kWave);
+      const float a1 = __shfl(oh[1][0], c, kWave) + __shfl(oh[1][0], c + 32, kWave);
+      o[tt] = upper ? a1 : a0;
+    } else {
+      const int src = (tt % 2) * 32 + (int)(lane % 32u);
+      const float a0 = __shfl(oh[0][tt / 2], src, kWave);
+      const float a1 = __shfl(oh[1][tt / 2], src, kWave);
+      o[tt] = upper ? a1 : a0;
+    }
   }
 }
 
@@ -297,7 +338,7 @@ __global__ __launch_bounds__(64) void k_sparse_attn(AttnArgs a) {
   // With G >= 2 the compressed segments run on the MFMA kernel; this one then
   // only serves the window of a call whose compressed cache is empty.
   if constexpr (G == 1) {
-    if (seg < a.n_sparse_segs) sparse_body<T, G, STAGE>(a, seg, bh, smem, m_run, l_run, o);
+    if (seg < a.n_sparse_segs) sparse_body<T, STAGE>(a, seg, bh, smem, m_run[0], l_run[0], o[0]);
     else dense_body<T, G>(a, seg - a.n_sparse_segs, bh, smem, m_run, l_run, o);
   } else {
     dense_body<T, G>(a, seg - a.n_sparse_segs, bh, smem, m_run, l_run, o);
@@ -400,8 +441,7 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void k_merge(const float2* __r
 // ------------------------------------------------------------------------------------------
 template <int T, int G, int STAGE>
 static hipError_t sparse_launch(const AttnShape& sh, const AttnArgs& a, hipStream_t s) {
-  const SparseLds L = sparse_lds_layout(T, G, a.kmaxK, a.kmaxV);
-  size_t lds = L.total;
+  size_t lds = G == 1 ? sparse_lds_layout(T, a.kmaxK, a.kmaxV).total : 0;
   if (sh.n_dense_segs > 0 && dense_lds_bytes(T, G) > lds) lds = dense_lds_bytes(T, G);
   hipLaunchKernelGGL((k_sparse_attn<T, G, STAGE>), dim3(sh.n_sparse_segs + sh.n_dense_segs, sh.BHkv),
                      dim3(kWave), lds, s, a);
