@@ -119,11 +119,12 @@ struct SparseLds {
 constexpr int kHalfSlots = 33;
 constexpr uint32_t kPvRow = 36;  // dwords per half-tile row: 32 (T x NPT) + 4 pad
 
-// Bytes per tile of the q table. With one head the tiles sit 16 banks apart,
-// so the lanes of the two tiles of d = 128 read disjoint banks (but for the
-// scratch and boundary slots) in one key-walk load.
+// Bytes per tile of the q table: 49 dwords, so the two tiles of d = 128 sit 17
+// banks apart. A half's slots span 17 dwords; the lanes of the two tiles then
+// share only two banks in one key-walk load, and never on the slots that the
+// walks' surplus slots read (the scratch slot and channel 31 of the half).
 __host__ __device__ constexpr uint32_t qtab_stride(int G) {
-  return G == 1 ? 192u : ((uint32_t)(kSlots * G * 2) + 15u) & ~15u;
+  return G == 1 ? 196u : ((uint32_t)(kSlots * G * 2) + 15u) & ~15u;
 }
 
 __host__ __device__ constexpr uint32_t half_tile_bytes(int) { return kHalfSlots * kPvRow * 4u; }
@@ -132,7 +133,7 @@ __host__ __device__ inline SparseLds sparse_lds_layout(int T, int kmaxK, int kma
   const int NB = kWave / T;
   SparseLds L;
   uint32_t o = 0;
-  L.qtab = o;  o += T * qtab_stride(1);                          // [t][slot] fp16
+  L.qtab = o;  o += (T * qtab_stride(1) + 15u) & ~15u;           // [t][slot] fp16
   L.ps = o;    o += ((NB / 2) * 4 + 15) & ~15;                   // [pair] half2
   L.vst = o;   o += (run_region_elems(NB * kmaxV) * 2 + 15) & ~15u;
   const uint32_t kst_bytes = (run_region_elems(NB * kmaxK) * 2 + 15) & ~15u;
