@@ -38,10 +38,10 @@ struct KeyGroup {
   half2_t q[4];
 };
 
-template <bool PEEL>
+template <bool PEEL, bool HI>
 __device__ __forceinline__ void key_issue(uint32_t& x, uint32_t va, uint32_t qaddr, uint32_t m,
                                           KeyGroup& k) {
-  k.w = lds_load<u32x4>(va);
+  k.w = group_load<HI>(va);
 #pragma unroll
   for (int u = 0; u < 8; u += 2) {
     const uint32_t c0 = next_bit<PEEL>(x, u, m);
@@ -63,22 +63,22 @@ __device__ __forceinline__ void key_consume(const KeyGroup& k, float& acc) {
 // One 32-channel half of a key tile (bit 31 left out, see next_bit): n groups of
 // 8 from byte address a (n is the busiest lane's count, so the loop is uniform
 // and every iteration issues the next group before consuming the current one);
-// the first group has m phantom slots when PEEL.
-template <bool PEEL>
+// the upper half (HI) starts with m phantom slots.
+template <bool HI>
 __device__ __forceinline__ void key_half(int n, uint32_t x, uint32_t a, uint32_t qaddr, uint32_t m,
                                          float& acc) {
   if (n == 0) return;
   KeyGroup k0, k1;
-  key_issue<PEEL>(x, a, qaddr, m, k0);
+  key_issue<HI, HI>(x, a, qaddr, m, k0);
   int g = 1;
   for (; g + 1 < n; g += 2) {
-    key_issue<false>(x, a + 16u * g, qaddr, 0u, k1);
+    key_issue<false, HI>(x, a + 16u * g, qaddr, 0u, k1);
     key_consume(k0, acc);
-    key_issue<false>(x, a + 16u * (g + 1), qaddr, 0u, k0);
+    key_issue<false, HI>(x, a + 16u * (g + 1), qaddr, 0u, k0);
     key_consume(k1, acc);
   }
   if (g < n) {
-    key_issue<false>(x, a + 16u * g, qaddr, 0u, k1);
+    key_issue<false, HI>(x, a + 16u * g, qaddr, 0u, k1);
     key_consume(k0, acc);
     key_consume(k1, acc);
   } else {
@@ -92,7 +92,7 @@ __device__ __forceinline__ void key_half(int n, uint32_t x, uint32_t a, uint32_t
 __device__ __forceinline__ void key_walk(int nlo, int nhi, uint64_t bm, uint32_t va, uint32_t q_w0,
                                          uint32_t q_w1, _Float16 q31, _Float16 q63, float& acc) {
   const uint32_t lo = (uint32_t)bm, hi = (uint32_t)(bm >> 32);
-  const uint32_t s = (uint32_t)__popc(lo), c = s + (uint32_t)__popc(hi), m = s & 7u;
+  const uint32_t s = (uint32_t)__popc(lo), c = s + (uint32_t)__popc(hi), m = s & 3u;
   const _Float16 v31 = lds_load<_Float16>(va + 2u * s - 2u);
   const _Float16 v63 = lds_load<_Float16>(va + 2u * c - 2u);
   key_half<false>(nlo, lo & kLow31, va, q_w0, 0u, acc);
@@ -256,7 +256,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
     // overwrites the staged keys, read above), expand, p.V.
     const uint32_t va = base + L.vst + ((int)j < nb ? 2u * (cur.vo - rcur.vstart) : 0u);
     const uint32_t vlo = (uint32_t)cur.vb, vhi = (uint32_t)(cur.vb >> 32);
-    const uint32_t vs = (uint32_t)__popc(vlo), vm = vs & 7u;
+    const uint32_t vs = (uint32_t)__popc(vlo), vm = vs & 3u;
     const _Float16 v31 = lds_load<_Float16>(va + 2u * vs - 2u);
     const _Float16 v63 = lds_load<_Float16>(va + 2u * (vs + (uint32_t)__popc(vhi)) - 2u);
 #pragma unroll

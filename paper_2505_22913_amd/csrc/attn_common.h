@@ -293,7 +293,7 @@ __device__ __forceinline__ uint32_t dpp_or(uint32_t v) {
 __device__ __forceinline__ uint32_t half_groups_onehot(uint64_t bm, int shift) {
   const uint32_t s = (uint32_t)__popc((uint32_t)bm);
   const uint32_t lo = (s + 7u) >> 3;
-  const uint32_t hi = ((s & 7u) + (uint32_t)__popc((uint32_t)(bm >> 32)) + 7u) >> 3;
+  const uint32_t hi = ((s & 3u) + (uint32_t)__popc((uint32_t)(bm >> 32)) + 7u) >> 3;
   return (1u << (lo + shift)) | (1u << (hi + shift + 8));
 }
 
@@ -320,11 +320,10 @@ __device__ __forceinline__ WalkCounts walk_counts(uint64_t kb, uint64_t vb) {
 // and the scratch slot of the expanded tile, so the walk has no per-element
 // branch.
 //
-// The values of the upper half start at rank s = popcount(low half), which is
-// aligned only when s % 8 == 0. Its first group is read from the aligned
-// position below and its first s % 8 slots (values of the lower half, already
-// consumed) are phantom: they take channel -1 and consume no bit. Every later
-// group is aligned again.
+// The values of the upper half start at rank s = popcount(low half). Its groups
+// are read from rank s - s % 4 on (8-byte aligned, two 8-byte loads each), and
+// the first s % 4 slots (values of the lower half, already consumed) are
+// phantom: they take channel -1 and consume no bit.
 __device__ __forceinline__ _Float16 group_value(const u32x4& w, int u) {
   const half2_t h = as_h2(w[u >> 1]);
   return (u & 1) ? h.y : h.x;
@@ -365,29 +364,42 @@ __device__ __forceinline__ uint32_t next_bit(uint32_t& x, int u, uint32_t m) {
   }
 }
 
-template <bool PEEL>
+// 16 bytes of packed values: 16-byte aligned in the lower half (HI false),
+// 8-byte aligned in the upper half.
+template <bool HI>
+__device__ __forceinline__ u32x4 group_load(uint32_t va) {
+  if constexpr (HI) {
+    const u32x2 a = lds_load<u32x2>(va), b = lds_load<u32x2>(va + 8u);
+    return (u32x4){a.x, a.y, b.x, b.y};
+  } else {
+    return lds_load<u32x4>(va);
+  }
+}
+
+template <bool PEEL, bool HI>
 __device__ __forceinline__ void value_issue(uint32_t& x, uint32_t va, uint32_t m, ValueGroup& g) {
-  g.w = lds_load<u32x4>(va);
+  g.w = group_load<HI>(va);
 #pragma unroll
   for (int u = 0; u < 8; ++u) g.c[u] = next_bit<PEEL>(x, u, m);
 }
 
 // One 32-channel half of a tile scattered into the expanded tile, pipelined
-// like the key walk: n groups (the wave's maximum), m phantom slots first when PEEL.
-template <bool PEEL, uint32_t STRIDE>
+// like the key walk: n groups (the wave's maximum); the upper half (HI) starts
+// with m phantom slots.
+template <bool HI, uint32_t STRIDE>
 __device__ __forceinline__ void value_half(int n, uint32_t x, uint32_t a, uint32_t daddr, uint32_t m) {
   if (n == 0) return;
   ValueGroup g0, g1;
-  value_issue<PEEL>(x, a, m, g0);
+  value_issue<HI, HI>(x, a, m, g0);
   int g = 1;
   for (; g + 1 < n; g += 2) {
-    value_issue<false>(x, a + 16u * g, 0u, g1);
+    value_issue<false, HI>(x, a + 16u * g, 0u, g1);
     value_consume<STRIDE>(g0, daddr);
-    value_issue<false>(x, a + 16u * (g + 1), 0u, g0);
+    value_issue<false, HI>(x, a + 16u * (g + 1), 0u, g0);
     value_consume<STRIDE>(g1, daddr);
   }
   if (g < n) {
-    value_issue<false>(x, a + 16u * g, 0u, g1);
+    value_issue<false, HI>(x, a + 16u * g, 0u, g1);
     value_consume<STRIDE>(g0, daddr);
     value_consume<STRIDE>(g1, daddr);
   } else {
@@ -403,7 +415,7 @@ template <uint32_t STRIDE>
 __device__ __forceinline__ void expand_tile(int nlo, int nhi, uint64_t bm, uint32_t va, uint32_t d_w0,
                                             uint32_t d_w1) {
   const uint32_t lo = (uint32_t)bm, hi = (uint32_t)(bm >> 32);
-  const uint32_t s = (uint32_t)__popc(lo), c = s + (uint32_t)__popc(hi), m = s & 7u;
+  const uint32_t s = (uint32_t)__popc(lo), c = s + (uint32_t)__popc(hi), m = s & 3u;
   const _Float16 v31 = lds_load<_Float16>(va + 2u * s - 2u);
   const _Float16 v63 = lds_load<_Float16>(va + 2u * c - 2u);
   value_half<false, STRIDE>(nlo, lo & kLow31, va, d_w0, 0u);
