@@ -103,21 +103,24 @@ __device__ __forceinline__ void key_walk(int nlo, int nhi, uint64_t bm, uint32_t
 
 // LDS layout of the compressed body (byte offsets). Values are expanded one
 // 32-channel half at a time (both halves of every tile of the block), into a
-// channel-major half tile: row `slot` (0 = the scratch slot, 1 + c = channel c
-// of the half) holds dword t * NPT + p = tokens 2p, 2p+1 of tile t (NPT token
-// pairs per block), rows kPvRow dwords apart. The scatter's lanes write the
-// banks of their token pairs whatever their channel, and p.V reads four token
-// pairs of one channel with one 16-byte load, conflict-free across a row of
-// lanes (the row stride is 9 x 16 bytes). The half tile shares its bytes with
-// the staged keys: it is cleared after the key walk of a block and read by p.V
-// before the next block's keys are committed. A workgroup is one wave, whose
-// LDS operations execute in program order, so the phases need no barrier.
+// channel-major half tile of 32-dword rows: row `slot` (0 = the scratch slot,
+// 1 + c = channel c of the half) holds, in dword t * NBH + j % NBH, token j of
+// tile t (low half for the block's first NBH = NB / 2 tokens, high half for the
+// others). A 32-lane pass of the scatter is then one token half, and its lanes
+// write 32 different banks whatever their channels; p.V reads four dwords (eight
+// tokens) of one channel per 16-byte load, with the lanes of two tiles
+// interleaved and each lane's four chunks rotated by its channel, so eight
+// neighbouring lanes read eight different bank groups. The half tile shares its
+// bytes with the staged keys: it is cleared after the key walk of a block and
+// read by p.V before the next block's keys are committed. A workgroup is one
+// wave, whose LDS operations execute in program order, so the phases need no
+// barrier.
 struct SparseLds {
   uint32_t qtab, ps, dense, kst, vst, total;
 };
 
 constexpr int kHalfSlots = 33;
-constexpr uint32_t kPvRow = 36;  // dwords per half-tile row: 32 (T x NPT) + 4 pad
+constexpr uint32_t kPvRow = 32;  // dwords per half-tile row (T x NBH)
 
 // Bytes per tile of the q table: 49 dwords, so the two tiles of d = 128 sit 17
 // banks apart. A half's slots span 17 dwords; the lanes of the two tiles then
@@ -134,7 +137,7 @@ __host__ __device__ inline SparseLds sparse_lds_layout(int T, int kmaxK, int kma
   SparseLds L;
   uint32_t o = 0;
   L.qtab = o;  o += (T * qtab_stride(1) + 15u) & ~15u;           // [t][slot] fp16
-  L.ps = o;    o += ((NB / 2) * 4 + 15) & ~15;                   // [pair] half2
+  L.ps = o;    o += ((NB / 2) * 4 + 15) & ~15;                   // [j % NBH] half2
   L.vst = o;   o += (run_region_elems(NB * kmaxV) * 2 + 15) & ~15u;
   const uint32_t kst_bytes = (run_region_elems(NB * kmaxK) * 2 + 15) & ~15u;
   L.kst = o;
@@ -144,14 +147,14 @@ __host__ __device__ inline SparseLds sparse_lds_layout(int T, int kmaxK, int kma
   return L;
 }
 
-// p.V work of a lane per half: (tile, channel-of-half) units. With T >= 2 the
-// 32 T units are spread over the 64 lanes (unit L + 64 k of lane L); with T = 1
-// lanes L and L + 32 share unit L % 32 and split the token pairs.
+// p.V work of a lane per half: units (tile u % T, channel u / T of the half).
+// With T >= 2 lane L takes units L + 64 k; with T = 1 lanes L and L + 32 share
+// unit L % 32 and split its row. NQL 16-byte chunks per unit and lane.
 template <int T>
 struct PvUnits {
   static constexpr int UPL = T >= 2 ? T / 2 : 1;
-  static constexpr int NP = kWave / T / 2;                 // token pairs per block
-  static constexpr int NPL = T == 1 ? NP / 2 : NP;         // pairs per lane
+  static constexpr int NBH = kWave / T / 2;                // dwords of one tile in a row
+  static constexpr int NQL = T == 1 ? NBH / 8 : NBH / 4;
 };
 
 // Compressed segment, one head per kv-head.
@@ -203,16 +206,19 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   const uint16_t* qrow = a.q + (int64_t)bh * d + kTile * t;
   const _Float16 q31 = __builtin_bit_cast(_Float16, qrow[31]);
   const _Float16 q63 = __builtin_bit_cast(_Float16, qrow[63]);
-  constexpr uint32_t NPT = PU::NP;
+  constexpr uint32_t NBH = PU::NBH;
   constexpr uint32_t kRowB = kPvRow * 4u;  // expanded-tile stride per channel
-  const uint32_t d_w = base + L.dense + kRowB + (t * NPT + (j >> 1)) * 4u + (j & 1) * 2u;
-  // ... and p.V units (tile tu, channel lane % 32 of the half).
-  const uint32_t pv_pair0 = T == 1 ? (lane / 32u) * PU::NPL : 0u;
-  uint32_t pv_addr[PU::UPL];
+  const uint32_t d_w = base + L.dense + kRowB + (t * NBH + j % NBH) * 4u + (j / NBH) * 2u;
+  // ... and p.V units: row start of each unit, the lane's first dword in it and
+  // its chunk rotation.
+  const uint32_t pv_dw0 = T == 1 ? (lane / 32u) * (NBH / 2) : 0u;
+  uint32_t pv_row[PU::UPL], pv_rot[PU::UPL];
 #pragma unroll
   for (int k = 0; k < PU::UPL; ++k) {
-    const uint32_t tu = T == 1 ? 0u : lane / 32u + 2u * k;
-    pv_addr[k] = base + L.dense + ((1u + lane % 32u) * kPvRow + tu * NPT + pv_pair0) * 4u;
+    const uint32_t u = T == 1 ? lane % 32u : lane + 64u * k;
+    const uint32_t tu = u % T, c = u / T;
+    pv_row[k] = base + L.dense + ((1u + c) * kPvRow + tu * NBH + pv_dw0) * 4u;
+    pv_rot[k] = c;
   }
   float oh[2][PU::UPL];
 #pragma unroll
@@ -249,7 +255,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int k = 0; k < PU::UPL; ++k) oh[h][k] *= alpha;
-      if (t == 0) lds_store<_Float16>(base + L.ps + (j >> 1) * 4 + (j & 1) * 2, ph);
+      if (t == 0) lds_store<_Float16>(base + L.ps + (j % PU::NBH) * 4 + (j / PU::NBH) * 2, ph);
     }
 
     // Values, one half of every tile at a time: clear the half tile (it
@@ -275,27 +281,28 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
         value_half<true, kRowB>(wc.vhi, vhi & kLow31, va + 2u * (vs - vm), d_w, vm);
         lds_store<_Float16>(d_w + kRowB * 31u, (int)vhi < 0 ? v63 : (_Float16)0.f);
       }
-      // p.V over the lane's token pairs (tokens past the block end have p = 0
-      // and zero values), four pairs per 16-byte load of p and of each unit.
-      constexpr int NQ = PU::NPL / 4;
-      constexpr int QB = NQ >= 2 ? 2 : 1;  // 16-byte loads in flight per unit
+      // p.V over the lane's tokens (tokens past the block end have p = 0 and
+      // zero values): per 16-byte chunk, eight tokens of p and of each unit.
+      constexpr int QB = PU::NQL >= 2 ? 2 : 1;  // chunks in flight per unit
 #pragma unroll 1
-      for (int q0 = 0; q0 < NQ; q0 += QB) {
-        u32x4 p4[QB], v4[QB][PU::UPL];
-#pragma unroll
-        for (int q = 0; q < QB; ++q) {
-          p4[q] = lds_load<u32x4>(base + L.ps + (pv_pair0 + 4u * (q0 + q)) * 4u);
-#pragma unroll
-          for (int k = 0; k < PU::UPL; ++k) v4[q][k] = lds_load<u32x4>(pv_addr[k] + 16u * (q0 + q));
-        }
+      for (int q0 = 0; q0 < PU::NQL; q0 += QB) {
+        u32x4 p4[QB][PU::UPL], v4[QB][PU::UPL];
 #pragma unroll
         for (int q = 0; q < QB; ++q)
 #pragma unroll
           for (int k = 0; k < PU::UPL; ++k) {
-            oh[h][k] = __builtin_amdgcn_fdot2(as_h2(v4[q][k].x), as_h2(p4[q].x), oh[h][k], false);
-            oh[h][k] = __builtin_amdgcn_fdot2(as_h2(v4[q][k].y), as_h2(p4[q].y), oh[h][k], false);
-            oh[h][k] = __builtin_amdgcn_fdot2(as_h2(v4[q][k].z), as_h2(p4[q].z), oh[h][k], false);
-            oh[h][k] = __builtin_amdgcn_fdot2(as_h2(v4[q][k].w), as_h2(p4[q].w), oh[h][k], false);
+            const uint32_t ch = ((uint32_t)(q0 + q) + pv_rot[k]) % (uint32_t)PU::NQL;
+            p4[q][k] = lds_load<u32x4>(base + L.ps + (pv_dw0 + 4u * ch) * 4u);
+            v4[q][k] = lds_load<u32x4>(pv_row[k] + 16u * ch);
+          }
+#pragma unroll
+        for (int q = 0; q < QB; ++q)
+#pragma unroll
+          for (int k = 0; k < PU::UPL; ++k) {
+            oh[h][k] = __builtin_amdgcn_fdot2(as_h2(v4[q][k].x), as_h2(p4[q][k].x), oh[h][k], false);
+            oh[h][k] = __builtin_amdgcn_fdot2(as_h2(v4[q][k].y), as_h2(p4[q][k].y), oh[h][k], false);
+            oh[h][k] = __builtin_amdgcn_fdot2(as_h2(v4[q][k].z), as_h2(p4[q][k].z), oh[h][k], false);
+            oh[h][k] = __builtin_amdgcn_fdot2(as_h2(v4[q][k].w), as_h2(p4[q][k].w), oh[h][k], false);
           }
       }
     }
@@ -310,21 +317,27 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
     nb_next = nb_next2;
   }
 
-  // Back to the partial layout (lane = channel of each tile): channel lane of
-  // tile tt is unit tt * 32 + lane % 32 of half lane / 32.
+  // Back to the partial layout (lane = channel of each tile): channel `lane`
+  // of tile tt is channel lane % 32 of half lane / 32, unit (lane % 32) T + tt.
   const bool upper = lane >= 32u;
+  const int c = (int)(lane % 32u);
 #pragma unroll
   for (int tt = 0; tt < T; ++tt) {
     if constexpr (T == 1) {
-      const int c = (int)(lane % 32u);
       const float a0 = __shfl(oh[0][0], c, kWave) + __shfl(oh[0][0], c + 32, kWave);
       const float a1 = __shfl(oh[1][0], c, kWave) + __shfl(oh[1][0], c + 32, kWave);
       o[tt] = upper ? a1 : a0;
-    } else {
-      const int src = (tt % 2) * 32 + (int)(lane % 32u);
-      const float a0 = __shfl(oh[0][tt / 2], src, kWave);
-      const float a1 = __shfl(oh[1][tt / 2], src, kWave);
+    } else if constexpr (T == 2) {
+      const int src = c * 2 + tt;
+      const float a0 = __shfl(oh[0][0], src, kWave);
+      const float a1 = __shfl(oh[1][0], src, kWave);
       o[tt] = upper ? a1 : a0;
+    } else {
+      const int u = c * T + tt, src = u % 64;
+      const bool k1 = u >= 64;
+      const float a00 = __shfl(oh[0][0], src, kWave), a01 = __shfl(oh[0][1], src, kWave);
+      const float a10 = __shfl(oh[1][0], src, kWave), a11 = __shfl(oh[1][1], src, kWave);
+      o[tt] = upper ? (k1 ? a11 : a10) : (k1 ? a01 : a00);
     }
   }
 }
