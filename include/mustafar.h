@@ -164,6 +164,74 @@ int mustafar_dense_decode_attn(const void* q, int B, int Hq, int Hkv, const void
                                const void* v, int n_tokens, int d, float scale, void* out,
                                int n_splits, void* ws, size_t ws_bytes, void* stream);
 
+/* THE DENSE LOCAL WINDOW (Sec. 3: the most recent tokens stay dense and are
+ * not pruned; tokens leaving the window are pruned and compressed at decode
+ * time). A ring of W token slots per stream, with device-side state per batch
+ * entry so that the entries of a batch may hold different numbers of tokens:
+ *   k, v     [B][H][W][d] fp16 ring slots, 16-byte aligned
+ *   len[b]   tokens in the window of batch entry b (0..W)
+ *   head[b]  slot of its oldest token; the i-th oldest is in slot (head+i) % W
+ *   n_comp[b] tokens of entry b already in the compressed caches (they are
+ *            tokens 0 .. n_comp[b]-1 of every stream of b; the window holds
+ *            tokens n_comp[b] .. n_comp[b]+len[b]-1)
+ * len, head and n_comp are int32 device arrays owned by the caller, who sets
+ * them after filling the caches (a prefill of entry b with P tokens compresses
+ * its first P - min(P, W) tokens and copies the rest into slots 0.. with
+ * head = 0). The host-side max_len is an upper bound of len[b] over the batch
+ * and the caches' n_tokens an upper bound of n_comp[b]; the calls below keep
+ * both bounds and use them for capacity checks and launch geometry. */
+typedef struct mustafar_window {
+    uint16_t* k;      /* [B][H][W][d] fp16                                        */
+    uint16_t* v;      /* [B][H][W][d] fp16                                        */
+    int32_t* len;     /* [B] device                                               */
+    int32_t* head;    /* [B] device                                               */
+    int32_t* n_comp;  /* [B] device                                               */
+    int32_t B, H, d, W;
+    int32_t max_len;  /* host: upper bound of len[b]                              */
+} mustafar_window_t;
+
+/* Fills *w for caller-allocated buffers (host only; touches no buffer).
+ * 1 <= W <= 1024; 0 <= max_len <= W. Errors: EINVAL. */
+int mustafar_window_init(mustafar_window_t* w, void* k, void* v, void* len, void* head,
+                         void* n_comp, int B, int H, int d, int W, int max_len);
+
+/* Prefill of the window lifecycle with prompts of different lengths: batch
+ * entry b holds the first seq_len[b] tokens of x_k, x_v [B][H][n_max][d] fp16
+ * (16-byte aligned; seq_len is a HOST array, 0 <= seq_len[b] <= n_max). Its
+ * first seq_len[b] - min(seq_len[b], W) tokens are pruned, compressed and
+ * written to the EMPTY caches Kc, Vc (n_tokens == 0); the remaining tokens
+ * fill window slots 0.. in order; len[b], head[b] = 0 and n_comp[b] are set.
+ * Afterwards Kc/Vc->n_tokens and w->max_len hold the batch maxima. ws: at
+ * least mustafar_compress_workspace_bytes(1, H, n_max) bytes, 8-byte aligned
+ * (used by one entry after the other). Errors: EINVAL, ECAPACITY, EWORKSPACE. */
+int mustafar_window_prefill(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
+                            const void* x_k, const void* x_v, int n_max, const int32_t* seq_len,
+                            void* ws, size_t ws_bytes, void* stream);
+
+/* One decode step of the window lifecycle for every batch entry b with
+ * active[b] != 0 (active may be NULL: every entry): the new token
+ * k_new, v_new [B][H][d] fp16 (16-byte aligned) enters the window; if the
+ * window of b was full (len[b] == W), its oldest token first leaves it: it is
+ * pruned, compressed and appended to Kc and Vc as token n_comp[b] (the same
+ * result as mustafar_append, per batch entry) and n_comp[b] += 1; otherwise
+ * len[b] += 1. Kc and Vc must have B, H = w->H and d = w->d. The host bounds
+ * advance: if w->max_len == W, Kc->n_tokens and Vc->n_tokens grow by one (the
+ * call fails with ECAPACITY, enqueuing nothing, if that would pass
+ * cap_tokens), else w->max_len grows by one. */
+int mustafar_window_step(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
+                         const void* k_new, const void* v_new, const void* active, void* stream);
+
+/* Decode attention of Algorithm 1 per batch entry b over its n_comp[b]
+ * compressed tokens and the len[b] tokens of its window (the window is
+ * Algorithm 1's dense local part). Every batch entry must hold at least one
+ * token. Shapes and the other arguments as for mustafar_sparse_decode_attn;
+ * the workspace is mustafar_attn_workspace_bytes(B, Hq, H, d, Kc->n_tokens,
+ * n_splits). Errors: EINVAL, EUNSUPPORTED, EWORKSPACE. */
+int mustafar_window_decode_attn(const void* q, int B, int Hq, const mustafar_ccache_t* Kc,
+                                const mustafar_ccache_t* Vc, const mustafar_window_t* w,
+                                float scale, void* out, int n_splits, void* ws, size_t ws_bytes,
+                                void* stream);
+
 /* Static message for a status code. */
 const char* mustafar_strerror(int status);
 

@@ -40,6 +40,14 @@ class ccache_t(ctypes.Structure):
                 ("n_tokens", ctypes.c_int32), ("val_stride", ctypes.c_int64)]
 
 
+class window_t(ctypes.Structure):
+    """Mirror of ``mustafar_window_t``."""
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("len", ctypes.c_void_p),
+                ("head", ctypes.c_void_p), ("n_comp", ctypes.c_void_p),
+                ("B", ctypes.c_int32), ("H", ctypes.c_int32), ("d", ctypes.c_int32),
+                ("W", ctypes.c_int32), ("max_len", ctypes.c_int32)]
+
+
 _SIGS = {
     "mustafar_keep_count": (ctypes.c_int, [ctypes.c_int, ctypes.c_float]),
     "mustafar_token_max_elems": (ctypes.c_int64, [ctypes.c_int, ctypes.c_int]),
@@ -67,6 +75,22 @@ _SIGS = {
                                                   ctypes.c_int, ctypes.c_int, ctypes.c_float,
                                                   ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                                   ctypes.c_size_t, ctypes.c_void_p]),
+    "mustafar_window_init": (ctypes.c_int, [ctypes.POINTER(window_t)] + [ctypes.c_void_p] * 5
+                             + [ctypes.c_int] * 5),
+    "mustafar_window_prefill": (ctypes.c_int, [ctypes.POINTER(window_t), ctypes.POINTER(ccache_t),
+                                               ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                               ctypes.c_void_p, ctypes.c_int,
+                                               ctypes.POINTER(ctypes.c_int32), ctypes.c_void_p,
+                                               ctypes.c_size_t, ctypes.c_void_p]),
+    "mustafar_window_step": (ctypes.c_int, [ctypes.POINTER(window_t), ctypes.POINTER(ccache_t),
+                                            ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "mustafar_window_decode_attn": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                                   ctypes.POINTER(ccache_t),
+                                                   ctypes.POINTER(ccache_t),
+                                                   ctypes.POINTER(window_t), ctypes.c_float,
+                                                   ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                                   ctypes.c_size_t, ctypes.c_void_p]),
     "mustafar_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "mustafar_stream_read_sink_bytes": (ctypes.c_size_t, []),
     "mustafar_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
@@ -239,6 +263,74 @@ def mustafar_dense_decode_attn(q, k, v, scale: float = 0.0, out=None, n_splits: 
     _check("mustafar_dense_decode_attn", lib().mustafar_dense_decode_attn(
         _dptr(q), B, Hq, Hkv, _dptr(k), _dptr(v), N, d, float(scale), _dptr(out), int(n_splits),
         _dptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+    return out
+
+
+# ---- the dense local window (lifecycle) -------------------------------------------------
+class DenseWindow:
+    """The dense window of the W most recent tokens of every stream: ring slots
+    k, v [B][H][W][d] fp16 and int32 device state len, head, n_comp [B]."""
+
+    def __init__(self, B: int, H: int, d: int, W: int, device="cuda"):
+        import torch
+        self.k = torch.zeros((B, H, W, d), dtype=torch.float16, device=device)
+        self.v = torch.zeros((B, H, W, d), dtype=torch.float16, device=device)
+        self.len = torch.zeros(B, dtype=torch.int32, device=device)
+        self.head = torch.zeros(B, dtype=torch.int32, device=device)
+        self.n_comp = torch.zeros(B, dtype=torch.int32, device=device)
+        self.desc = window_t()
+        _check("mustafar_window_init", lib().mustafar_window_init(
+            ctypes.byref(self.desc), self.k.data_ptr(), self.v.data_ptr(), self.len.data_ptr(),
+            self.head.data_ptr(), self.n_comp.data_ptr(), B, H, d, W, 0))
+
+    @property
+    def W(self) -> int:
+        return self.desc.W
+
+    @property
+    def max_len(self) -> int:
+        return self.desc.max_len
+
+
+def mustafar_window_prefill(win: DenseWindow, Kc: CompressedCache, Vc: CompressedCache, x_k, x_v,
+                            seq_len, ws=None, stream=None) -> None:
+    """Prompts of seq_len[b] tokens (host ints) in x_k, x_v [B][H][n_max][d] fp16: the
+    tokens before each entry's last min(seq_len[b], W) are compressed, the rest fill
+    its window."""
+    import torch
+    n_max = int(x_k.shape[2])
+    lens = (ctypes.c_int32 * len(seq_len))(*[int(n) for n in seq_len])
+    need = mustafar_compress_workspace_bytes(1, win.desc.H, max(n_max, 1))
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=x_k.device)
+    _check("mustafar_window_prefill", lib().mustafar_window_prefill(
+        ctypes.byref(win.desc), ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), _dptr(x_k),
+        _dptr(x_v), n_max, lens, _dptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def mustafar_window_step(win: DenseWindow, Kc: CompressedCache, Vc: CompressedCache, k_new, v_new,
+                         active=None, stream=None) -> None:
+    """One decode step: k_new, v_new [B][H][d] enter the windows of the active entries
+    (active: int32 device [B] or None); full windows first hand their oldest token
+    to the compressed caches."""
+    _check("mustafar_window_step", lib().mustafar_window_step(
+        ctypes.byref(win.desc), ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), _dptr(k_new),
+        _dptr(v_new), _dptr(active), _stream(stream)))
+
+
+def mustafar_window_decode_attn(q, Kc: CompressedCache, Vc: CompressedCache, win: DenseWindow,
+                                scale: float = 0.0, out=None, n_splits: int = 0, ws=None,
+                                stream=None):
+    """Algorithm 1 per batch entry over its compressed tokens and its window."""
+    import torch
+    B, Hq, d = (int(s) for s in q.shape)
+    if out is None:
+        out = torch.empty((B, Hq, d), dtype=torch.float16, device=q.device)
+    ws = _attn_ws(B, Hq, Kc.desc.H, d, Kc.n_tokens, n_splits, ws, q.device)
+    _check("mustafar_window_decode_attn", lib().mustafar_window_decode_attn(
+        _dptr(q), B, Hq, ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), ctypes.byref(win.desc),
+        float(scale), _dptr(out), int(n_splits), _dptr(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
     return out
 
 

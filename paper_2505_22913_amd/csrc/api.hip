@@ -61,6 +61,22 @@ mf::SparseSide side_of(const mustafar_ccache_t* c) {
   return s;
 }
 
+constexpr int kMaxWindow = 1024;  // window slots per stream (one attention segment)
+
+int check_window(const mustafar_window_t* w) {
+  if (!w || !aligned(w->k, 16) || !aligned(w->v, 16) || !aligned(w->len, 4) ||
+      !aligned(w->head, 4) || !aligned(w->n_comp, 4))
+    return MUSTAFAR_EINVAL;
+  if (w->B < 1 || w->H < 1 || (int64_t)w->B * w->H > kMaxGrid || !head_dim_ok(w->d))
+    return MUSTAFAR_EINVAL;
+  if (w->W < 1 || w->W > kMaxWindow || w->max_len < 0 || w->max_len > w->W) return MUSTAFAR_EINVAL;
+  return MUSTAFAR_OK;
+}
+
+bool window_matches(const mustafar_window_t* w, const mustafar_ccache_t* c) {
+  return c->B == w->B && c->H == w->H && c->d == w->d;
+}
+
 int round_up(int x, int a) { return (x + a - 1) / a * a; }
 
 // Segment size (tokens, multiple of 64) for n tokens split n_splits ways.
@@ -74,6 +90,33 @@ int n_segments(int n, int seg) { return n <= 0 ? 0 : (n + seg - 1) / seg; }
 float scale_log2_of(float scale, int d) {
   const double s = scale > 0.f ? (double)scale : 1.0 / sqrt((double)d);
   return (float)(s * 1.4426950408889634);  // log2(e): scores live in the exp2 domain
+}
+
+mf::WindowView window_view_of(const mustafar_window_t* w) {
+  mf::WindowView wv;
+  wv.k = w->k;
+  wv.v = w->v;
+  wv.len = w->len;
+  wv.head = w->head;
+  wv.n_comp = w->n_comp;
+  wv.B = w->B;
+  wv.H = w->H;
+  wv.W = w->W;
+  return wv;
+}
+
+// The streams of batch entry b as a one-entry cache (same buffers).
+mustafar_ccache_t entry_view(const mustafar_ccache_t* c, int b) {
+  mustafar_ccache_t v = *c;
+  const int64_t s0 = (int64_t)b * c->H;
+  const int64_t tiles = s0 * c->cap_tokens * (c->d / kTile);
+  v.bitmaps = c->bitmaps + tiles;
+  v.offsets = c->offsets + tiles;
+  v.values = c->values + s0 * c->val_stride;
+  v.stream_len = c->stream_len + s0;
+  v.B = 1;
+  v.n_tokens = 0;
+  return v;
 }
 
 }  // namespace
@@ -257,6 +300,116 @@ int mustafar_dense_decode_attn(const void* q, int B, int Hq, int Hkv, const void
   return status_of(mf::launch_attention(sh, (const uint16_t*)q, none, none, (const uint16_t*)k,
                                         (const uint16_t*)v, ws_ml, ws_o, (uint16_t*)out,
                                         (hipStream_t)stream));
+}
+
+int mustafar_window_init(mustafar_window_t* w, void* k, void* v, void* len, void* head,
+                         void* n_comp, int B, int H, int d, int W, int max_len) {
+  if (!w || !aligned(k, 16) || !aligned(v, 16) || !aligned(len, 4) || !aligned(head, 4) ||
+      !aligned(n_comp, 4))
+    return MUSTAFAR_EINVAL;
+  if (B < 1 || H < 1 || (int64_t)B * H > kMaxGrid || !head_dim_ok(d)) return MUSTAFAR_EINVAL;
+  if (W < 1 || W > kMaxWindow || max_len < 0 || max_len > W) return MUSTAFAR_EINVAL;
+  w->k = (uint16_t*)k;
+  w->v = (uint16_t*)v;
+  w->len = (int32_t*)len;
+  w->head = (int32_t*)head;
+  w->n_comp = (int32_t*)n_comp;
+  w->B = B;
+  w->H = H;
+  w->d = d;
+  w->W = W;
+  w->max_len = max_len;
+  return MUSTAFAR_OK;
+}
+
+int mustafar_window_prefill(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
+                            const void* x_k, const void* x_v, int n_max, const int32_t* seq_len,
+                            void* ws, size_t ws_bytes, void* stream) {
+  int st = check_window(w);
+  if (st != MUSTAFAR_OK) return st;
+  if ((st = check_cache(Kc)) != MUSTAFAR_OK || (st = check_cache(Vc)) != MUSTAFAR_OK) return st;
+  if (!window_matches(w, Kc) || !window_matches(w, Vc)) return MUSTAFAR_EINVAL;
+  if (Kc->n_tokens != 0 || Vc->n_tokens != 0) return MUSTAFAR_EINVAL;
+  if (n_max < 0 || !seq_len || !aligned(x_k, 16) || !aligned(x_v, 16)) return MUSTAFAR_EINVAL;
+  int max_comp = 0, max_len = 0;
+  for (int b = 0; b < w->B; ++b) {
+    if (seq_len[b] < 0 || seq_len[b] > n_max) return MUSTAFAR_EINVAL;
+    const int len = seq_len[b] < w->W ? seq_len[b] : w->W;
+    if (seq_len[b] - len > max_comp) max_comp = seq_len[b] - len;
+    if (len > max_len) max_len = len;
+  }
+  if (max_comp > Kc->cap_tokens || max_comp > Vc->cap_tokens) return MUSTAFAR_ECAPACITY;
+  if (max_comp > 0 && (!aligned(ws, 8) || ws_bytes < mustafar_compress_workspace_bytes(1, w->H, n_max)))
+    return MUSTAFAR_EWORKSPACE;
+  const hipStream_t s = (hipStream_t)stream;
+  const int64_t entry = (int64_t)w->H * n_max * w->d;  // fp16 elements per batch entry of x
+  for (int b = 0; b < w->B; ++b) {
+    const int len = seq_len[b] < w->W ? seq_len[b] : w->W;
+    const int n_comp = seq_len[b] - len;
+    const uint16_t* xk = (const uint16_t*)x_k + b * entry;
+    const uint16_t* xv = (const uint16_t*)x_v + b * entry;
+    if (n_comp > 0) {
+      const mustafar_ccache_t kb = entry_view(Kc, b), vb = entry_view(Vc, b);
+      if ((st = status_of(mf::launch_compress(view_of(&kb), xk, n_comp, 0, (uint32_t*)ws, s, n_max))) !=
+              MUSTAFAR_OK ||
+          (st = status_of(mf::launch_compress(view_of(&vb), xv, n_comp, 0, (uint32_t*)ws, s, n_max))) !=
+              MUSTAFAR_OK)
+        return st;
+    }
+    if ((st = status_of(mf::launch_window_fill(window_view_of(w), b, w->d, xk, xv, n_max, n_comp, len,
+                                               s))) != MUSTAFAR_OK)
+      return st;
+  }
+  Kc->n_tokens = max_comp;
+  Vc->n_tokens = max_comp;
+  w->max_len = max_len;
+  return MUSTAFAR_OK;
+}
+
+int mustafar_window_step(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
+                         const void* k_new, const void* v_new, const void* active, void* stream) {
+  int st = check_window(w);
+  if (st != MUSTAFAR_OK) return st;
+  if ((st = check_cache(Kc)) != MUSTAFAR_OK || (st = check_cache(Vc)) != MUSTAFAR_OK) return st;
+  if (!window_matches(w, Kc) || !window_matches(w, Vc)) return MUSTAFAR_EINVAL;
+  if (!aligned(k_new, 16) || !aligned(v_new, 16)) return MUSTAFAR_EINVAL;
+  if (active && !aligned(active, 4)) return MUSTAFAR_EINVAL;
+  const bool may_graduate = w->max_len >= w->W;
+  if (may_graduate && (Kc->n_tokens + 1 > Kc->cap_tokens || Vc->n_tokens + 1 > Vc->cap_tokens))
+    return MUSTAFAR_ECAPACITY;
+  st = status_of(mf::launch_window_step(view_of(Kc), view_of(Vc), window_view_of(w), (const uint16_t*)k_new,
+                                        (const uint16_t*)v_new, (const int32_t*)active,
+                                        (hipStream_t)stream));
+  if (st != MUSTAFAR_OK) return st;
+  if (may_graduate) {
+    Kc->n_tokens += 1;
+    Vc->n_tokens += 1;
+  } else {
+    w->max_len += 1;
+  }
+  return MUSTAFAR_OK;
+}
+
+int mustafar_window_decode_attn(const void* q, int B, int Hq, const mustafar_ccache_t* Kc,
+                                const mustafar_ccache_t* Vc, const mustafar_window_t* w,
+                                float scale, void* out, int n_splits, void* ws, size_t ws_bytes,
+                                void* stream) {
+  int st = check_window(w);
+  if (st != MUSTAFAR_OK) return st;
+  if ((st = check_cache(Kc)) != MUSTAFAR_OK || (st = check_cache(Vc)) != MUSTAFAR_OK) return st;
+  if (!window_matches(w, Kc) || !window_matches(w, Vc) || w->B != B) return MUSTAFAR_EINVAL;
+  if (Kc->n_tokens != Vc->n_tokens) return MUSTAFAR_EINVAL;
+  mf::AttnShape sh;
+  float *ws_ml, *ws_o;
+  st = decode_common(q, B, Hq, Kc->H, Kc->d, Kc->n_tokens, w->W, 1, n_splits, scale, out, ws,
+                     ws_bytes, &sh, &ws_ml, &ws_o);
+  if (st != MUSTAFAR_OK) return st;
+  sh.n_comp = w->n_comp;
+  sh.win_len = w->len;
+  sh.win_head = w->head;
+  sh.Hkv = Kc->H;
+  return status_of(mf::launch_attention(sh, (const uint16_t*)q, side_of(Kc), side_of(Vc), w->k, w->v,
+                                        ws_ml, ws_o, (uint16_t*)out, (hipStream_t)stream));
 }
 
 const char* mustafar_strerror(int status) {

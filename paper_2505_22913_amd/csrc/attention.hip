@@ -183,7 +183,8 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   }
 
   const int j0 = seg * a.sparse_seg_tokens;
-  const int j1 = min(j0 + a.sparse_seg_tokens, a.n_s);
+  const int j1 = min(j0 + a.sparse_seg_tokens, stream_tokens(a, bh));
+  if (j0 >= j1) return;  // past this stream's tokens: an empty partial
   const int64_t kt0 = (int64_t)bh * a.K.cap_tokens * T;
   const int64_t vt0 = (int64_t)bh * a.V.cap_tokens * T;
   const uint16_t* kv = a.K.values + (int64_t)bh * a.K.val_stride;
@@ -540,6 +541,10 @@ hipError_t launch_attention(const AttnShape& sh, const uint16_t* q, const Sparse
   a.BHq = sh.BHkv * sh.G;
   a.kmaxK = K.bitmaps != nullptr ? token_max_elems_dev(d, K.n_keep) : 0;
   a.kmaxV = V.bitmaps != nullptr ? token_max_elems_dev(d, V.n_keep) : 0;
+  a.n_comp = sh.n_comp;
+  a.win_len = sh.win_len;
+  a.win_head = sh.win_head;
+  a.Hkv = sh.Hkv;
   switch (sh.T) {
     case 1: return attention_T<1>(sh, a, out, s);
     case 2: return attention_T<2>(sh, a, out, s);

@@ -98,7 +98,8 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
   }
 
   const int j0 = seg * a.sparse_seg_tokens;
-  const int j1 = min(j0 + a.sparse_seg_tokens, a.n_s);
+  const int j1 = min(j0 + a.sparse_seg_tokens, stream_tokens(a, bh));
+  if (j0 >= j1) return;  // past this stream's tokens: an empty partial
   const int64_t kt0 = (int64_t)bh * a.K.cap_tokens * T;
   const int64_t vt0 = (int64_t)bh * a.V.cap_tokens * T;
   const uint16_t* kv = a.K.values + (int64_t)bh * a.K.val_stride;

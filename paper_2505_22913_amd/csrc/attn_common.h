@@ -38,7 +38,17 @@ struct AttnArgs {
   float* ws_o;
   int BHq;
   int kmaxK, kmaxV;  // worst-case fp16 elements per token of each cache
+  // Per-batch-entry lengths, null for uniform streams (see AttnShape).
+  const int32_t* n_comp;
+  const int32_t* win_len;
+  const int32_t* win_head;
+  int Hkv;
 };
+
+// Compressed tokens of stream bh (its batch entry's count when ragged).
+__device__ __forceinline__ int stream_tokens(const AttnArgs& a, int bh) {
+  return a.n_comp ? min(a.n_comp[bh / a.Hkv], a.n_s) : a.n_s;
+}
 
 __device__ __forceinline__ uint32_t ffbl(uint32_t x) {  // 0xffffffff when x == 0
   uint32_t r;
@@ -123,9 +133,15 @@ __device__ __forceinline__ void dense_body(const AttnArgs& a, int dseg, int bh, 
   const int j1 = min(j0 + a.dense_seg_tokens, a.n_dense);
   const uint16_t* kd = a.kd + (int64_t)bh * a.n_dense * d;
   const uint16_t* vd = a.vd + (int64_t)bh * a.n_dense * d;
+  // A ring window holds win_len tokens from slot win_head on; its other slots
+  // are skipped (their contents are arbitrary).
+  const bool ring = a.win_len != nullptr;
+  const int w_len = ring ? a.win_len[bh / a.Hkv] : a.n_dense;
+  const int w_head = ring ? a.win_head[bh / a.Hkv] : 0;
   for (int b0 = j0; b0 < j1; b0 += NB) {
     const int nb = min(NB, j1 - b0);
-    const bool valid = (int)j < nb;
+    const int slot = b0 + (int)j;
+    const bool valid = (int)j < nb && (!ring || (slot - w_head + a.n_dense) % a.n_dense < w_len);
     float acc[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g] = 0.f;
@@ -164,9 +180,11 @@ __device__ __forceinline__ void dense_body(const AttnArgs& a, int dseg, int bh, 
 #pragma unroll
       for (int g = 0; g < G; ++g) pv[g] = ps[jj * G + g];
       const uint16_t* vr = vd + (int64_t)(b0 + jj) * d;
+      // Skipped ring slots have p = 0 and may hold non-finite bits: read as 0.
+      const bool live = !ring || (b0 + jj - w_head + a.n_dense) % a.n_dense < w_len;
 #pragma unroll
       for (int tt = 0; tt < T; ++tt) {
-        const float v = half_bits_to_float(vr[lane + kTile * tt]);
+        const float v = live ? half_bits_to_float(vr[lane + kTile * tt]) : 0.f;
 #pragma unroll
         for (int g = 0; g < G; ++g) o[g][tt] = fmaf(pv[g], v, o[g][tt]);
       }

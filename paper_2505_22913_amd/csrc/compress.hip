@@ -17,7 +17,8 @@
 // selects and packs every token in place, publishes its chunk total, reads the
 // totals or prefixes of the chunks before it, and writes its packed run with
 // 16-byte stores. k_append handles the one-token-per-stream case of a decode
-// step.
+// step, and k_window_step the dense-window lifecycle around it: the token that
+// leaves a full window is the one appended.
 #include "mf_device.h"
 #include "mf_launch.h"
 
@@ -227,7 +228,8 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
                                                     uint32_t* __restrict__ stream_len,
                                                     int cap_tokens, int tok0, int64_t val_stride,
                                                     uint64_t* __restrict__ flags,
-                                                    uint32_t* __restrict__ ticket_ctr, int n_chunks) {
+                                                    uint32_t* __restrict__ ticket_ctr, int n_chunks,
+                                                    int64_t x_stride) {
   constexpr int d = kTile * T;
   constexpr int LPT = T >= 4 ? 2 : 1;      // lanes per token in the threshold search
   constexpr int TPW = kWave / LPT;          // tokens per chunk
@@ -249,7 +251,7 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
   // Stage the chunk's dense rows: 16-byte coalesced non-temporal loads (every
   // load issued; lanes past the chunk re-read its first piece and store nothing).
   {
-    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(x + ((int64_t)bh * n_new + j0) * d);
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(x + ((int64_t)bh * x_stride + j0) * d);
     const int n16 = nt * P16;
     constexpr int kIt = TPW * P16 / kWave;
     u32x4_t r[kIt];
@@ -408,39 +410,114 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
   }
 }
 
-// One wave per stream, 4 streams per 256-thread block.
+// Prune, compress and append one token (d fp16 at src) to stream bh as token
+// tok: the token's bitmaps and offsets, its packed values after the stream's
+// stream_len values (none when tok == 0), then the new stream_len. One wave.
 template <int T>
-__global__ __launch_bounds__(256) void k_append(const uint16_t* __restrict__ x, int BH, int k,
-                                                uint64_t* __restrict__ bitmaps,
-                                                uint32_t* __restrict__ offsets,
-                                                uint16_t* __restrict__ values,
-                                                uint32_t* __restrict__ stream_len, int cap_tokens,
-                                                int tok0, int64_t val_stride) {
-  constexpr int d = kTile * T;
-  const int bh = blockIdx.x * (256 / kWave) + threadIdx.x / kWave;
-  if (bh >= BH) return;
-  const uint32_t lane = lane_id();
-  const uint32_t base = tok0 > 0 ? stream_len[bh] : 0u;
+__device__ __forceinline__ void append_one(const CacheView& c, int bh, int tok,
+                                           const uint16_t* __restrict__ src, uint32_t lane) {
+  const uint32_t base = tok > 0 ? c.stream_len[bh] : 0u;
   uint16_t xv[T];
-  load_token<T>(x + (int64_t)bh * d, lane, xv);
+  load_token<T>(src, lane, xv);
   uint32_t mag[T];
 #pragma unroll
   for (int t = 0; t < T; ++t) mag[t] = xv[t] & 0x7fffu;
   uint64_t bm[T];
-  select_token<T>(mag, k, bm);
-  const int64_t tile0 = ((int64_t)bh * cap_tokens + tok0) * T;
+  select_token<T>(mag, c.n_keep, bm);
+  const int64_t tile0 = ((int64_t)bh * c.cap_tokens + tok) * T;
   uint64_t mine = bm[0];
 #pragma unroll
   for (int t = 1; t < T; ++t) mine = (lane == (uint32_t)t) ? bm[t] : mine;
-  if (lane < (uint32_t)T) bitmaps[tile0 + lane] = mine;
+  if (lane < (uint32_t)T) c.bitmaps[tile0 + lane] = mine;
   const uint32_t used =
-      pack_token<T>(xv, bm, base, values + (int64_t)bh * val_stride, offsets + tile0, lane);
-  if (lane == 0) stream_len[bh] = base + used;
+      pack_token<T>(xv, bm, base, c.values + (int64_t)bh * c.val_stride, c.offsets + tile0, lane);
+  if (lane == 0) c.stream_len[bh] = base + used;
+}
+
+// One wave per stream, 4 streams per 256-thread block.
+template <int T>
+__global__ __launch_bounds__(256) void k_append(CacheView c, const uint16_t* __restrict__ x, int tok0) {
+  const int bh = blockIdx.x * (256 / kWave) + threadIdx.x / kWave;
+  if (bh >= c.BH) return;
+  append_one<T>(c, bh, tok0, x + (int64_t)bh * kTile * T, lane_id());
+}
+
+// Window step, one wave per stream: if the batch entry's window is full, its
+// oldest token (slot head) goes to both compressed caches as token n_comp and
+// the new token takes its slot; otherwise the new token goes to slot
+// (head + len) % W. The per-entry counters advance in k_window_commit, after
+// every stream of the entry has read them.
+template <int T>
+__global__ __launch_bounds__(256) void k_window_step(CacheView kc, CacheView vc, WindowView w,
+                                                     const uint16_t* __restrict__ k_new,
+                                                     const uint16_t* __restrict__ v_new,
+                                                     const int32_t* __restrict__ active) {
+  constexpr int d = kTile * T;
+  const int bh = blockIdx.x * (256 / kWave) + threadIdx.x / kWave;
+  if (bh >= kc.BH) return;
+  const int b = bh / w.H;
+  if (active != nullptr && active[b] == 0) return;
+  const uint32_t lane = lane_id();
+  const int len = w.len[b], head = w.head[b];
+  if (len < 0 || len > w.W || head < 0 || head >= w.W) return;  // not a state these calls produce
+  uint16_t* kr = w.k + (int64_t)bh * w.W * d;
+  uint16_t* vr = w.v + (int64_t)bh * w.W * d;
+  int slot = (head + len) % w.W;
+  if (len >= w.W) {
+    slot = head;
+    const int tok = w.n_comp[b];
+    if (tok >= 0 && tok < kc.cap_tokens && tok < vc.cap_tokens) {  // guaranteed by the host's bound
+      append_one<T>(kc, bh, tok, kr + (int64_t)slot * d, lane);
+      append_one<T>(vc, bh, tok, vr + (int64_t)slot * d, lane);
+    }
+  }
+  // The old token was consumed above (its loads feed the selection), so the
+  // slot can take the new one.
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    kr[(int64_t)slot * d + kTile * t + lane] = k_new[(int64_t)bh * d + kTile * t + lane];
+    vr[(int64_t)slot * d + kTile * t + lane] = v_new[(int64_t)bh * d + kTile * t + lane];
+  }
+}
+
+__global__ void k_window_commit(WindowView w, const int32_t* __restrict__ active) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= w.B || (active != nullptr && active[b] == 0)) return;
+  if (w.len[b] < 0 || w.len[b] > w.W || w.head[b] < 0 || w.head[b] >= w.W) return;
+  if (w.len[b] >= w.W) {
+    w.head[b] = (w.head[b] + 1) % w.W;
+    w.n_comp[b] += 1;
+  } else {
+    w.len[b] += 1;
+  }
+}
+
+// Prefill of one batch entry's window: tokens [first, first + count) of each of
+// its H streams (x: [H][x_stride][d]) into ring slots 0.., and its state.
+__global__ __launch_bounds__(256) void k_window_fill(WindowView w, int b, int d,
+                                                     const uint16_t* __restrict__ xk,
+                                                     const uint16_t* __restrict__ xv,
+                                                     int64_t x_stride, int first, int count) {
+  const int64_t per_stream = (int64_t)count * d;
+  const int64_t n = (int64_t)w.H * per_stream;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t h = i / per_stream, r = i % per_stream;
+    const int64_t dst = ((int64_t)b * w.H + h) * w.W * d + r;
+    const int64_t src = (h * x_stride + first) * d + r;
+    w.k[dst] = xk[src];
+    w.v[dst] = xv[src];
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    w.len[b] = count;
+    w.head[b] = 0;
+    w.n_comp[b] = first;
+  }
 }
 
 template <int T>
-static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, int tok0,
-                             uint32_t* ws, hipStream_t s) {
+static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, int64_t x_stride,
+                             int tok0, uint32_t* ws, hipStream_t s) {
   const int n_chunks = (n_new + compress_chunk_tokens(T) - 1) / compress_chunk_tokens(T);
   const int64_t n_wg = (int64_t)c.BH * n_chunks;
   uint64_t* flags = reinterpret_cast<uint64_t*>(ws);
@@ -452,24 +529,36 @@ static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, i
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_compress<T>, dim3((uint32_t)n_wg), dim3(kWave), 0, s, x, n_new, c.n_keep,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
-                     flags, ticket, n_chunks);
+                     flags, ticket, n_chunks, x_stride);
   return hipGetLastError();
 }
 
 template <int T>
 static hipError_t append_T(const CacheView& c, const uint16_t* x, int tok0, hipStream_t s) {
   dim3 grid((c.BH + 3) / 4);
-  hipLaunchKernelGGL(k_append<T>, grid, dim3(256), 0, s, x, c.BH, c.n_keep, c.bitmaps, c.offsets,
-                     c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride);
+  hipLaunchKernelGGL(k_append<T>, grid, dim3(256), 0, s, c, x, tok0);
+  return hipGetLastError();
+}
+
+template <int T>
+static hipError_t window_step_T(const CacheView& kc, const CacheView& vc, const WindowView& w,
+                                const uint16_t* k_new, const uint16_t* v_new, const int32_t* active,
+                                hipStream_t s) {
+  hipLaunchKernelGGL(k_window_step<T>, dim3((kc.BH + 3) / 4), dim3(256), 0, s, kc, vc, w, k_new, v_new,
+                     active);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_window_commit, dim3((w.B + 255) / 256), dim3(256), 0, s, w, active);
   return hipGetLastError();
 }
 
 hipError_t launch_compress(const CacheView& c, const uint16_t* x, int n_new, int tok0, uint32_t* ws,
-                           hipStream_t s) {
+                           hipStream_t s, int64_t x_stride) {
+  if (x_stride <= 0) x_stride = n_new;
   switch (c.T) {
-    case 1: return compress_T<1>(c, x, n_new, tok0, ws, s);
-    case 2: return compress_T<2>(c, x, n_new, tok0, ws, s);
-    case 4: return compress_T<4>(c, x, n_new, tok0, ws, s);
+    case 1: return compress_T<1>(c, x, n_new, x_stride, tok0, ws, s);
+    case 2: return compress_T<2>(c, x, n_new, x_stride, tok0, ws, s);
+    case 4: return compress_T<4>(c, x, n_new, x_stride, tok0, ws, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -479,6 +568,28 @@ hipError_t launch_append(const CacheView& c, const uint16_t* x, int tok0, hipStr
     case 1: return append_T<1>(c, x, tok0, s);
     case 2: return append_T<2>(c, x, tok0, s);
     case 4: return append_T<4>(c, x, tok0, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_window_fill(const WindowView& w, int b, int d, const uint16_t* xk,
+                              const uint16_t* xv, int64_t x_stride, int first, int count,
+                              hipStream_t s) {
+  const int64_t n = (int64_t)w.H * count * d;
+  int blocks = (int)((n + 255) / 256);
+  blocks = blocks < 1 ? 1 : (blocks > 1024 ? 1024 : blocks);
+  hipLaunchKernelGGL(k_window_fill, dim3(blocks), dim3(256), 0, s, w, b, d, xk, xv, x_stride, first,
+                     count);
+  return hipGetLastError();
+}
+
+hipError_t launch_window_step(const CacheView& kc, const CacheView& vc, const WindowView& w,
+                              const uint16_t* k_new, const uint16_t* v_new, const int32_t* active,
+                              hipStream_t s) {
+  switch (kc.T) {
+    case 1: return window_step_T<1>(kc, vc, w, k_new, v_new, active, s);
+    case 2: return window_step_T<2>(kc, vc, w, k_new, v_new, active, s);
+    case 4: return window_step_T<4>(kc, vc, w, k_new, v_new, active, s);
     default: return hipErrorInvalidValue;
   }
 }

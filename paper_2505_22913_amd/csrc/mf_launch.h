@@ -24,13 +24,31 @@ struct CacheView {
   int64_t val_stride;
 };
 
-// Compress n_new tokens per stream (x: [BH][n_new][64T] fp16) after tok0 tokens.
+// Compress n_new tokens per stream (x: [BH][x_stride][64T] fp16, x_stride = n_new
+// when 0) after tok0 tokens.
 // ws: u64 look-back flags [BH][n_chunks] followed by a u32 ticket counter; it is
 // cleared by the call itself.
 hipError_t launch_compress(const CacheView& c, const uint16_t* x, int n_new, int tok0, uint32_t* ws,
-                           hipStream_t s);
+                           hipStream_t s, int64_t x_stride = 0);
 // Compress one token per stream (x: [BH][64T]) as token tok0.
 hipError_t launch_append(const CacheView& c, const uint16_t* x, int tok0, hipStream_t s);
+
+// One window step per active batch entry (see mustafar_window_step): the ring
+// slots k, v [BH][W][64T], device state len/head/n_comp [B], H streams per entry.
+struct WindowView {
+  uint16_t* k;
+  uint16_t* v;
+  int32_t* len;
+  int32_t* head;
+  int32_t* n_comp;
+  int B, H, W;
+};
+hipError_t launch_window_fill(const WindowView& w, int b, int d, const uint16_t* xk,
+                              const uint16_t* xv, int64_t x_stride, int first, int count,
+                              hipStream_t s);
+hipError_t launch_window_step(const CacheView& kc, const CacheView& vc, const WindowView& w,
+                              const uint16_t* k_new, const uint16_t* v_new, const int32_t* active,
+                              hipStream_t s);
 
 struct SparseSide {
   const uint64_t* bitmaps;
@@ -50,6 +68,13 @@ struct AttnShape {
   int n_sparse_segs, sparse_seg_tokens;
   int n_dense_segs, dense_seg_tokens;
   float scale_log2;  // score scale times log2(e)
+  // Per-batch-entry lengths (all null for uniform streams): compressed tokens
+  // n_comp[b] <= n_s, and a ring window of n_dense slots holding len[b] tokens
+  // from slot head[b] on. Hkv maps a stream to its batch entry.
+  const int32_t* n_comp = nullptr;
+  const int32_t* win_len = nullptr;
+  const int32_t* win_head = nullptr;
+  int Hkv = 1;
 };
 
 // Split-K merge in two levels when a single level would run on too few

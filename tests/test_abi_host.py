@@ -190,3 +190,76 @@ def test_stream_read_helper_rejects_bad_arguments(lib):
     assert lib.mustafar_stream_read(0x100000, 24, 0x200000, None) == mf.EINVAL   # bytes % 16
     assert lib.mustafar_stream_read(None, 64, 0x200000, None) == mf.EINVAL
     assert lib.mustafar_stream_read(0x100000, 64, None, None) == mf.EINVAL
+
+
+def _fake_window(B=2, H=4, d=128, W=32, max_len=0):
+    w = mf.window_t()
+    st = mf.lib().mustafar_window_init(ctypes.byref(w), 0xc00000, 0xd00000, 0xe00000, 0xe10000,
+                                       0xe20000, B, H, d, W, max_len)
+    return w, st
+
+
+def test_window_struct_layout_matches_the_c_compiler(tmp_path):
+    prog = tmp_path / "wlayout.c"
+    prog.write_text(
+        '#include <stddef.h>\n#include <stdio.h>\n#include "mustafar.h"\n'
+        "int main(void){printf(\"%zu %zu %zu %zu\\n\", sizeof(mustafar_window_t),"
+        " offsetof(mustafar_window_t, n_comp), offsetof(mustafar_window_t, B),"
+        " offsetof(mustafar_window_t, max_len));return 0;}\n")
+    exe = tmp_path / "wlayout"
+    subprocess.run(["gcc", "-std=c11", f"-I{os.path.dirname(HEADER)}", "-o", str(exe), str(prog)],
+                   check=True)
+    c_vals = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                             check=True).stdout.split()]
+    T = mf.window_t
+    assert c_vals == [ctypes.sizeof(T), T.n_comp.offset, T.B.offset, T.max_len.offset]
+
+
+def test_window_calls_reject_before_launch(lib):
+    w, st = _fake_window()
+    assert st == mf.OK and w.W == 32 and w.max_len == 0
+    assert _fake_window(W=0)[1] == mf.EINVAL
+    assert _fake_window(W=1025)[1] == mf.EINVAL
+    assert _fake_window(max_len=33)[1] == mf.EINVAL
+    assert _fake_window(d=96)[1] == mf.EINVAL
+    w2 = mf.window_t()
+    assert lib.mustafar_window_init(ctypes.byref(w2), 0xc00008, 0xd00000, 0xe00000, 0xe10000,
+                                    0xe20000, 2, 4, 128, 32, 0) == mf.EINVAL  # ring not 16-aligned
+    K, _ = _fake_cache(B=2, H=4, cap=10)
+    V, _ = _fake_cache(B=2, H=4, s=0.7, cap=10)
+    kn, vn, act = 0xf00000, 0xf10000, 0xf20000
+    step = lambda **kw: lib.mustafar_window_step(  # noqa: E731
+        ctypes.byref(kw.get("w", w)), ctypes.byref(kw.get("K", K)), ctypes.byref(kw.get("V", V)),
+        kw.get("kn", kn), vn, kw.get("act", act), None)
+    assert step(kn=kn + 2) == mf.EINVAL
+    assert step(act=act + 2) == mf.EINVAL
+    K3, _ = _fake_cache(B=3, H=4, cap=10)
+    assert step(K=K3) == mf.EINVAL                   # batch differs from the window
+    # A full window graduates a token: no room left in the caches.
+    wf, _ = _fake_window(max_len=32)
+    K.n_tokens = V.n_tokens = 10
+    assert step(w=wf) == mf.ECAPACITY
+    assert K.n_tokens == 10 and wf.max_len == 32     # nothing changed
+    # Prefill: host lengths are validated before anything runs.
+    K0, _ = _fake_cache(B=2, H=4, cap=10)
+    V0, _ = _fake_cache(B=2, H=4, s=0.7, cap=10)
+    lens = (ctypes.c_int32 * 2)(5, 50)
+    need = lib.mustafar_compress_workspace_bytes(1, 4, 50)
+    pre = lambda **kw: lib.mustafar_window_prefill(  # noqa: E731
+        ctypes.byref(w), ctypes.byref(kw.get("K", K0)), ctypes.byref(V0), 0x1000000, 0x2000000,
+        kw.get("n_max", 50), kw.get("lens", lens), 0x3000000, kw.get("ws_bytes", need), None)
+    assert pre(n_max=49) == mf.EINVAL                # a length beyond n_max
+    assert pre() == mf.ECAPACITY                     # 50 - 32 = 18 compressed > cap 10
+    lens2 = (ctypes.c_int32 * 2)(5, 40)
+    assert pre(lens=lens2, ws_bytes=need - 8) == mf.EWORKSPACE
+    K0.n_tokens = 1
+    assert pre(lens=lens2) == mf.EINVAL              # caches must start empty
+    # Attention over the window: shapes checked against the window.
+    K.n_tokens = V.n_tokens = 5
+    anb = lib.mustafar_attn_workspace_bytes(2, 8, 4, 128, 5, 0)
+    att = lambda **kw: lib.mustafar_window_decode_attn(  # noqa: E731
+        0x700000, kw.get("B", 2), kw.get("Hq", 8), ctypes.byref(K), ctypes.byref(V),
+        ctypes.byref(w), 0.0, 0x800000, 0, 0xb00000, kw.get("ws_bytes", anb), None)
+    assert att(B=3) == mf.EINVAL
+    assert att(Hq=12) == mf.EUNSUPPORTED
+    assert att(ws_bytes=anb - 4) == mf.EWORKSPACE

@@ -1,0 +1,99 @@
+"""Pins of the window-lifecycle oracle (oracle/window.py).
+
+The lifecycle is fixed by token positions (Sec. 3): after t arrivals an entry's
+window holds its last min(t, W) tokens and every earlier token is compressed.
+The pins check the oracle's bookkeeping against that closed form, with tokens
+that carry their own arrival index, and its attention against the same
+attention computed without the compressed format.
+"""
+import numpy as np
+import pytest
+
+from oracle.window import WindowOracle
+
+D = 64
+
+
+def _indexed_tokens(B, H, n, d, rng, base=0):
+    """Random fp16 tokens whose channel 0 holds the arrival index (exact in fp16)."""
+    x = rng.standard_normal((B, H, n, d)).astype(np.float16)
+    x[..., 0] = (base + np.arange(n, dtype=np.float64)).astype(np.float16)[None, None, :]
+    return x
+
+
+@pytest.mark.parametrize("W", [1, 2, 8, 32])
+def test_counts_follow_the_closed_form(W):
+    rng = np.random.default_rng(1)
+    B, H = 4, 2
+    seq = [0, 3, W, W + 5]
+    n_max = max(seq) or 1
+    xk = _indexed_tokens(B, H, n_max, D, rng)
+    xv = _indexed_tokens(B, H, n_max, D, rng)
+    o = WindowOracle(B, H, D, W, 0.5, 0.7)
+    o.prefill(xk, xv, seq)
+    arrived = list(seq)
+    masks = [None, [1, 0, 1, 1], [0, 0, 0, 1], None, [1, 1, 0, 0]]
+    for s in range(12):
+        act = masks[s % len(masks)]
+        kn = rng.standard_normal((B, H, D)).astype(np.float16)
+        o.step(kn, kn, act)
+        for b in range(B):
+            if act is None or act[b]:
+                arrived[b] += 1
+        for b in range(B):
+            t = arrived[b]
+            assert o.arrived(b) == t
+            assert o.window_len(b) == min(t, W)
+            assert o.n_comp(b) == max(0, t - W)
+
+
+def test_window_holds_the_last_tokens_oldest_first():
+    rng = np.random.default_rng(2)
+    B, H, W = 3, 2, 4
+    seq = [2, 4, 9]
+    xk = _indexed_tokens(B, H, 9, D, rng)
+    o = WindowOracle(B, H, D, W, 0.5, 0.5)
+    o.prefill(xk, xk, seq)
+    for s in range(6):
+        kn = rng.standard_normal((B, H, D)).astype(np.float16)
+        kn[..., 0] = np.float16(100 + s)
+        o.step(kn, kn, [1, s % 2, 1])
+    for b in range(B):
+        wk, _ = o.window(b)
+        idx = wk[0, :, 0].view(np.float16).astype(np.float64)
+        # arrival order of entry b: prefill indices, then the steps it took part in
+        order = list(range(seq[b])) + [100 + s for s in range(6) if b != 1 or s % 2]
+        assert list(idx) == order[-min(len(order), W):]
+
+
+def test_hand_example_window_of_two():
+    """W = 2, three tokens a, b, c: a is compressed, the window is [b, c]."""
+    o = WindowOracle(1, 1, D, 2, 0.5, 0.5)
+    toks = [np.full((1, 1, D), v, dtype=np.float16) for v in (1.0, 2.0, 3.0)]
+    for t in toks:
+        o.step(t, t)
+    assert o.n_comp(0) == 1 and o.window_len(0) == 2
+    wk, _ = o.window(0)
+    assert wk[0, :, 0].view(np.float16).tolist() == [2.0, 3.0]
+    enc_k, _ = o.compressed(0)
+    # All channels of token a tie at 1.0: the lower half of the channels is kept.
+    assert int(enc_k["bitmaps"][0, 0, 0, 0]) == (1 << 32) - 1
+
+
+@pytest.mark.parametrize("G", [1, 4])
+def test_attention_equals_the_direct_computation(G):
+    rng = np.random.default_rng(3)
+    B, H, W = 3, 2, 5
+    seq = [1, 5, 11]
+    xk = _indexed_tokens(B, H, 11, D, rng)
+    xv = rng.standard_normal((B, H, 11, D)).astype(np.float16)
+    o = WindowOracle(B, H, D, W, 0.5, 0.7)
+    o.prefill(xk, xv, seq)
+    for s in range(4):
+        o.step(rng.standard_normal((B, H, D)).astype(np.float16),
+               rng.standard_normal((B, H, D)).astype(np.float16), [1, 1, s % 2])
+    q = rng.standard_normal((B, H * G, D)).astype(np.float16)
+    for b in range(B):
+        a = o.attention(q[b], b)
+        r = o.attention_direct(q[b], b)
+        np.testing.assert_allclose(a, r, rtol=0, atol=1e-12)
