@@ -42,6 +42,7 @@ def parse():
     ap.add_argument("--splits", type=int, default=0, help="split-K segments (0: library default)")
     ap.add_argument("--seed", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-window", action="store_true", help="skip the dense-window lifecycle leg")
     ap.add_argument("--cpu-sample-streams", type=int, default=256)
     ap.add_argument("--cpu-threads", type=int, default=0, help="0: min(16, cpu count)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -268,6 +269,44 @@ def main():
     dense_kv = 2 * 2 * w.B * w.Hkv * w.N * w.d
     comp_kv = 12 * w.B * w.Hkv * w.N * (w.d // 64) * 2 + 2 * (k_len0 + v_len0)
 
+    # ---- the same decode steps through the dense-window lifecycle: the ring of the
+    # last n_tail tokens, a push per step that graduates the oldest token of the full
+    # ring (prune + compress + append), then attention over compressed + ring ----
+    window = None
+    if not args.no_window:
+        del Kc, Vc
+        torch.cuda.empty_cache()
+        Kw = mf.CompressedCache(w.B, w.Hkv, w.d, w.sK, cap, device=dev)
+        Vw = mf.CompressedCache(w.B, w.Hkv, w.d, w.sV, cap, device=dev)
+        win = mf.DenseWindow(w.B, w.Hkv, w.d, w.n_tail, device=dev)
+        mf.mustafar_window_prefill(win, Kw, Vw, K, V, [w.N + w.n_tail] * w.B, ws_c)
+
+        def wstep(marks=None):
+            mf.mustafar_window_step(win, Kw, Vw, new_k, new_v)
+            if marks is not None:
+                marks[0].record()
+            mf.mustafar_window_decode_attn(q, Kw, Vw, win, out=out, n_splits=args.splits, ws=ws_a)
+            if marks is not None:
+                marks[1].record()
+
+        for _ in range(warm):
+            wstep()
+        torch.cuda.synchronize()
+        wmarks = [(ev(), ev()) for _ in range(steps)]
+        a, b = ev(), ev()
+        a.record()
+        for i in range(steps):
+            wstep(wmarks[i])
+        b.record()
+        torch.cuda.synchronize()
+        w_total = a.elapsed_time(b) / 1e3 / steps
+        w_attn = float(np.mean([m[0].elapsed_time(m[1]) for m in wmarks])) / 1e3
+        window = {"us_per_step": w_total * 1e6, "attention_us": w_attn * 1e6,
+                  "window_step_us": (w_total - w_attn) * 1e6, "tokens_per_s": w.B / w_total,
+                  "how": "mustafar_window_step + mustafar_window_decode_attn, ring of "
+                         f"{w.n_tail} tokens per stream"}
+        del Kw, Vw, win
+
     ceiling = read_ceiling_gbs()
 
     result = {
@@ -304,6 +343,7 @@ def main():
                            "frac": (dense_kv + comp_kv) / t_pc / 1e9 / HBM_PEAK_GBS,
                            "traffic": measured_traffic("k_compress", w.name, "bytes_k_plus_v")},
         "append_us_per_step": (total_s / steps - attn_s) * 1e6,
+        "window_lifecycle": window,
         "compression_ratio": comp_kv / dense_kv,
         "wall_s_timed": wall,
     }

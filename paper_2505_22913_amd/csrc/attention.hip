@@ -368,7 +368,7 @@ __global__ __launch_bounds__(64) void k_dense_attn(AttnArgs a) {
   const int seg = blockIdx.x, bh = blockIdx.y;
   float m_run[G], l_run[G], o[G][T];
   init_state<T, G>(m_run, l_run, o);
-  dense_body<T, G>(a, seg, bh, smem, m_run, l_run, o);
+  dense_body<T, G, false>(a, seg, bh, smem, m_run, l_run, o);
   write_partial<T, G>(a, seg, bh, m_run, l_run, o);
 }
 

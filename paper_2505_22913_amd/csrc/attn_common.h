@@ -115,7 +115,9 @@ __device__ __forceinline__ void lds_store(uint32_t byte_addr, V v) {
 // ------------------------------------------------------------------------------------------
 // Dense segment body: the local window of the sparse call, or a range of a dense cache.
 // ------------------------------------------------------------------------------------------
-template <int T, int G>
+// RING: the segment may be a ring window (win_len set) whose unused slots are
+// skipped; the dense baseline's segments are plain (RING false).
+template <int T, int G, bool RING = true>
 __device__ __forceinline__ void dense_body(const AttnArgs& a, int dseg, int bh, unsigned char* smem,
                                            float (&m_run)[G], float (&l_run)[G],
                                            float (&o)[G][T]) {
@@ -135,13 +137,13 @@ __device__ __forceinline__ void dense_body(const AttnArgs& a, int dseg, int bh, 
   const uint16_t* vd = a.vd + (int64_t)bh * a.n_dense * d;
   // A ring window holds win_len tokens from slot win_head on; its other slots
   // are skipped (their contents are arbitrary).
-  const bool ring = a.win_len != nullptr;
+  const bool ring = RING && a.win_len != nullptr;
   const int w_len = ring ? a.win_len[bh / a.Hkv] : a.n_dense;
   const int w_head = ring ? a.win_head[bh / a.Hkv] : 0;
   for (int b0 = j0; b0 < j1; b0 += NB) {
     const int nb = min(NB, j1 - b0);
-    const int slot = b0 + (int)j;
-    const bool valid = (int)j < nb && (!ring || (slot - w_head + a.n_dense) % a.n_dense < w_len);
+    const int rel = b0 + (int)j - w_head;  // age rank of the slot's token (ring), or its index
+    const bool valid = (int)j < nb && (!RING || (rel < 0 ? rel + a.n_dense : rel) < w_len);
     float acc[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) acc[g] = 0.f;
@@ -181,7 +183,8 @@ __device__ __forceinline__ void dense_body(const AttnArgs& a, int dseg, int bh, 
       for (int g = 0; g < G; ++g) pv[g] = ps[jj * G + g];
       const uint16_t* vr = vd + (int64_t)(b0 + jj) * d;
       // Skipped ring slots have p = 0 and may hold non-finite bits: read as 0.
-      const bool live = !ring || (b0 + jj - w_head + a.n_dense) % a.n_dense < w_len;
+      const int rj = b0 + jj - w_head;
+      const bool live = !RING || (rj < 0 ? rj + a.n_dense : rj) < w_len;
 #pragma unroll
       for (int tt = 0; tt < T; ++tt) {
         const float v = live ? half_bits_to_float(vr[lane + kTile * tt]) : 0.f;
