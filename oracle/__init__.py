@@ -14,6 +14,10 @@ loops over streams:
 * ``decode_attention`` -- Algorithm 1 over zero-filled pruned caches plus a
   dense local window, in float64.
 * ``sparse_decode_attention`` -- decompress, then ``decode_attention``.
+* ``prune_token_24``, ``prune_token_scored``, ``compress_variant`` -- the
+  pruner variants in the same format: 2:4 per token (Appendix B), output-aware
+  key pruning (Sec. 2), per-head kept counts (Sec. 4.5's finer-grained
+  sparsity); ``query_lookahead`` -- the channel weights of output-aware pruning.
 
 Streams are independent, so the batched helpers accept ``threads``: ctypes
 releases the GIL during each C call and streams are spread over a thread pool.
@@ -87,6 +91,13 @@ def _bind(lib):
     lib.oracle_decode_attention.argtypes = [P, ctypes.c_int, ctypes.c_int, P, P, ctypes.c_int,
                                             P, P, ctypes.c_int, ctypes.c_double, P]
     lib.oracle_decode_attention.restype = ctypes.c_int
+    lib.oracle_prune_token_24.argtypes = [P, ctypes.c_int, P]
+    lib.oracle_prune_token_24.restype = None
+    lib.oracle_prune_token_scored.argtypes = [P, P, ctypes.c_int, ctypes.c_int, P]
+    lib.oracle_prune_token_scored.restype = None
+    lib.oracle_encode_stream.argtypes = [P, P, ctypes.c_int, ctypes.c_int, P, P, P,
+                                         ctypes.c_int64, P]
+    lib.oracle_encode_stream.restype = ctypes.c_int
     return lib
 
 
@@ -237,6 +248,108 @@ def sparse_decode_attention(q, enc_k: dict, enc_v: dict, k_tail=None, v_tail=Non
     kc = decompress(enc_k, threads=threads)
     vc = decompress(enc_v, threads=threads)
     return decode_attention(q, kc, vc, k_tail, v_tail, scale, threads=threads)
+
+
+def prune_token_24(x) -> np.ndarray:
+    """Keep-mask of one token under 2:4 pruning (2 of every 4 consecutive channels)."""
+    xb = _bits(x).reshape(-1)
+    keep = np.zeros(xb.size, dtype=np.uint8)
+    _load().oracle_prune_token_24(_ptr(xb), xb.size, _ptr(keep))
+    return keep.astype(bool)
+
+
+def prune_token_scored(x, w, k: int) -> np.ndarray:
+    """Keep-mask of one key token under output-aware pruning: the k channels of
+    largest fp32 score |x_c| * w_c (w: float32 channel weights)."""
+    xb = _bits(x).reshape(-1)
+    wf = np.ascontiguousarray(np.asarray(w, dtype=np.float32).reshape(-1))
+    keep = np.zeros(xb.size, dtype=np.uint8)
+    _load().oracle_prune_token_scored(_ptr(xb), _ptr(wf), xb.size, int(k), _ptr(keep))
+    return keep.astype(bool)
+
+
+def compress_variant(x, mode: str = "magnitude", *, k: int | None = None, head_keep=None,
+                     weights=None, threads: int = 1) -> dict:
+    """The compressed format of x [B][H][N][d] under a pruner variant.
+
+    mode "magnitude": k kept channels per token (head h keeps head_keep[h] if given);
+    mode "2:4": 2 of every 4 consecutive channels; mode "output_aware": k (or
+    head_keep[h]) channels of largest |x| * weights, weights float32 [B][H][N][d].
+    Same dict as ``compress``.
+    """
+    xb = _bits(x)
+    B, H, N, d = xb.shape
+    T = d // TILE
+    if mode == "2:4":
+        ks = [d // 2] * H
+    elif head_keep is not None:
+        ks = [int(v) for v in head_keep]
+    else:
+        ks = [int(k)] * H
+    cap = max(N * token_max_elems(d, max(ks)), PAD)
+    bitmaps = np.zeros((B, H, N, T), dtype=np.uint64)
+    offsets = np.zeros((B, H, N, T), dtype=np.uint32)
+    values = np.zeros((B, H, cap), dtype=np.uint16)
+    stream_len = np.zeros((B, H), dtype=np.uint32)
+    if mode == "output_aware":
+        wts = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
+    lib = _load()
+
+    def one(bh):
+        b, h = bh
+        xs = np.ascontiguousarray(xb[b, h])
+        keep = np.zeros((N, d), dtype=np.uint8)
+        for j in range(N):
+            row = np.zeros(d, dtype=np.uint8)
+            if mode == "magnitude":
+                lib.oracle_prune_token(_ptr(np.ascontiguousarray(xs[j])), d, ks[h], _ptr(row))
+            elif mode == "2:4":
+                lib.oracle_prune_token_24(_ptr(np.ascontiguousarray(xs[j])), d, _ptr(row))
+            elif mode == "output_aware":
+                lib.oracle_prune_token_scored(_ptr(np.ascontiguousarray(xs[j])),
+                                              _ptr(np.ascontiguousarray(wts[b, h, j])), d, ks[h],
+                                              _ptr(row))
+            else:
+                raise ValueError(mode)
+            keep[j] = row
+        out_len = np.zeros(1, dtype=np.uint32)
+        bm = np.zeros((N, T), dtype=np.uint64)
+        off = np.zeros((N, T), dtype=np.uint32)
+        val = np.zeros(cap, dtype=np.uint16)
+        rc = lib.oracle_encode_stream(_ptr(xs), _ptr(keep), N, d, _ptr(bm), _ptr(off), _ptr(val),
+                                      cap, _ptr(out_len))
+        if rc != 0:
+            raise ValueError(f"oracle_encode_stream failed with {rc}")
+        bitmaps[b, h], offsets[b, h], values[b, h], stream_len[b, h] = bm, off, val, out_len[0]
+
+    _map(one, [(b, h) for b in range(B) for h in range(H)], threads)
+    return {"bitmaps": bitmaps, "offsets": offsets, "values": values,
+            "stream_len": stream_len, "n_keep": max(ks), "d": d}
+
+
+def query_lookahead(q, Hkv: int, L: int = 32) -> np.ndarray:
+    """Channel weights of output-aware key pruning (Sec. 2): for key token T of
+    kv-head h, the L1 sum over the queries t = T .. T+L-1 (those that exist) and
+    over the query heads of h's group of |q_t|, in float32, added in the order
+    t ascending, then query head ascending.
+
+    q [B][Hq][Nq][d] fp16 (one query per token position). Returns float32
+    [B][Hkv][Nq][d].
+    """
+    qb = _bits(q)
+    B, Hq, Nq, d = qb.shape
+    G = Hq // Hkv
+    mag = np.abs(qb.view(np.float16).astype(np.float32))
+    out = np.zeros((B, Hkv, Nq, d), dtype=np.float32)
+    for b in range(B):
+        for h in range(Hkv):
+            for T in range(Nq):
+                acc = np.zeros(d, dtype=np.float32)
+                for t in range(T, min(T + L, Nq)):
+                    for g in range(G):
+                        acc = acc + mag[b, h * G + g, t]
+                out[b, h, T] = acc
+    return out
 
 
 def compressed_bytes(enc: dict) -> int:

@@ -101,6 +101,49 @@ void oracle_prune_token(const uint16_t* x, int d, int k, uint8_t* keep)
 }
 
 /* ---------------------------------------------------------------------------
+ * Pruner variants that keep the same format.
+ * ------------------------------------------------------------------------- */
+
+/* 2:4 semi-structured pruning of one token (Appendix B): in every group of 4
+ * consecutive channels the 2 of largest magnitude are kept (R3 ties: lower
+ * channel first). d must be a multiple of 4. */
+void oracle_prune_token_24(const uint16_t* x, int d, uint8_t* keep)
+{
+    for (int g = 0; g + 4 <= d; g += 4) {
+        ranked_t r[4];
+        for (int i = 0; i < 4; ++i) {
+            r[i].mag = fabs(oracle_half_to_double(x[g + i]));
+            r[i].idx = g + i;
+        }
+        qsort(r, 4, sizeof(ranked_t), rank_cmp);
+        for (int i = 0; i < 4; ++i)
+            keep[r[i].idx] = i < 2;
+    }
+}
+
+/* Output-aware pruning of one key token (Sec. 2): the score of channel c is
+ * |x_c| * w_c with w the channel weights (the L1 sum of the query vectors that
+ * will attend to the token); the k channels of largest score are kept, ties
+ * to the lower channel. The score is the fp32 product of |x_c| (exact in fp32)
+ * and w_c, rounded once: the selection is decided in the precision the GPU
+ * decides it in. */
+void oracle_prune_token_scored(const uint16_t* x, const float* w, int d, int k, uint8_t* keep)
+{
+    ranked_t* r = (ranked_t*)malloc(sizeof(ranked_t) * (size_t)(d > 0 ? d : 1));
+    for (int c = 0; c < d; ++c) {
+        const float mag = (float)fabs(oracle_half_to_double(x[c]));
+        const float score = mag * w[c];
+        r[c].mag = (double)score;
+        r[c].idx = c;
+    }
+    qsort(r, (size_t)d, sizeof(ranked_t), rank_cmp);
+    memset(keep, 0, (size_t)d);
+    for (int i = 0; i < k && i < d; ++i)
+        keep[r[i].idx] = 1;
+    free(r);
+}
+
+/* ---------------------------------------------------------------------------
  * Bitmap-based compressed format (Sec. 3; padding and offset overhead Sec. 4.3).
  * One stream = the tokens of one (batch, kv-head).  T = d/64 tiles per token.
  *   bitmaps[j*T+t] : 64-bit kept mask of channels 64t..64t+63 of token j
@@ -110,18 +153,20 @@ void oracle_prune_token(const uint16_t* x, int d, int k, uint8_t* keep)
  *   *stream_len    : total fp16 elements used by the stream
  * Returns 0, or -1 if d is not a multiple of 64, -2 if values_cap is too small.
  * ------------------------------------------------------------------------- */
-int oracle_compress_stream(const uint16_t* x, int n_tokens, int d, int k,
-                           uint64_t* bitmaps, uint32_t* offsets, uint16_t* values,
-                           int64_t values_cap, uint32_t* stream_len)
+/* The format of n_tokens tokens whose kept channels are given: keep_all
+ * [n_tokens][d] (1 = kept). oracle_compress_stream is this after
+ * oracle_prune_token; the pruner variants use it with their own masks. */
+int oracle_encode_stream(const uint16_t* x, const uint8_t* keep_all, int n_tokens, int d,
+                         uint64_t* bitmaps, uint32_t* offsets, uint16_t* values,
+                         int64_t values_cap, uint32_t* stream_len)
 {
     if (d <= 0 || d % ORACLE_TILE != 0)
         return -1;
     int T = d / ORACLE_TILE;
-    uint8_t* keep = (uint8_t*)malloc((size_t)d);
     int64_t pos = 0; /* running offset in fp16 elements */
     for (int j = 0; j < n_tokens; ++j) {
         const uint16_t* tok = x + (int64_t)j * d;
-        oracle_prune_token(tok, d, k, keep);
+        const uint8_t* keep = keep_all + (int64_t)j * d;
         for (int t = 0; t < T; ++t) {
             uint64_t bm = 0;
             int count = 0;
@@ -131,10 +176,8 @@ int oracle_compress_stream(const uint16_t* x, int n_tokens, int d, int k,
                     ++count;
                 }
             int padded = (count + ORACLE_PAD - 1) / ORACLE_PAD * ORACLE_PAD;
-            if (pos + padded > values_cap) {
-                free(keep);
+            if (pos + padded > values_cap)
                 return -2;
-            }
             bitmaps[(int64_t)j * T + t] = bm;
             offsets[(int64_t)j * T + t] = (uint32_t)pos;
             int w = 0;
@@ -147,8 +190,22 @@ int oracle_compress_stream(const uint16_t* x, int n_tokens, int d, int k,
         }
     }
     *stream_len = (uint32_t)pos;
-    free(keep);
     return 0;
+}
+
+int oracle_compress_stream(const uint16_t* x, int n_tokens, int d, int k,
+                           uint64_t* bitmaps, uint32_t* offsets, uint16_t* values,
+                           int64_t values_cap, uint32_t* stream_len)
+{
+    if (d <= 0 || d % ORACLE_TILE != 0)
+        return -1;
+    uint8_t* keep = (uint8_t*)malloc((size_t)d * (size_t)(n_tokens > 0 ? n_tokens : 1));
+    for (int j = 0; j < n_tokens; ++j)
+        oracle_prune_token(x + (int64_t)j * d, d, k, keep + (int64_t)j * d);
+    const int rc = oracle_encode_stream(x, keep, n_tokens, d, bitmaps, offsets, values, values_cap,
+                                        stream_len);
+    free(keep);
+    return rc;
 }
 
 /* Inverse of the format: the zero-filled pruned cache, fp16 bits [n_tokens][d].

@@ -87,3 +87,46 @@ def test_planted_mistake_is_caught(tmp_path, name, orig, planted):
     so = _build(tmp_path, text.replace(orig, planted), "mut")
     with oracle.using_library(so):
         assert _battery() is not None, f"no pin caught: {name}"
+
+
+# Mistakes in the pruner variants, caught by the variant pins.
+VARIANT_MUTATIONS = [
+    ("2:4 keeps the two smallest", "keep[r[i].idx] = i < 2;", "keep[r[i].idx] = i >= 2;"),
+    ("2:4 groups of three", "for (int g = 0; g + 4 <= d; g += 4) {",
+     "for (int g = 0; g + 4 <= d; g += 3) {"),
+    ("output-aware score ignores the weights", "const float score = mag * w[c];",
+     "const float score = mag;"),
+    ("output-aware score ignores the magnitude", "const float score = mag * w[c];",
+     "const float score = w[c];"),
+]
+
+
+def _variant_battery():
+    from tests import test_oracle_variants as v
+    checks = [
+        ("24 enumeration", v.test_24_equals_enumeration_of_each_group),
+        ("24 numpy", v.test_24_numpy_stable_sort_and_invariants),
+        ("oa unit", v.test_output_aware_with_unit_weights_is_magnitude_pruning),
+        ("oa numpy", lambda: v.test_output_aware_equals_numpy_float32_scores(64)),
+    ]
+    for name, fn in checks:
+        try:
+            fn()
+        except Exception:  # noqa: BLE001 - any failure of a pin counts
+            return name
+    return None
+
+
+def test_unmodified_oracle_passes_the_variant_battery(tmp_path):
+    so = _build(tmp_path, open(SRC).read(), "vclean")
+    with oracle.using_library(so):
+        assert _variant_battery() is None
+
+
+@pytest.mark.parametrize("name,orig,planted", VARIANT_MUTATIONS, ids=[m[0] for m in VARIANT_MUTATIONS])
+def test_planted_variant_mistake_is_caught(tmp_path, name, orig, planted):
+    text = open(SRC).read()
+    assert text.count(orig) == 1, f"mutation anchor not unique: {orig!r}"
+    so = _build(tmp_path, text.replace(orig, planted), "vmut")
+    with oracle.using_library(so):
+        assert _variant_battery() is not None, f"no pin caught: {name}"
