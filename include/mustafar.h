@@ -127,6 +127,54 @@ int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void
  * one mustafar_prune_compress call. */
 int mustafar_append(mustafar_ccache_t* c, const void* x_new, void* stream);
 
+/* PRUNER VARIANTS in the same compressed format (the decode attention reads
+ * any bitmaps):
+ *   MUSTAFAR_PRUNE_MAGNITUDE     per-token magnitude top-k (the default above),
+ *                                optionally with a kept count per head;
+ *   MUSTAFAR_PRUNE_2_4           2:4 semi-structured per token (Appendix B): in
+ *                                every 4 consecutive channels the 2 of largest
+ *                                magnitude, ties to the lower channel; needs a
+ *                                cache with n_keep == d/2;
+ *   MUSTAFAR_PRUNE_OUTPUT_AWARE  output-aware key pruning (Sec. 2): the n_keep
+ *                                channels of largest score |x_c| * w_c, the fp32
+ *                                product rounded once, ties to the lower
+ *                                channel; w are non-negative fp32 channel
+ *                                weights per token (see mustafar_query_lookahead).
+ * head_keep (all modes but 2:4): NULL, or a HOST array [H] of kept counts per
+ * head, each in [0, c->n_keep] (finer-grained sparsity, Sec. 4.5; the cache's
+ * capacity is the one of n_keep). H <= 256 with head_keep. */
+enum mustafar_prune_mode {
+    MUSTAFAR_PRUNE_MAGNITUDE = 0,
+    MUSTAFAR_PRUNE_2_4 = 1,
+    MUSTAFAR_PRUNE_OUTPUT_AWARE = 2
+};
+typedef struct mustafar_prune_opts {
+    int32_t mode;
+    const int32_t* head_keep; /* host [H] or NULL                                  */
+    const float* weights;     /* device fp32 [B][H][n_tokens][d], 4-byte aligned;  */
+                              /* OUTPUT_AWARE only                                 */
+} mustafar_prune_opts_t;
+
+/* mustafar_prune_compress / mustafar_append under a pruner variant (opts NULL:
+ * the default magnitude pruning). For _ex compress, weights has n_new tokens
+ * per stream; for _ex append, one. Same workspace, capacity and errors as the
+ * default calls, plus EINVAL for a bad mode, head_keep or weights. */
+int mustafar_prune_compress_ex(mustafar_ccache_t* c, const void* x, int n_new,
+                               const mustafar_prune_opts_t* opts, void* ws, size_t ws_bytes,
+                               void* stream);
+int mustafar_append_ex(mustafar_ccache_t* c, const void* x_new, const mustafar_prune_opts_t* opts,
+                       void* stream);
+
+/* Channel weights of output-aware key pruning (Sec. 2: the L1 sum of the
+ * current and the next L-1 queries, summed over the query heads of a group):
+ *   w[b][h][t][c] = sum_{u = t}^{min(t+L, n_q)-1} sum_{g < Hq/Hkv}
+ *                   |q[b][h*(Hq/Hkv)+g][u][c]|
+ * in fp32, added in that order (u ascending, then g). q [B][Hq][n_q][d] fp16
+ * holds the query of every token position; w [B][Hkv][n_q][d] fp32 (both
+ * 16-byte aligned). The paper uses L = 32. Errors: EINVAL, EUNSUPPORTED. */
+int mustafar_query_lookahead(const void* q, int B, int Hq, int Hkv, int n_q, int d, int L,
+                             void* w, void* stream);
+
 /* Split-K segment count chosen when a decode call passes n_splits <= 0. */
 int mustafar_attn_default_splits(int B, int Hkv, int n_tokens);
 

@@ -48,6 +48,14 @@ class window_t(ctypes.Structure):
                 ("W", ctypes.c_int32), ("max_len", ctypes.c_int32)]
 
 
+class prune_opts_t(ctypes.Structure):
+    """Mirror of ``mustafar_prune_opts_t``."""
+    _fields_ = [("mode", ctypes.c_int32), ("head_keep", ctypes.c_void_p),
+                ("weights", ctypes.c_void_p)]
+
+
+PRUNE_MAGNITUDE, PRUNE_2_4, PRUNE_OUTPUT_AWARE = 0, 1, 2
+
 _SIGS = {
     "mustafar_keep_count": (ctypes.c_int, [ctypes.c_int, ctypes.c_float]),
     "mustafar_token_max_elems": (ctypes.c_int64, [ctypes.c_int, ctypes.c_int]),
@@ -91,6 +99,14 @@ _SIGS = {
                                                    ctypes.POINTER(window_t), ctypes.c_float,
                                                    ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                                    ctypes.c_size_t, ctypes.c_void_p]),
+    "mustafar_prune_compress_ex": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                                  ctypes.c_int, ctypes.POINTER(prune_opts_t),
+                                                  ctypes.c_void_p, ctypes.c_size_t,
+                                                  ctypes.c_void_p]),
+    "mustafar_append_ex": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                          ctypes.POINTER(prune_opts_t), ctypes.c_void_p]),
+    "mustafar_query_lookahead": (ctypes.c_int, [ctypes.c_void_p] + [ctypes.c_int] * 6
+                                 + [ctypes.c_void_p, ctypes.c_void_p]),
     "mustafar_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "mustafar_stream_read_sink_bytes": (ctypes.c_size_t, []),
     "mustafar_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
@@ -222,6 +238,53 @@ def mustafar_append(cache: CompressedCache, x_new, stream=None) -> None:
     """Append one token per stream, x_new [B][H][d] (fp16, device)."""
     _check("mustafar_append", lib().mustafar_append(ctypes.byref(cache.desc), _dptr(x_new),
                                                     _stream(stream)))
+
+
+def _prune_opts(mode, head_keep, weights):
+    """(prune_opts_t, keep-alive objects) for the _ex calls."""
+    o = prune_opts_t()
+    o.mode = int(mode)
+    keep = None
+    if head_keep is not None:
+        keep = (ctypes.c_int32 * len(head_keep))(*[int(v) for v in head_keep])
+        o.head_keep = ctypes.cast(keep, ctypes.c_void_p)
+    o.weights = _dptr(weights)
+    return o, keep
+
+
+def mustafar_prune_compress_ex(cache: CompressedCache, x, mode: int = 0, head_keep=None,
+                               weights=None, ws=None, stream=None) -> None:
+    """mustafar_prune_compress under a pruner variant (PRUNE_MAGNITUDE with optional
+    per-head counts, PRUNE_2_4, PRUNE_OUTPUT_AWARE with fp32 weights [B][H][n_new][d])."""
+    import torch
+    n_new = int(x.shape[2])
+    need = mustafar_compress_workspace_bytes(cache.desc.B, cache.desc.H, n_new)
+    if ws is None:
+        ws = torch.empty(max(need, 4), dtype=torch.uint8, device=x.device)
+    o, _keep = _prune_opts(mode, head_keep, weights)
+    _check("mustafar_prune_compress_ex", lib().mustafar_prune_compress_ex(
+        ctypes.byref(cache.desc), _dptr(x), n_new, ctypes.byref(o), _dptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def mustafar_append_ex(cache: CompressedCache, x_new, mode: int = 0, head_keep=None, weights=None,
+                       stream=None) -> None:
+    """mustafar_append under a pruner variant (weights fp32 [B][H][d] when output-aware)."""
+    o, _keep = _prune_opts(mode, head_keep, weights)
+    _check("mustafar_append_ex", lib().mustafar_append_ex(
+        ctypes.byref(cache.desc), _dptr(x_new), ctypes.byref(o), _stream(stream)))
+
+
+def mustafar_query_lookahead(q, Hkv: int, L: int = 32, out=None, stream=None):
+    """Output-aware channel weights from queries q [B][Hq][n_q][d] fp16: fp32
+    [B][Hkv][n_q][d]."""
+    import torch
+    B, Hq, n_q, d = (int(s) for s in q.shape)
+    if out is None:
+        out = torch.empty((B, Hkv, n_q, d), dtype=torch.float32, device=q.device)
+    _check("mustafar_query_lookahead", lib().mustafar_query_lookahead(
+        _dptr(q), B, Hq, int(Hkv), n_q, d, int(L), _dptr(out), _stream(stream)))
+    return out
 
 
 def _attn_ws(B, Hq, Hkv, d, n, n_splits, ws, device):

@@ -119,6 +119,35 @@ mustafar_ccache_t entry_view(const mustafar_ccache_t* c, int b) {
   return v;
 }
 
+// Host checks of a pruner-variant request; fills the kernel's options.
+int prune_opts_of(const mustafar_ccache_t* c, const mustafar_prune_opts_t* opts, mf::PruneOpts* o) {
+  o->mode = mf::kPruneMagnitude;
+  o->H = c->H;
+  o->per_head = 0;
+  o->weights = nullptr;
+  if (!opts) return MUSTAFAR_OK;
+  if (opts->mode != MUSTAFAR_PRUNE_MAGNITUDE && opts->mode != MUSTAFAR_PRUNE_2_4 &&
+      opts->mode != MUSTAFAR_PRUNE_OUTPUT_AWARE)
+    return MUSTAFAR_EINVAL;
+  o->mode = opts->mode;
+  if (opts->mode == MUSTAFAR_PRUNE_2_4) {
+    if (opts->head_keep || c->n_keep * 2 != c->d) return MUSTAFAR_EINVAL;
+  }
+  if (opts->mode == MUSTAFAR_PRUNE_OUTPUT_AWARE) {
+    if (!aligned(opts->weights, 4)) return MUSTAFAR_EINVAL;
+    o->weights = opts->weights;
+  }
+  if (opts->head_keep) {
+    if (c->H > mf::kMaxPruneHeads) return MUSTAFAR_EUNSUPPORTED;
+    for (int h = 0; h < c->H; ++h) {
+      if (opts->head_keep[h] < 0 || opts->head_keep[h] > c->n_keep) return MUSTAFAR_EINVAL;
+      o->head_keep[h] = opts->head_keep[h];
+    }
+    o->per_head = 1;
+  }
+  return MUSTAFAR_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -200,6 +229,48 @@ int mustafar_append(mustafar_ccache_t* c, const void* x_new, void* stream) {
                                    (hipStream_t)stream));
   if (st == MUSTAFAR_OK) c->n_tokens += 1;
   return st;
+}
+
+int mustafar_prune_compress_ex(mustafar_ccache_t* c, const void* x, int n_new,
+                               const mustafar_prune_opts_t* opts, void* ws, size_t ws_bytes,
+                               void* stream) {
+  if (!opts) return mustafar_prune_compress(c, x, n_new, ws, ws_bytes, stream);
+  int st = check_cache(c);
+  if (st != MUSTAFAR_OK) return st;
+  if (n_new < 1 || !aligned(x, 16)) return MUSTAFAR_EINVAL;
+  mf::PruneOpts o;
+  if ((st = prune_opts_of(c, opts, &o)) != MUSTAFAR_OK) return st;
+  if ((int64_t)c->n_tokens + n_new > c->cap_tokens) return MUSTAFAR_ECAPACITY;
+  const size_t need = mustafar_compress_workspace_bytes(c->B, c->H, n_new);
+  if (!aligned(ws, 8) || ws_bytes < need) return MUSTAFAR_EWORKSPACE;
+  st = status_of(mf::launch_compress_variant(view_of(c), (const uint16_t*)x, n_new, c->n_tokens,
+                                             (uint32_t*)ws, (hipStream_t)stream, o));
+  if (st == MUSTAFAR_OK) c->n_tokens += n_new;
+  return st;
+}
+
+int mustafar_append_ex(mustafar_ccache_t* c, const void* x_new, const mustafar_prune_opts_t* opts,
+                       void* stream) {
+  if (!opts) return mustafar_append(c, x_new, stream);
+  int st = check_cache(c);
+  if (st != MUSTAFAR_OK) return st;
+  if (!aligned(x_new, 16)) return MUSTAFAR_EINVAL;
+  mf::PruneOpts o;
+  if ((st = prune_opts_of(c, opts, &o)) != MUSTAFAR_OK) return st;
+  if (c->n_tokens + 1 > c->cap_tokens) return MUSTAFAR_ECAPACITY;
+  st = status_of(mf::launch_append_variant(view_of(c), (const uint16_t*)x_new, c->n_tokens,
+                                           (hipStream_t)stream, o));
+  if (st == MUSTAFAR_OK) c->n_tokens += 1;
+  return st;
+}
+
+int mustafar_query_lookahead(const void* q, int B, int Hq, int Hkv, int n_q, int d, int L,
+                             void* w, void* stream) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || n_q < 1 || L < 1) return MUSTAFAR_EINVAL;
+  if (!head_dim_ok(d)) return MUSTAFAR_EINVAL;
+  if (!aligned(q, 16) || !aligned(w, 16)) return MUSTAFAR_EINVAL;
+  return status_of(mf::launch_query_lookahead((const uint16_t*)q, B, Hq, Hkv, n_q, d / kTile, L,
+                                              (float*)w, (hipStream_t)stream));
 }
 
 int mustafar_attn_default_splits(int B, int Hkv, int n_tokens) {

@@ -36,10 +36,12 @@ __device__ __forceinline__ void lds_st(uint32_t byte_addr, V v) {
   *reinterpret_cast<__attribute__((address_space(3))) V*>(byte_addr) = v;
 }
 
-// Keep-mask of one token. mag[t] is the fp16 magnitude (bits & 0x7fff) of this
-// lane's channel in tile t. Sets bm[t] (wave-uniform) so that exactly k bits
-// are set over the T tiles: the k largest magnitudes, ties to lower channels.
-template <int T>
+// Keep-mask of one token. mag[t] is the key of this lane's channel in tile t:
+// the fp16 magnitude (bits & 0x7fff, 15 bits) or a non-negative fp32 score
+// (its bits, 31 bits, order like the values). Sets bm[t] (wave-uniform) so that
+// exactly k bits are set over the T tiles: the k largest keys, ties to lower
+// channels.
+template <int T, int NBITS = 15>
 __device__ __forceinline__ void select_token(const uint32_t (&mag)[T], int k, uint64_t (&bm)[T]) {
   if (k <= 0) {
 #pragma unroll
@@ -51,10 +53,10 @@ __device__ __forceinline__ void select_token(const uint32_t (&mag)[T], int k, ui
     for (int t = 0; t < T; ++t) bm[t] = ~0ull;
     return;
   }
-  // Largest threshold m with #{mag >= m} >= k: that is the k-th largest magnitude.
+  // Largest threshold m with #{mag >= m} >= k: that is the k-th largest key.
   uint32_t thr = 0;
 #pragma unroll
-  for (int b = 14; b >= 0; --b) {
+  for (int b = NBITS - 1; b >= 0; --b) {
     const uint32_t cand = thr | (1u << b);
     int cnt = 0;
 #pragma unroll
@@ -220,7 +222,9 @@ __device__ __forceinline__ uint32_t lowest_bits(uint32_t w, int n) {
 }
 
 // One wave per workgroup; a chunk is 64 tokens (32 when d = 256) of one stream.
-template <int T>
+// PRESET: the keep-masks are the bitmaps already in the cache for these tokens
+// (a pruner variant selected them); only the scan and the packing run.
+template <int T, bool PRESET = false>
 __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__ x, int n_new, int k,
                                                     uint64_t* __restrict__ bitmaps,
                                                     uint32_t* __restrict__ offsets,
@@ -271,7 +275,16 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
   // the last row and store nothing): NW words of 32 channels, channel order.
   constexpr int NW = NR / 16;
   uint32_t keep[NW];
-  {
+  if constexpr (PRESET) {
+    const int jt = min((int)lane / LPT, nt - 1);
+    const int64_t tb = ((int64_t)bh * cap_tokens + tok0 + j0 + jt) * T + ((int)lane % LPT) * (T / LPT);
+#pragma unroll
+    for (int t = 0; t < NW / 2; ++t) {
+      const uint64_t bm = bitmaps[tb + t];
+      keep[2 * t] = (uint32_t)bm;
+      keep[2 * t + 1] = (uint32_t)(bm >> 32);
+    }
+  } else {
     const int jt = min((int)lane / LPT, nt - 1);
     const unsigned char* row = s_rows + jt * ROW + ((int)lane % LPT) * CPL * 2;
     uint32_t pl[NR];
@@ -404,9 +417,100 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
     const int64_t tile0 = ((int64_t)bh * cap_tokens + tok0 + j0) * T + (int)lane * TPL;
 #pragma unroll
     for (int t = 0; t < TPL; ++t) {
-      bitmaps[tile0 + t] = (uint64_t)keep[2 * t] | ((uint64_t)keep[2 * t + 1] << 32);
+      if constexpr (!PRESET) bitmaps[tile0 + t] = (uint64_t)keep[2 * t] | ((uint64_t)keep[2 * t + 1] << 32);
       offsets[tile0 + t] = base + lane_off + tile_pos[t];
     }
+  }
+}
+
+// Keep-mask of one token under a pruner variant, lane = channel; xv[t] is the
+// lane's fp16 bits in tile t, w the token's fp32 channel weights (output-aware).
+template <int T>
+__device__ __forceinline__ void select_variant(const PruneOpts& o, int k, const uint16_t (&xv)[T],
+                                               const float* __restrict__ w, uint32_t lane,
+                                               uint64_t (&bm)[T]) {
+  if (o.mode == kPrune24) {
+    // 2 of every 4 consecutive channels (the lanes of a quad): a lane is kept if
+    // it beats at least two of the other three (larger magnitude, or equal and
+    // a lower channel).
+    const uint32_t i = lane & 3u;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const int key = xv[t] & 0x7fff;
+      const int k1 = __builtin_amdgcn_mov_dpp(key, 0xB1, 0xF, 0xF, false);  // lane ^ 1
+      const int k2 = __builtin_amdgcn_mov_dpp(key, 0x4E, 0xF, 0xF, false);  // lane ^ 2
+      const int k3 = __builtin_amdgcn_mov_dpp(key, 0x1B, 0xF, 0xF, false);  // lane ^ 3
+      const int wins = (key > k1 || (key == k1 && i < (i ^ 1u))) + (key > k2 || (key == k2 && i < (i ^ 2u))) +
+                       (key > k3 || (key == k3 && i < (i ^ 3u)));
+      bm[t] = ballot(wins >= 2);
+    }
+  } else if (o.mode == kPruneOutputAware) {
+    // Score |x| * w in fp32 (one rounding); non-negative, so its bits order
+    // like its value (31 significant bits).
+    uint32_t key[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const float m = fabsf(half_bits_to_float(xv[t]));
+      key[t] = __builtin_bit_cast(uint32_t, m * w[kTile * t + lane]);
+    }
+    select_token<T, 31>(key, k, bm);
+  } else {
+    uint32_t mag[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) mag[t] = xv[t] & 0x7fffu;
+    select_token<T>(mag, k, bm);
+  }
+}
+
+__device__ __forceinline__ int stream_keep(const PruneOpts& o, int bh, int n_keep) {
+  return o.per_head ? o.head_keep[bh % o.H] : n_keep;
+}
+
+// Bitmaps of tokens tok0 .. tok0+n_new-1 of every stream under a pruner
+// variant: one wave per token, lane = channel, kTokPerWave tokens per wave.
+constexpr int kTokPerWave = 8;
+
+template <int T>
+__global__ __launch_bounds__(256) void k_select(CacheView c, const uint16_t* __restrict__ x, int n_new,
+                                                int64_t x_stride, int tok0, PruneOpts o) {
+  constexpr int d = kTile * T;
+  const int64_t wave = (int64_t)blockIdx.x * (256 / kWave) + threadIdx.x / kWave;
+  const uint32_t lane = lane_id();
+  const int64_t total = (int64_t)c.BH * n_new;
+  for (int64_t i = wave * kTokPerWave; i < min(total, (wave + 1) * kTokPerWave); ++i) {
+    const int bh = (int)(i / n_new), j = (int)(i % n_new);
+    const int64_t row = (int64_t)bh * x_stride + j;
+    uint16_t xv[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) xv[t] = x[row * d + kTile * t + lane];
+    uint64_t bm[T];
+    select_variant<T>(o, stream_keep(o, bh, c.n_keep), xv, o.weights ? o.weights + row * d : nullptr,
+                      lane, bm);
+    uint64_t mine = bm[0];
+#pragma unroll
+    for (int t = 1; t < T; ++t) mine = (lane == (uint32_t)t) ? bm[t] : mine;
+    if (lane < (uint32_t)T) c.bitmaps[((int64_t)bh * c.cap_tokens + tok0 + j) * T + lane] = mine;
+  }
+}
+
+// Output-aware weights, one thread per (b, h, T, channel).
+__global__ __launch_bounds__(256) void k_query_lookahead(const uint16_t* __restrict__ q, int B, int Hq,
+                                                         int Hkv, int n_q, int d, int L,
+                                                         float* __restrict__ w) {
+  const int G = Hq / Hkv;
+  const int64_t n = (int64_t)B * Hkv * n_q * d;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int c = (int)(i % d);
+    const int tq = (int)((i / d) % n_q);
+    const int64_t bh = i / ((int64_t)d * n_q);
+    const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
+    float acc = 0.f;
+    const int t1 = min(tq + L, n_q);
+    for (int t = tq; t < t1; ++t)
+      for (int g = 0; g < G; ++g)
+        acc += fabsf(half_bits_to_float(q[(((int64_t)b * Hq + h * G + g) * n_q + t) * d + c]));
+    w[i] = acc;
   }
 }
 
@@ -432,6 +536,35 @@ __device__ __forceinline__ void append_one(const CacheView& c, int bh, int tok,
   const uint32_t used =
       pack_token<T>(xv, bm, base, c.values + (int64_t)bh * c.val_stride, c.offsets + tile0, lane);
   if (lane == 0) c.stream_len[bh] = base + used;
+}
+
+// append_one under a pruner variant (w: the token's fp32 weights, output-aware).
+template <int T>
+__device__ __forceinline__ void append_one_variant(const CacheView& c, const PruneOpts& o, int bh, int tok,
+                                                   const uint16_t* __restrict__ src,
+                                                   const float* __restrict__ w, uint32_t lane) {
+  const uint32_t base = tok > 0 ? c.stream_len[bh] : 0u;
+  uint16_t xv[T];
+  load_token<T>(src, lane, xv);
+  uint64_t bm[T];
+  select_variant<T>(o, stream_keep(o, bh, c.n_keep), xv, w, lane, bm);
+  const int64_t tile0 = ((int64_t)bh * c.cap_tokens + tok) * T;
+  uint64_t mine = bm[0];
+#pragma unroll
+  for (int t = 1; t < T; ++t) mine = (lane == (uint32_t)t) ? bm[t] : mine;
+  if (lane < (uint32_t)T) c.bitmaps[tile0 + lane] = mine;
+  const uint32_t used =
+      pack_token<T>(xv, bm, base, c.values + (int64_t)bh * c.val_stride, c.offsets + tile0, lane);
+  if (lane == 0) c.stream_len[bh] = base + used;
+}
+
+template <int T>
+__global__ __launch_bounds__(256) void k_append_variant(CacheView c, const uint16_t* __restrict__ x,
+                                                        int tok0, PruneOpts o) {
+  const int bh = blockIdx.x * (256 / kWave) + threadIdx.x / kWave;
+  if (bh >= c.BH) return;
+  const int64_t row = (int64_t)bh * kTile * T;
+  append_one_variant<T>(c, o, bh, tok0, x + row, o.weights ? o.weights + row : nullptr, lane_id());
 }
 
 // One wave per stream, 4 streams per 256-thread block.
@@ -570,6 +703,59 @@ hipError_t launch_append(const CacheView& c, const uint16_t* x, int tok0, hipStr
     case 4: return append_T<4>(c, x, tok0, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+template <int T>
+static hipError_t compress_variant_T(const CacheView& c, const uint16_t* x, int n_new, int tok0,
+                                     uint32_t* ws, hipStream_t s, const PruneOpts& o) {
+  const int64_t waves = ((int64_t)c.BH * n_new + kTokPerWave - 1) / kTokPerWave;
+  hipLaunchKernelGGL(k_select<T>, dim3((uint32_t)((waves + 3) / 4)), dim3(256), 0, s, c, x, n_new,
+                     (int64_t)n_new, tok0, o);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int n_chunks = (n_new + compress_chunk_tokens(T) - 1) / compress_chunk_tokens(T);
+  const int64_t n_wg = (int64_t)c.BH * n_chunks;
+  uint64_t* flags = reinterpret_cast<uint64_t*>(ws);
+  uint32_t* ticket = reinterpret_cast<uint32_t*>(flags + n_wg);
+  const int64_t words = 2 * n_wg + 1;
+  const int clear_blocks = (int)((words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024);
+  hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, words);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL((k_compress<T, true>), dim3((uint32_t)n_wg), dim3(kWave), 0, s, x, n_new, 0,
+                     c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
+                     flags, ticket, n_chunks, (int64_t)n_new);
+  return hipGetLastError();
+}
+
+hipError_t launch_compress_variant(const CacheView& c, const uint16_t* x, int n_new, int tok0,
+                                   uint32_t* ws, hipStream_t s, const PruneOpts& o) {
+  switch (c.T) {
+    case 1: return compress_variant_T<1>(c, x, n_new, tok0, ws, s, o);
+    case 2: return compress_variant_T<2>(c, x, n_new, tok0, ws, s, o);
+    case 4: return compress_variant_T<4>(c, x, n_new, tok0, ws, s, o);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_append_variant(const CacheView& c, const uint16_t* x, int tok0, hipStream_t s,
+                                 const PruneOpts& o) {
+  dim3 grid((c.BH + 3) / 4);
+  switch (c.T) {
+    case 1: hipLaunchKernelGGL(k_append_variant<1>, grid, dim3(256), 0, s, c, x, tok0, o); break;
+    case 2: hipLaunchKernelGGL(k_append_variant<2>, grid, dim3(256), 0, s, c, x, tok0, o); break;
+    case 4: hipLaunchKernelGGL(k_append_variant<4>, grid, dim3(256), 0, s, c, x, tok0, o); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_query_lookahead(const uint16_t* q, int B, int Hq, int Hkv, int n_q, int T, int L,
+                                  float* w, hipStream_t s) {
+  const int64_t n = (int64_t)B * Hkv * n_q * kTile * T;
+  int blocks = (int)((n + 255) / 256);
+  blocks = blocks < 1 ? 1 : (blocks > 65536 ? 65536 : blocks);
+  hipLaunchKernelGGL(k_query_lookahead, dim3(blocks), dim3(256), 0, s, q, B, Hq, Hkv, n_q, kTile * T, L, w);
+  return hipGetLastError();
 }
 
 hipError_t launch_window_fill(const WindowView& w, int b, int d, const uint16_t* xk,

@@ -33,6 +33,28 @@ hipError_t launch_compress(const CacheView& c, const uint16_t* x, int n_new, int
 // Compress one token per stream (x: [BH][64T]) as token tok0.
 hipError_t launch_append(const CacheView& c, const uint16_t* x, int tok0, hipStream_t s);
 
+// Pruner variants of the same format (the magnitude top-k of k_compress is the
+// default): per-head kept counts, 2:4 per token, output-aware key scores.
+constexpr int kPruneMagnitude = 0, kPrune24 = 1, kPruneOutputAware = 2;
+constexpr int kMaxPruneHeads = 256;
+struct PruneOpts {
+  int mode;
+  int H;                      // kv-heads: stream s is head s % H
+  int per_head;               // head_keep holds each head's kept count
+  const float* weights;       // output-aware: fp32 [BH][x_stride][64T] channel weights
+  int32_t head_keep[kMaxPruneHeads];
+};
+// Selection (bitmaps of tokens tok0.., one wave per token) then packing with the
+// given bitmaps (k_compress in its preset mode).
+hipError_t launch_compress_variant(const CacheView& c, const uint16_t* x, int n_new, int tok0,
+                                   uint32_t* ws, hipStream_t s, const PruneOpts& o);
+hipError_t launch_append_variant(const CacheView& c, const uint16_t* x, int tok0, hipStream_t s,
+                                 const PruneOpts& o);
+// Output-aware weights: w[b][h][T][c] = sum over t = T .. min(T+L, Nq)-1, then over
+// the G query heads of h, of |q[b][h*G+g][t][c]| (fp32, in that order).
+hipError_t launch_query_lookahead(const uint16_t* q, int B, int Hq, int Hkv, int n_q, int T, int L,
+                                  float* w, hipStream_t s);
+
 // One window step per active batch entry (see mustafar_window_step): the ring
 // slots k, v [BH][W][64T], device state len/head/n_comp [B], H streams per entry.
 struct WindowView {

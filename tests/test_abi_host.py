@@ -263,3 +263,30 @@ def test_window_calls_reject_before_launch(lib):
     assert att(B=3) == mf.EINVAL
     assert att(Hq=12) == mf.EUNSUPPORTED
     assert att(ws_bytes=anb - 4) == mf.EWORKSPACE
+
+
+def test_prune_variants_reject_before_launch(lib):
+    c, _ = _fake_cache(B=2, H=4, cap=100, s=0.5)
+    x, ws = 0x500000, 0x600000
+    need = lib.mustafar_compress_workspace_bytes(2, 4, 50)
+    o = mf.prune_opts_t()
+    call = lambda opts, **kw: lib.mustafar_prune_compress_ex(  # noqa: E731
+        ctypes.byref(kw.get("c", c)), x, kw.get("n", 50), ctypes.byref(opts), ws, need, None)
+    o.mode = 7
+    assert call(o) == mf.EINVAL                       # unknown mode
+    o.mode = mf.PRUNE_OUTPUT_AWARE
+    assert call(o) == mf.EINVAL                       # output-aware without weights
+    o.mode = mf.PRUNE_2_4
+    c7, _ = _fake_cache(B=2, H=4, cap=100, s=0.7)
+    assert call(o, c=c7) == mf.EINVAL                 # 2:4 needs n_keep = d/2
+    hk = (ctypes.c_int32 * 4)(64, 64, 65, 1)
+    o.mode = mf.PRUNE_MAGNITUDE
+    o.head_keep = ctypes.cast(hk, ctypes.c_void_p)
+    assert call(o) == mf.EINVAL                       # a head above the cache's n_keep
+    o2 = mf.prune_opts_t()
+    o2.mode = mf.PRUNE_2_4
+    o2.head_keep = ctypes.cast(hk, ctypes.c_void_p)
+    assert call(o2) == mf.EINVAL                      # 2:4 takes no per-head counts
+    assert lib.mustafar_query_lookahead(0x700000, 1, 6, 4, 10, 128, 32, 0x800000, None) == mf.EINVAL
+    assert lib.mustafar_query_lookahead(0x700000, 1, 8, 4, 10, 128, 0, 0x800000, None) == mf.EINVAL
+    assert lib.mustafar_query_lookahead(0x700008, 1, 8, 4, 10, 128, 32, 0x800000, None) == mf.EINVAL
