@@ -43,6 +43,7 @@ def parse():
     ap.add_argument("--seed", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-window", action="store_true", help="skip the dense-window lifecycle leg")
+    ap.add_argument("--no-variants", action="store_true", help="skip the pruner-variant leg")
     ap.add_argument("--cpu-sample-streams", type=int, default=256)
     ap.add_argument("--cpu-threads", type=int, default=0, help="0: min(16, cpu count)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -307,6 +308,50 @@ def main():
                          f"{w.n_tail} tokens per stream"}
         del Kw, Vw, win
 
+    # ---- pruner variants on the same prefill cache (K: N tokens per stream) ----
+    variants = None
+    if not args.no_variants:
+        torch.cuda.empty_cache()
+        Kv = mf.CompressedCache(w.B, w.Hkv, w.d, 0.5, w.N, device=dev)
+
+        def timed(fn, reps=3):
+            ts = []
+            for _ in range(reps):
+                Kv.desc.n_tokens = 0
+                a, b = ev(), ev()
+                a.record()
+                fn()
+                b.record()
+                torch.cuda.synchronize()
+                ts.append(a.elapsed_time(b) / 1e3)
+            return float(np.median(ts))
+
+        toks = w.B * w.Hkv * w.N
+        t24 = timed(lambda: mf.mustafar_prune_compress_ex(Kv, Kp, mode=mf.PRUNE_2_4, ws=ws_c))
+        hk = [Kv.n_keep if h % 2 == 0 else Kv.n_keep // 2 for h in range(w.Hkv)]
+        thead = timed(lambda: mf.mustafar_prune_compress_ex(Kv, Kp, head_keep=hk, ws=ws_c))
+        # output-aware keys: the lookahead weights of the queries at every position
+        gqh = torch.Generator(device=dev)
+        gqh.manual_seed(args.seed + 1)
+        qhist = torch.randn((w.B, w.Hq, w.N, w.d), generator=gqh, device=dev).half()
+        wts = torch.empty((w.B, w.Hkv, w.N, w.d), dtype=torch.float32, device=dev)
+        a, b = ev(), ev()
+        a.record()
+        mf.mustafar_query_lookahead(qhist, w.Hkv, 32, out=wts)
+        b.record()
+        torch.cuda.synchronize()
+        t_look = a.elapsed_time(b) / 1e3
+        toa = timed(lambda: mf.mustafar_prune_compress_ex(Kv, Kp, mode=mf.PRUNE_OUTPUT_AWARE,
+                                                          weights=wts, ws=ws_c))
+        variants = {"cache": "K, 50%", "tokens": toks,
+                    "two_four_tokens_per_s": toks / t24,
+                    "per_head_tokens_per_s": toks / thead,
+                    "output_aware_tokens_per_s": toks / toa,
+                    "query_lookahead_ms": t_look * 1e3,
+                    "magnitude_tokens_per_s_for_reference": 2 * toks / t_pc}
+        del Kv, qhist, wts
+        torch.cuda.empty_cache()
+
     ceiling = read_ceiling_gbs()
 
     result = {
@@ -344,6 +389,7 @@ def main():
                            "traffic": measured_traffic("k_compress", w.name, "bytes_k_plus_v")},
         "append_us_per_step": (total_s / steps - attn_s) * 1e6,
         "window_lifecycle": window,
+        "prune_variants": variants,
         "compression_ratio": comp_kv / dense_kv,
         "wall_s_timed": wall,
     }
