@@ -120,6 +120,7 @@ struct SparseLds {
 };
 
 constexpr int kHalfSlots = 33;
+constexpr float kSlack = 8.f;  // log2 headroom of the lazy softmax base
 constexpr uint32_t kPvRow = 32;  // dwords per half-tile row (T x NBH)
 
 // Bytes per tile of the q table: 49 dwords, so the two tiles of d = 128 sit 17
@@ -226,6 +227,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   for (int h = 0; h < 2; ++h)
 #pragma unroll
     for (int k = 0; k < PU::UPL; ++k) oh[h][k] = 0.f;
+  float l_lane = 0.f;
 
   for (int b0 = j0; b0 < j1; b0 += NB) {
     // Software pipeline: fetch the next block's values and the metadata after it.
@@ -245,17 +247,24 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
       key_walk(wc.klo, wc.khi, cur.kb, va, q_w0, q_w1, q31, q63, acc);
     }
     {
+      // Online softmax with a lazy base: m_run moves only when a score passes it
+      // by more than kSlack, so p = exp2(score - m_run) stays below 2^kSlack
+      // (well inside fp16) and most blocks need neither a wave-wide maximum nor
+      // a rescale. The sum of p is kept per lane and reduced once at the end.
       const bool valid = (int)j < nb;
       const float sc = valid ? tile_sum<T>(acc) * a.scale_log2 : -INFINITY;
-      const float mnew = fmaxf(m_run, wave_max_u(sc));
-      const float alpha = __builtin_amdgcn_exp2f(m_run - mnew);
-      const _Float16 ph = valid ? (_Float16)__builtin_amdgcn_exp2f(sc - mnew) : (_Float16)0.f;
-      l_run = l_run * alpha + wave_sum_u(t == 0 ? (float)ph : 0.f);
-      m_run = mnew;
+      if (ballot(sc > m_run + kSlack)) {
+        const float mnew = fmaxf(m_run, wave_max_u(sc));
+        const float alpha = __builtin_amdgcn_exp2f(m_run - mnew);
+        l_lane *= alpha;
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int k = 0; k < PU::UPL; ++k) oh[h][k] *= alpha;
+          for (int k = 0; k < PU::UPL; ++k) oh[h][k] *= alpha;
+        m_run = mnew;
+      }
+      const _Float16 ph = valid ? (_Float16)__builtin_amdgcn_exp2f(sc - m_run) : (_Float16)0.f;
+      l_lane += t == 0 ? (float)ph : 0.f;
       if (t == 0) lds_store<_Float16>(base + L.ps + (j % PU::NBH) * 4 + (j / PU::NBH) * 2, ph);
     }
 
@@ -317,6 +326,8 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
     nb = nb_next;
     nb_next = nb_next2;
   }
+
+  l_run = wave_sum_u(l_lane);
 
   // Back to the partial layout (lane = channel of each tile): channel `lane`
   // of tile tt is channel lane % 32 of half lane / 32, unit (lane % 32) T + tt.
