@@ -18,6 +18,10 @@ loops over streams:
   pruner variants in the same format: 2:4 per token (Appendix B), output-aware
   key pruning (Sec. 2), per-head kept counts (Sec. 4.5's finer-grained
   sparsity); ``query_lookahead`` -- the channel weights of output-aware pruning.
+* ``prune_channel_group``, ``compress_grouped`` -- per-channel value pruning in
+  groups of 32 tokens, by magnitude or output-aware (Sec. 2's value-cache
+  study), in the same format; ``attention_probs`` -- the softmax weights of
+  Algorithm 1, which the output-aware form accumulates per token.
 
 Streams are independent, so the batched helpers accept ``threads``: ctypes
 releases the GIL during each C call and streams are spread over a thread pool.
@@ -37,6 +41,7 @@ _SRC = os.path.join(_HERE, "mustafar_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 TILE = 64
 PAD = 8
+GROUP = 32  # tokens per per-channel pruning group (Sec. 2, value cache)
 
 _lib = None
 
@@ -98,6 +103,11 @@ def _bind(lib):
     lib.oracle_encode_stream.argtypes = [P, P, ctypes.c_int, ctypes.c_int, P, P, P,
                                          ctypes.c_int64, P]
     lib.oracle_encode_stream.restype = ctypes.c_int
+    lib.oracle_prune_channel_group.argtypes = [P, P, ctypes.c_int, ctypes.c_int, ctypes.c_int, P]
+    lib.oracle_prune_channel_group.restype = None
+    lib.oracle_attention_probs.argtypes = [P, ctypes.c_int, ctypes.c_int, P, ctypes.c_int, P,
+                                           ctypes.c_int, ctypes.c_double, P]
+    lib.oracle_attention_probs.restype = ctypes.c_int
     return lib
 
 
@@ -357,3 +367,126 @@ def compressed_bytes(enc: dict) -> int:
     2 bytes per stored fp16 element (padding included)."""
     tiles = enc["bitmaps"].size
     return 12 * tiles + 2 * int(enc["stream_len"].astype(np.int64).sum())
+
+
+# ---- per-channel value pruning in groups of 32 tokens ------------------------------------
+def prune_channel_group(x, k: int, w=None) -> np.ndarray:
+    """Keep-mask [n][d] of a group of n tokens x [n][d]: per channel the k tokens
+    of largest |x| (or, with token weights w float32 [n], of largest fp32
+    |x| * w_j), ties to the lower token."""
+    xb = np.ascontiguousarray(_bits(x))
+    n, d = xb.shape
+    keep = np.zeros((n, d), dtype=np.uint8)
+    wf = None if w is None else np.ascontiguousarray(np.asarray(w, dtype=np.float32).reshape(-1))
+    _load().oracle_prune_channel_group(_ptr(xb), _ptr(wf), n, d, int(k), _ptr(keep))
+    return keep.astype(bool)
+
+
+def grouped_stream_capacity(d: int, k: int, n_tokens: int) -> int:
+    """Worst-case fp16 elements of n_tokens (a multiple of 32) pruned per channel:
+    per group k * d kept values plus at most 7 pad slots in each of its 32 * T tiles."""
+    T = d // TILE
+    return n_tokens // GROUP * (k * d + GROUP * T * (PAD - 1))
+
+
+def compress_grouped(x, sparsity: float | None = None, *, k: int | None = None, weights=None,
+                     threads: int = 1) -> dict:
+    """The compressed format of x [B][H][N][d] (N a multiple of 32) pruned per
+    channel in groups of 32 consecutive tokens: each channel keeps k =
+    keep_count(32, sparsity) of every group (output-aware with token weights
+    float32 [B][H][N] if given). Same dict as ``compress``; ``n_keep`` is k."""
+    xb = _bits(x)
+    B, H, N, d = xb.shape
+    if N % GROUP:
+        raise ValueError("per-channel pruning takes whole groups of 32 tokens")
+    if k is None:
+        k = keep_count(GROUP, sparsity)
+    T = d // TILE
+    cap = max(grouped_stream_capacity(d, k, N), PAD)
+    bitmaps = np.zeros((B, H, N, T), dtype=np.uint64)
+    offsets = np.zeros((B, H, N, T), dtype=np.uint32)
+    values = np.zeros((B, H, cap), dtype=np.uint16)
+    stream_len = np.zeros((B, H), dtype=np.uint32)
+    wts = None if weights is None else np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
+    lib = _load()
+
+    def one(bh):
+        b, h = bh
+        xs = np.ascontiguousarray(xb[b, h])
+        keep = np.zeros((N, d), dtype=np.uint8)
+        for g0 in range(0, N, GROUP):
+            part = np.zeros((GROUP, d), dtype=np.uint8)
+            wg = None if wts is None else np.ascontiguousarray(wts[b, h, g0:g0 + GROUP])
+            lib.oracle_prune_channel_group(_ptr(np.ascontiguousarray(xs[g0:g0 + GROUP])), _ptr(wg),
+                                           GROUP, d, int(k), _ptr(part))
+            keep[g0:g0 + GROUP] = part
+        out_len = np.zeros(1, dtype=np.uint32)
+        bm = np.zeros((N, T), dtype=np.uint64)
+        off = np.zeros((N, T), dtype=np.uint32)
+        val = np.zeros(cap, dtype=np.uint16)
+        rc = lib.oracle_encode_stream(_ptr(xs), _ptr(keep), N, d, _ptr(bm), _ptr(off), _ptr(val),
+                                      cap, _ptr(out_len))
+        if rc != 0:
+            raise ValueError(f"oracle_encode_stream failed with {rc}")
+        bitmaps[b, h], offsets[b, h], values[b, h], stream_len[b, h] = bm, off, val, out_len[0]
+
+    _map(one, [(b, h) for b in range(B) for h in range(H)], threads)
+    return {"bitmaps": bitmaps, "offsets": offsets, "values": values,
+            "stream_len": stream_len, "n_keep": int(k), "d": d}
+
+
+def encode(x, keep, threads: int = 1) -> dict:
+    """The compressed format of x [B][H][N][d] with the kept channels given by
+    keep [B][H][N][d] (bool). Same dict as ``compress`` (``n_keep`` is d)."""
+    xb = _bits(x)
+    B, H, N, d = xb.shape
+    T = d // TILE
+    cap = max(N * d, PAD)
+    kp = np.ascontiguousarray(np.asarray(keep, dtype=np.uint8))
+    bitmaps = np.zeros((B, H, N, T), dtype=np.uint64)
+    offsets = np.zeros((B, H, N, T), dtype=np.uint32)
+    values = np.zeros((B, H, cap), dtype=np.uint16)
+    stream_len = np.zeros((B, H), dtype=np.uint32)
+    lib = _load()
+
+    def one(bh):
+        b, h = bh
+        out_len = np.zeros(1, dtype=np.uint32)
+        bm = np.zeros((N, T), dtype=np.uint64)
+        off = np.zeros((N, T), dtype=np.uint32)
+        val = np.zeros(cap, dtype=np.uint16)
+        rc = lib.oracle_encode_stream(_ptr(np.ascontiguousarray(xb[b, h])),
+                                      _ptr(np.ascontiguousarray(kp[b, h])), N, d, _ptr(bm),
+                                      _ptr(off), _ptr(val), cap, _ptr(out_len))
+        if rc != 0:
+            raise ValueError(f"oracle_encode_stream failed with {rc}")
+        bitmaps[b, h], offsets[b, h], values[b, h], stream_len[b, h] = bm, off, val, out_len[0]
+
+    _map(one, [(b, h) for b in range(B) for h in range(H)], threads)
+    return {"bitmaps": bitmaps, "offsets": offsets, "values": values,
+            "stream_len": stream_len, "n_keep": d, "d": d}
+
+
+def attention_probs(q, kc, k_tail=None, scale: float = 0.0) -> np.ndarray:
+    """Softmax weights of Algorithm 1 in float64: q [B][Hq][d], kc [B][Hkv][Ns][d]
+    zero-filled pruned keys, k_tail [B][Hkv][Nd][d] or None. Returns [B][Hq][Ns+Nd]
+    (compressed tokens first, then the dense ones)."""
+    qb, kcb = _bits(q), _bits(kc)
+    B, Hq, d = qb.shape
+    Hkv, Ns = kcb.shape[1], kcb.shape[2]
+    klb = np.zeros((B, Hkv, 0, d), dtype=np.uint16) if k_tail is None else _bits(k_tail)
+    Nd = klb.shape[2]
+    G = Hq // Hkv
+    out = np.zeros((B, Hq, Ns + Nd), dtype=np.float64)
+    lib = _load()
+    for b in range(B):
+        for h in range(Hkv):
+            p = np.zeros((G, Ns + Nd), dtype=np.float64)
+            rc = lib.oracle_attention_probs(
+                _ptr(np.ascontiguousarray(qb[b, h * G:(h + 1) * G])), G, d,
+                _ptr(np.ascontiguousarray(kcb[b, h])), Ns, _ptr(np.ascontiguousarray(klb[b, h])), Nd,
+                float(scale), _ptr(p))
+            if rc != 0:
+                raise ValueError(f"oracle_attention_probs failed with {rc}")
+            out[b, h * G:(h + 1) * G] = p
+    return out

@@ -143,6 +143,39 @@ void oracle_prune_token_scored(const uint16_t* x, const float* w, int d, int k, 
     free(r);
 }
 
+/* Per-channel pruning of one group of n consecutive tokens of a stream
+ * (Sec. 2, value-cache study: every channel is pruned to the target sparsity
+ * within groups of 32 tokens). For each channel c the k of the n tokens with
+ * the largest key are kept; equal keys go to the lower token. The key is
+ * |x_jc| in the magnitude form (w NULL); in the output-aware form it is the
+ * fp32 product |x_jc| * w_j, rounded once, where w_j >= 0 is the attention
+ * probability mass token j received (summed over its queries). The selection is
+ * thus decided in the precision the GPU decides it in.
+ * x, keep: [n][d]. */
+void oracle_prune_channel_group(const uint16_t* x, const float* w, int n, int d, int k,
+                                uint8_t* keep)
+{
+    ranked_t* r = (ranked_t*)malloc(sizeof(ranked_t) * (size_t)(n > 0 ? n : 1));
+    for (int c = 0; c < d; ++c) {
+        for (int j = 0; j < n; ++j) {
+            const double mag = fabs(oracle_half_to_double(x[(int64_t)j * d + c]));
+            if (w) {
+                const float score = (float)mag * w[j];
+                r[j].mag = (double)score;
+            } else {
+                r[j].mag = mag;
+            }
+            r[j].idx = j;
+        }
+        qsort(r, (size_t)n, sizeof(ranked_t), rank_cmp);
+        for (int j = 0; j < n; ++j)
+            keep[(int64_t)j * d + c] = 0;
+        for (int i = 0; i < k && i < n; ++i)
+            keep[(int64_t)r[i].idx * d + c] = 1;
+    }
+    free(r);
+}
+
 /* ---------------------------------------------------------------------------
  * Bitmap-based compressed format (Sec. 3; padding and offset overhead Sec. 4.3).
  * One stream = the tokens of one (batch, kv-head).  T = d/64 tiles per token.
@@ -229,6 +262,42 @@ int oracle_decompress_stream(const uint64_t* bitmaps, const uint32_t* offsets,
                 x_out[(int64_t)j * d + t * ORACLE_TILE + i] = v;
             }
         }
+    return 0;
+}
+
+/* The attention probabilities of Algorithm 1 for one kv-head: the softmax
+ * over concat(S_C, S_L) of the scores scale * q_g . k_j, for each of the G
+ * query heads. probs: [G][n_s + n_d] double. Output-aware per-channel value
+ * pruning (Sec. 2) weighs value token j by the probability mass it receives. */
+int oracle_attention_probs(const uint16_t* q, int G, int d, const uint16_t* kc, int n_s,
+                           const uint16_t* kl, int n_d, double scale, double* probs)
+{
+    const int n_all = n_s + n_d; /* every token of concat(S_C, S_L) */
+    if (n_all <= 0 || d <= 0 || G <= 0)
+        return -1;
+    if (scale <= 0.0)
+        scale = 1.0 / sqrt((double)d);
+    for (int g = 0; g < G; ++g) {
+        double* p = probs + (int64_t)g * n_all;
+        for (int j = 0; j < n_all; ++j) {
+            const uint16_t* kj = (j < n_s) ? kc + (int64_t)j * d : kl + (int64_t)(j - n_s) * d;
+            double acc = 0.0;
+            for (int c = 0; c < d; ++c)
+                acc += oracle_half_to_double(q[(int64_t)g * d + c]) * oracle_half_to_double(kj[c]);
+            p[j] = scale * acc;
+        }
+        double m = p[0];
+        for (int j = 1; j < n_all; ++j)
+            if (p[j] > m)
+                m = p[j];
+        double l = 0.0;
+        for (int j = 0; j < n_all; ++j) {
+            p[j] = exp(p[j] - m);
+            l += p[j];
+        }
+        for (int j = 0; j < n_all; ++j)
+            p[j] /= l;
+    }
     return 0;
 }
 

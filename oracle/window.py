@@ -22,7 +22,8 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import compress, decode_attention, prune_token, sparse_decode_attention
+from . import (GROUP, attention_probs, compress, decode_attention, decompress, encode,
+               keep_count, prune_channel_group, prune_token, sparse_decode_attention)
 
 
 class WindowOracle:
@@ -115,3 +116,113 @@ class WindowOracle:
 def _keep_count(d: int, sparsity: float) -> int:
     from . import keep_count
     return keep_count(d, sparsity)
+
+
+class GroupedWindowOracle:
+    """The window lifecycle of per-channel value pruning in groups of 32 tokens
+    (Sec. 2, value-cache study), for B entries with H kv-heads of dimension d.
+
+    An entry's compressed prefix is always whole groups. A prefill of n tokens
+    compresses the first 32 * floor((n - 1) / 32) (values by per-channel
+    magnitude) and keeps the rest, 1 to 32 tokens, dense. A decode step first
+    lets a full window (W tokens) hand its oldest 32 tokens over as one group,
+    then appends the new token. Keys are pruned per token (magnitude, sk);
+    values per channel within each group (keep_count(32, sv) tokens per channel),
+    by magnitude or, when the step is given that group's token weights, by the
+    fp32 key |v| * w_j. The window a token sits in is thus at least 32 steps
+    old when it leaves, and the output-aware weight of a token is the sum of
+    the attention probabilities it received (over the query heads of its
+    kv-head) in the step it arrived and the 31 after: ``score_increments``
+    gives a step's contributions.
+    """
+
+    def __init__(self, B: int, H: int, d: int, W: int, sk: float, sv: float):
+        assert W >= 2 * GROUP and W % GROUP == 0
+        self.B, self.H, self.d, self.W = B, H, d, W
+        self.sk, self.sv = sk, sv
+        self.hist_k = [[] for _ in range(B)]
+        self.hist_v = [[] for _ in range(B)]
+        self.ncomp = [0] * B
+        # per entry, one entry per compressed group: None (magnitude) or float32 [H][32]
+        self.group_w = [[] for _ in range(B)]
+
+    def prefill(self, xk, xv, seq_len) -> None:
+        xk = np.asarray(xk).view(np.uint16)
+        xv = np.asarray(xv).view(np.uint16)
+        for b in range(self.B):
+            n = int(seq_len[b])
+            for j in range(n):
+                self.hist_k[b].append(np.array(xk[b, :, j]))
+                self.hist_v[b].append(np.array(xv[b, :, j]))
+            self.ncomp[b] = 0 if n == 0 else (n - 1) // GROUP * GROUP
+            self.group_w[b] = [None] * (self.ncomp[b] // GROUP)
+
+    def step(self, k_new, v_new, active=None, weights=None) -> None:
+        """weights: None, or a dict {b: float32 [H][32] or None} with the token
+        weights of the group entry b hands over in this step (if any)."""
+        k_new = np.asarray(k_new).view(np.uint16)
+        v_new = np.asarray(v_new).view(np.uint16)
+        for b in range(self.B):
+            if active is not None and not active[b]:
+                continue
+            if self.window_len(b) == self.W:
+                self.ncomp[b] += GROUP
+                w = None if weights is None else weights.get(b)
+                self.group_w[b].append(None if w is None else np.asarray(w, dtype=np.float32))
+            self.hist_k[b].append(np.array(k_new[b]))
+            self.hist_v[b].append(np.array(v_new[b]))
+
+    def arrived(self, b: int) -> int:
+        return len(self.hist_k[b])
+
+    def n_comp(self, b: int) -> int:
+        return self.ncomp[b]
+
+    def window_len(self, b: int) -> int:
+        return self.arrived(b) - self.ncomp[b]
+
+    def _tokens(self, hist, b: int, lo: int, hi: int) -> np.ndarray:
+        if hi <= lo:
+            return np.zeros((self.H, 0, self.d), dtype=np.uint16)
+        return np.stack(hist[b][lo:hi], axis=1)
+
+    def window(self, b: int):
+        lo, hi = self.ncomp[b], self.arrived(b)
+        return self._tokens(self.hist_k, b, lo, hi), self._tokens(self.hist_v, b, lo, hi)
+
+    def compressed(self, b: int):
+        """(K, V) compressed streams of entry b in the oracle's format (B = 1)."""
+        n = self.ncomp[b]
+        k = self._tokens(self.hist_k, b, 0, n)[None]
+        v = self._tokens(self.hist_v, b, 0, n)[None]
+        enc_k = compress(k, self.sk)
+        gk = keep_count(GROUP, self.sv)
+        keep = np.zeros((1, self.H, n, self.d), dtype=bool)
+        for g, w in enumerate(self.group_w[b]):
+            for h in range(self.H):
+                keep[0, h, g * GROUP:(g + 1) * GROUP] = prune_channel_group(
+                    v[0, h, g * GROUP:(g + 1) * GROUP], gk, None if w is None else w[h])
+        return enc_k, encode(v, keep)
+
+    def attention(self, q, b: int, scale: float = 0.0) -> np.ndarray:
+        q = np.asarray(q).view(np.uint16)[None]
+        enc_k, enc_v = self.compressed(b)
+        wk, wv = self.window(b)
+        return sparse_decode_attention(q, enc_k, enc_v, wk[None], wv[None], scale)[0]
+
+    def score_increments(self, q, b: int, scale: float = 0.0) -> np.ndarray:
+        """float64 [H][len]: for every window token of entry b younger than 32
+        steps (the newest 32), the attention probability it receives from q
+        [Hq][d], summed over the query heads of each kv-head; 0 for older ones."""
+        q = np.asarray(q).view(np.uint16)[None]
+        enc_k, _ = self.compressed(b)
+        wk, _ = self.window(b)
+        p = attention_probs(q, decompress(enc_k), wk[None], scale)[0]
+        n, L = self.ncomp[b], self.window_len(b)
+        G = q.shape[1] // self.H
+        out = np.zeros((self.H, L), dtype=np.float64)
+        for h in range(self.H):
+            tot = p[h * G:(h + 1) * G, n:].sum(axis=0)
+            young = np.arange(L) >= L - GROUP
+            out[h] = np.where(young, tot, 0.0)
+        return out

@@ -130,3 +130,59 @@ def test_planted_variant_mistake_is_caught(tmp_path, name, orig, planted):
     so = _build(tmp_path, text.replace(orig, planted), "vmut")
     with oracle.using_library(so):
         assert _variant_battery() is not None, f"no pin caught: {name}"
+
+
+CHANNEL_MUTATIONS = [
+    ("channel group keeps one more", "for (int i = 0; i < k && i < n; ++i)\n            keep[(int64_t)r[i].idx * d + c] = 1;",
+     "for (int i = 0; i <= k && i < n; ++i)\n            keep[(int64_t)r[i].idx * d + c] = 1;"),
+    ("channel key ignores the token weights", "const float score = (float)mag * w[j];",
+     "const float score = (float)mag;"),
+    ("channel key ignores the magnitude", "const float score = (float)mag * w[j];",
+     "const float score = w[j];"),
+    ("channel key kept in double", "const float score = (float)mag * w[j];\n                r[j].mag = (double)score;",
+     "r[j].mag = mag * (double)w[j];"),
+    ("channel and token indexes swapped",
+     "const double mag = fabs(oracle_half_to_double(x[(int64_t)j * d + c]));",
+     "const double mag = fabs(oracle_half_to_double(x[(int64_t)c * n + j]));"),
+    ("channel ranked by signed value",
+     "const double mag = fabs(oracle_half_to_double(x[(int64_t)j * d + c]));",
+     "const double mag = oracle_half_to_double(x[(int64_t)j * d + c]);"),
+    ("probabilities without the scale", "p[j] = scale * acc;", "p[j] = acc;"),
+    ("probabilities not normalised", "p[j] /= l;", "p[j] /= 1.0;"),
+    ("probabilities without the dense tokens", "const int n_all = n_s + n_d;",
+     "const int n_all = n_s;"),
+]
+
+
+def _channel_battery():
+    from tests import test_oracle_channel as ch
+    checks = [
+        ("argsort", lambda: ch.test_channel_prune_equals_stable_argsort(10)),
+        ("brute force", ch.test_channel_prune_equals_brute_force),
+        ("oa numpy", lambda: ch.test_output_aware_channel_prune_equals_numpy_float32(10)),
+        ("oa invariances", ch.test_output_aware_invariances),
+        ("oa fp32", ch.test_output_aware_key_is_rounded_to_fp32),
+        ("probs", lambda: ch.test_attention_probs_equal_numpy_softmax(4)),
+        ("probs x values", ch.test_attention_output_equals_probabilities_times_values),
+    ]
+    for name, fn in checks:
+        try:
+            fn()
+        except Exception:  # noqa: BLE001 - any failure of a pin counts
+            return name
+    return None
+
+
+def test_unmodified_oracle_passes_the_channel_battery(tmp_path):
+    so = _build(tmp_path, open(SRC).read(), "cclean")
+    with oracle.using_library(so):
+        assert _channel_battery() is None
+
+
+@pytest.mark.parametrize("name,orig,planted", CHANNEL_MUTATIONS, ids=[m[0] for m in CHANNEL_MUTATIONS])
+def test_planted_channel_mistake_is_caught(tmp_path, name, orig, planted):
+    text = open(SRC).read()
+    assert text.count(orig) == 1, f"mutation anchor not unique: {orig!r}"
+    so = _build(tmp_path, text.replace(orig, planted), "cmut")
+    with oracle.using_library(so):
+        assert _channel_battery() is not None, f"no pin caught: {name}"

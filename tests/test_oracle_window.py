@@ -9,6 +9,7 @@ attention computed without the compressed format.
 import numpy as np
 import pytest
 
+import oracle
 from oracle.window import WindowOracle
 
 D = 64
@@ -97,3 +98,92 @@ def test_attention_equals_the_direct_computation(G):
         a = o.attention(q[b], b)
         r = o.attention_direct(q[b], b)
         np.testing.assert_allclose(a, r, rtol=0, atol=1e-12)
+
+
+# ---- the grouped lifecycle (per-channel value pruning in groups of 32) -------------------
+from oracle.window import GroupedWindowOracle  # noqa: E402
+
+
+@pytest.mark.parametrize("W", [64, 96])
+def test_grouped_counts_follow_the_closed_form(W):
+    """n_comp stays whole groups; a prefill of n leaves 1..32 tokens dense; a
+    window graduates 32 tokens exactly when it holds W before a push."""
+    rng = np.random.default_rng(11)
+    B, H = 4, 1
+    seq = [1, 32, 33, 100]
+    xk = _indexed_tokens(B, H, 100, D, rng)
+    o = GroupedWindowOracle(B, H, D, W, 0.5, 0.7)
+    o.prefill(xk, xk, seq)
+    comp = [(n - 1) // 32 * 32 for n in seq]
+    lens = [n - c for n, c in zip(seq, comp)]
+    assert [o.n_comp(b) for b in range(B)] == comp
+    assert all(1 <= L <= 32 for L in lens)
+    for s in range(3 * W):
+        act = [1, s % 2, 1, s % 3 != 0]
+        t = rng.standard_normal((B, H, D)).astype(np.float16)
+        o.step(t, t, act)
+        for b in range(B):
+            if act[b]:
+                if lens[b] == W:
+                    comp[b] += 32
+                    lens[b] -= 32
+                lens[b] += 1
+            assert o.n_comp(b) == comp[b] and o.window_len(b) == lens[b]
+            assert comp[b] % 32 == 0 and 1 <= lens[b] <= W
+
+
+def test_grouped_window_tokens_and_groups():
+    rng = np.random.default_rng(12)
+    B, H, W = 1, 2, 64
+    xk = _indexed_tokens(B, H, 40, D, rng)
+    o = GroupedWindowOracle(B, H, D, W, 0.5, 0.7)
+    o.prefill(xk, xk, [40])
+    for s in range(60):
+        t = rng.standard_normal((B, H, D)).astype(np.float16)
+        t[..., 0] = np.float16(40 + s)
+        o.step(t, t)
+    wk, _ = o.window(0)
+    idx = wk[0, :, 0].view(np.float16).astype(np.float64)
+    assert list(idx) == list(range(64, 100))      # 100 arrivals, 64 compressed
+    # Every compressed group keeps exactly keep_count(32, 0.7) = 10 tokens per channel.
+    _, ev = o.compressed(0)
+    bm = ev["bitmaps"][0, 0]
+    for g in range(2):
+        for c in range(D):
+            kept = sum((int(bm[g * 32 + j, 0]) >> c) & 1 for j in range(32))
+            assert kept == 10
+
+
+@pytest.mark.parametrize("G", [1, 4])
+def test_grouped_attention_and_scores_against_direct_computation(G):
+    rng = np.random.default_rng(13 + G)
+    B, H, W = 2, 2, 64
+    xk = rng.standard_normal((B, H, 70, D)).astype(np.float16)
+    xv = rng.standard_normal((B, H, 70, D)).astype(np.float16)
+    o = GroupedWindowOracle(B, H, D, W, 0.5, 0.7)
+    o.prefill(xk, xv, [70, 9])
+    for s in range(40):
+        w = {b: np.abs(rng.standard_normal((H, 32))).astype(np.float32) for b in range(B)}
+        o.step(rng.standard_normal((B, H, D)).astype(np.float16),
+               rng.standard_normal((B, H, D)).astype(np.float16), None, w)
+    q = rng.standard_normal((B, H * G, D)).astype(np.float16)
+    for b in range(B):
+        # attention over the compressed format = dense attention over the decoded tokens
+        ek, ev = o.compressed(b)
+        wk, wv = o.window(b)
+        kk = np.concatenate([oracle.decompress(ek)[0], wk], axis=1)
+        vv = np.concatenate([oracle.decompress(ev)[0], wv], axis=1)
+        direct = oracle.decode_attention(q[b][None], kk[None], vv[None])[0]
+        np.testing.assert_allclose(o.attention(q[b], b), direct, rtol=0, atol=1e-12)
+        # score increments: numpy softmax of the scores over all tokens, young window tokens
+        inc = o.score_increments(q[b], b)
+        L, n = o.window_len(b), o.n_comp(b)
+        for h in range(H):
+            keys = kk[h].view(np.float16).astype(np.float64)
+            tot = np.zeros(n + L)
+            for g in range(G):
+                s = keys @ q[b, h * G + g].astype(np.float64) / np.sqrt(D)
+                e = np.exp(s - s.max())
+                tot += e / e.sum()
+            want = np.where(np.arange(L) >= L - 32, tot[n:], 0.0)
+            np.testing.assert_allclose(inc[h], want, rtol=1e-12, atol=1e-15)
