@@ -77,6 +77,10 @@ typedef struct mustafar_ccache {
     int32_t cap_tokens;   /* tokens each stream can hold                        */
     int32_t n_tokens;     /* tokens compressed so far (same for every stream)   */
     int64_t val_stride;   /* fp16 elements reserved per stream, multiple of 8   */
+    int32_t group_keep;   /* -1: per-token cache (n_keep channels per token);   */
+                          /* >= 0: per-channel cache, every channel keeps       */
+                          /* group_keep tokens of each group of 32 (see         */
+                          /* mustafar_ccache_init_grouped); n_keep is then d    */
 } mustafar_ccache_t;
 
 /* Channels kept per token for a target sparsity s in [0, 1] (Sec. 2 prunes
@@ -104,6 +108,27 @@ int64_t mustafar_stream_capacity(int d, int n_keep, int cap_tokens);
 int mustafar_ccache_init(mustafar_ccache_t* c, void* bitmaps, void* offsets, void* values,
                          void* stream_len, int B, int H, int d, float sparsity,
                          int cap_tokens, int64_t val_stride);
+
+/* PER-CHANNEL CACHES (Sec. 2, value-cache study: each channel is pruned to the
+ * target sparsity within groups of 32 consecutive tokens). The format is the
+ * same (per-token 1x64 tiles, bitmaps, offsets, padded values), so the decode
+ * attention reads these caches like the others; a token keeps a variable number
+ * of channels, and every channel keeps group_keep = mustafar_keep_count(32, s)
+ * tokens of each group of 32 (tokens 32g .. 32g+31 of the stream).
+ * Capacity: per group, group_keep * d kept values plus at most 7 pad slots in
+ * each of its 32 * d/64 tiles; mustafar_grouped_stream_capacity returns that
+ * bound for ceil(cap_tokens / 32) groups (-1 on invalid arguments). */
+int64_t mustafar_grouped_stream_capacity(int d, int group_keep, int cap_tokens);
+
+/* As mustafar_ccache_init for a per-channel cache: sets group_keep =
+ * mustafar_keep_count(32, sparsity), n_keep = d, and checks val_stride >=
+ * mustafar_grouped_stream_capacity(d, group_keep, cap_tokens). Such a cache is
+ * filled by whole groups only: mustafar_prune_compress (per-channel magnitude
+ * pruning), mustafar_prune_compress_ex with a CHANNEL mode, or the grouped
+ * window lifecycle; the append calls reject it. */
+int mustafar_ccache_init_grouped(mustafar_ccache_t* c, void* bitmaps, void* offsets, void* values,
+                                 void* stream_len, int B, int H, int d, float sparsity,
+                                 int cap_tokens, int64_t val_stride);
 
 /* Device workspace needed by mustafar_prune_compress for n_new tokens. */
 size_t mustafar_compress_workspace_bytes(int B, int H, int n_new);
@@ -142,17 +167,34 @@ int mustafar_append(mustafar_ccache_t* c, const void* x_new, void* stream);
  *                                weights per token (see mustafar_query_lookahead).
  * head_keep (all modes but 2:4): NULL, or a HOST array [H] of kept counts per
  * head, each in [0, c->n_keep] (finer-grained sparsity, Sec. 4.5; the cache's
- * capacity is the one of n_keep). H <= 256 with head_keep. */
+ * capacity is the one of n_keep). H <= 256 with head_keep.
+ * Per-channel caches only (mustafar_prune_compress_ex; n_new and c->n_tokens
+ * multiples of 32; head_keep must be NULL):
+ *   MUSTAFAR_PRUNE_CHANNEL       per-channel magnitude pruning in groups of 32
+ *                                tokens: every channel keeps the group_keep
+ *                                tokens of largest |x|, ties to the lower token
+ *                                (the default of mustafar_prune_compress on
+ *                                such a cache);
+ *   MUSTAFAR_PRUNE_CHANNEL_OUTPUT_AWARE  per-channel output-aware pruning
+ *                                (Sec. 2): the key of token j is |x_jc| * w_j,
+ *                                the fp32 product rounded once, with w_j >= 0
+ *                                the attention probability mass token j
+ *                                received (fp32 [B][H][n_new], 4-byte aligned;
+ *                                see mustafar_window_decode_attn_scores); ties
+ *                                to the lower token. */
 enum mustafar_prune_mode {
     MUSTAFAR_PRUNE_MAGNITUDE = 0,
     MUSTAFAR_PRUNE_2_4 = 1,
-    MUSTAFAR_PRUNE_OUTPUT_AWARE = 2
+    MUSTAFAR_PRUNE_OUTPUT_AWARE = 2,
+    MUSTAFAR_PRUNE_CHANNEL = 3,
+    MUSTAFAR_PRUNE_CHANNEL_OUTPUT_AWARE = 4
 };
 typedef struct mustafar_prune_opts {
     int32_t mode;
     const int32_t* head_keep; /* host [H] or NULL                                  */
-    const float* weights;     /* device fp32 [B][H][n_tokens][d], 4-byte aligned;  */
-                              /* OUTPUT_AWARE only                                 */
+    const float* weights;     /* device fp32, 4-byte aligned: [B][H][n_tokens][d]  */
+                              /* (OUTPUT_AWARE) or [B][H][n_tokens] (CHANNEL_      */
+                              /* OUTPUT_AWARE); NULL for the other modes           */
 } mustafar_prune_opts_t;
 
 /* mustafar_prune_compress / mustafar_append under a pruner variant (opts NULL:
@@ -251,7 +293,10 @@ int mustafar_window_init(mustafar_window_t* w, void* k, void* v, void* len, void
  * fill window slots 0.. in order; len[b], head[b] = 0 and n_comp[b] are set.
  * Afterwards Kc/Vc->n_tokens and w->max_len hold the batch maxima. ws: at
  * least mustafar_compress_workspace_bytes(1, H, n_max) bytes, 8-byte aligned
- * (used by one entry after the other). Errors: EINVAL, ECAPACITY, EWORKSPACE. */
+ * (used by one entry after the other). With a per-channel Vc (the grouped
+ * lifecycle, see mustafar_window_step_grouped) the compressed prefix is instead
+ * the first 32 * floor((seq_len[b] - 1) / 32) tokens, whole groups, values
+ * pruned per channel by magnitude. Errors: EINVAL, ECAPACITY, EWORKSPACE. */
 int mustafar_window_prefill(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
                             const void* x_k, const void* x_v, int n_max, const int32_t* seq_len,
                             void* ws, size_t ws_bytes, void* stream);
@@ -279,6 +324,45 @@ int mustafar_window_decode_attn(const void* q, int B, int Hq, const mustafar_cca
                                 const mustafar_ccache_t* Vc, const mustafar_window_t* w,
                                 float scale, void* out, int n_splits, void* ws, size_t ws_bytes,
                                 void* stream);
+
+/* Decode attention as mustafar_window_decode_attn, then the output-aware
+ * scores of per-channel value pruning (Sec. 2): for every batch entry b,
+ * kv-head h and window slot holding one of the entry's tokens that arrived
+ * fewer than 32 steps ago (the newest 32 of its len[b]),
+ *   acc[b][h][slot] += sum over the G query heads of h of the attention
+ *                      probability of that token (Algorithm 1's softmax over
+ *                      the compressed and window tokens),
+ * so that once a token is 32 steps old, its slot holds the sum over the
+ * current and the 31 following decode steps. acc: device fp32 [B][H][W],
+ * 4-byte aligned, zeroed by the caller before the first step (the grouped
+ * window step clears the slots it frees). The workspace is the one of
+ * mustafar_window_decode_attn. Errors as mustafar_window_decode_attn. */
+int mustafar_window_decode_attn_scores(const void* q, int B, int Hq, const mustafar_ccache_t* Kc,
+                                       const mustafar_ccache_t* Vc, const mustafar_window_t* w,
+                                       float* acc, float scale, void* out, int n_splits, void* ws,
+                                       size_t ws_bytes, void* stream);
+
+/* One decode step of the GROUPED window lifecycle (per-channel value pruning in
+ * groups of 32 tokens, Sec. 2): Kc is a per-token cache, Vc a per-channel
+ * cache, the window has W >= 64 slots, W a multiple of 32. For every active
+ * batch entry b (active may be NULL): if its window is full (len[b] == W), its
+ * oldest 32 tokens leave it together: their keys are pruned per token
+ * (magnitude, Kc's n_keep) and their values per channel as one group, with the
+ * scores acc[b][h][slot] of their slots (CHANNEL_OUTPUT_AWARE) or by magnitude
+ * (acc NULL); both are appended as tokens n_comp[b] .. n_comp[b]+31,
+ * n_comp[b] += 32, head[b] advances by 32 and len[b] -= 32. Then the new
+ * token enters slot (head + len) % W, whose acc entries are set to 0, and
+ * len[b] += 1. A token is thus at least 32 steps old when it leaves,
+ * so its score covers exactly its first 32 steps. Host bounds as for
+ * mustafar_window_step, by 32 tokens (ECAPACITY if the caches could not take a
+ * group). Errors: EINVAL (shapes, W, cache kinds, alignment), ECAPACITY,
+ * ELAUNCH. The prefill of such a window (mustafar_window_prefill with a
+ * per-channel Vc) compresses the first 32 * floor((n - 1) / 32) tokens of an
+ * entry of n tokens, by magnitude, and keeps the rest (1 to 32 tokens) in the
+ * window. */
+int mustafar_window_step_grouped(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
+                                 const void* k_new, const void* v_new, const void* active,
+                                 float* acc, void* stream);
 
 /* Static message for a status code. */
 const char* mustafar_strerror(int status);

@@ -37,7 +37,8 @@ class ccache_t(ctypes.Structure):
                 ("values", ctypes.c_void_p), ("stream_len", ctypes.c_void_p),
                 ("B", ctypes.c_int32), ("H", ctypes.c_int32), ("d", ctypes.c_int32),
                 ("n_keep", ctypes.c_int32), ("cap_tokens", ctypes.c_int32),
-                ("n_tokens", ctypes.c_int32), ("val_stride", ctypes.c_int64)]
+                ("n_tokens", ctypes.c_int32), ("val_stride", ctypes.c_int64),
+                ("group_keep", ctypes.c_int32)]
 
 
 class window_t(ctypes.Structure):
@@ -55,6 +56,8 @@ class prune_opts_t(ctypes.Structure):
 
 
 PRUNE_MAGNITUDE, PRUNE_2_4, PRUNE_OUTPUT_AWARE = 0, 1, 2
+PRUNE_CHANNEL, PRUNE_CHANNEL_OUTPUT_AWARE = 3, 4
+GROUP = 32  # tokens per group of per-channel value pruning
 
 _SIGS = {
     "mustafar_keep_count": (ctypes.c_int, [ctypes.c_int, ctypes.c_float]),
@@ -64,6 +67,11 @@ _SIGS = {
                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                             ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                             ctypes.c_float, ctypes.c_int, ctypes.c_int64]),
+    "mustafar_grouped_stream_capacity": (ctypes.c_int64, [ctypes.c_int, ctypes.c_int, ctypes.c_int]),
+    "mustafar_ccache_init_grouped": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                                    ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                                    ctypes.c_float, ctypes.c_int, ctypes.c_int64]),
     "mustafar_compress_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int] * 3),
     "mustafar_prune_compress": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
                                                ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t,
@@ -99,6 +107,17 @@ _SIGS = {
                                                    ctypes.POINTER(window_t), ctypes.c_float,
                                                    ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                                    ctypes.c_size_t, ctypes.c_void_p]),
+    "mustafar_window_decode_attn_scores": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                                          ctypes.POINTER(ccache_t),
+                                                          ctypes.POINTER(ccache_t),
+                                                          ctypes.POINTER(window_t), ctypes.c_void_p,
+                                                          ctypes.c_float, ctypes.c_void_p, ctypes.c_int,
+                                                          ctypes.c_void_p, ctypes.c_size_t,
+                                                          ctypes.c_void_p]),
+    "mustafar_window_step_grouped": (ctypes.c_int, [ctypes.POINTER(window_t), ctypes.POINTER(ccache_t),
+                                                    ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                                    ctypes.c_void_p]),
     "mustafar_prune_compress_ex": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
                                                   ctypes.c_int, ctypes.POINTER(prune_opts_t),
                                                   ctypes.c_void_p, ctypes.c_size_t,
@@ -193,18 +212,23 @@ class CompressedCache:
     values fp16 bits [B][H][val_stride], stream_len u32 [B][H].
     """
 
-    def __init__(self, B: int, H: int, d: int, sparsity: float, cap_tokens: int, device="cuda"):
+    def __init__(self, B: int, H: int, d: int, sparsity: float, cap_tokens: int, device="cuda",
+                 grouped: bool = False):
         import torch
-        k = mustafar_keep_count(d, sparsity)
         T = d // TILE
-        stride = mustafar_stream_capacity(d, k, cap_tokens)
+        if grouped:   # per-channel pruning in groups of 32 tokens
+            stride = lib().mustafar_grouped_stream_capacity(d, mustafar_keep_count(GROUP, sparsity),
+                                                            cap_tokens)
+        else:
+            stride = mustafar_stream_capacity(d, mustafar_keep_count(d, sparsity), cap_tokens)
         stride = max(PAD, (stride + PAD - 1) // PAD * PAD)
         self.bitmaps = torch.zeros((B, H, cap_tokens, T), dtype=torch.int64, device=device)
         self.offsets = torch.zeros((B, H, cap_tokens, T), dtype=torch.int32, device=device)
         self.values = torch.zeros((B, H, stride), dtype=torch.int16, device=device)
         self.stream_len = torch.zeros((B, H), dtype=torch.int32, device=device)
         self.desc = ccache_t()
-        _check("mustafar_ccache_init", lib().mustafar_ccache_init(
+        init = "mustafar_ccache_init_grouped" if grouped else "mustafar_ccache_init"
+        _check(init, getattr(lib(), init)(
             ctypes.byref(self.desc), self.bitmaps.data_ptr(), self.offsets.data_ptr(),
             self.values.data_ptr(), self.stream_len.data_ptr(), B, H, d, float(sparsity),
             cap_tokens, stride))
@@ -216,6 +240,10 @@ class CompressedCache:
     @property
     def n_keep(self) -> int:
         return self.desc.n_keep
+
+    @property
+    def group_keep(self) -> int:
+        return self.desc.group_keep
 
     @property
     def shape(self):
@@ -255,7 +283,9 @@ def _prune_opts(mode, head_keep, weights):
 def mustafar_prune_compress_ex(cache: CompressedCache, x, mode: int = 0, head_keep=None,
                                weights=None, ws=None, stream=None) -> None:
     """mustafar_prune_compress under a pruner variant (PRUNE_MAGNITUDE with optional
-    per-head counts, PRUNE_2_4, PRUNE_OUTPUT_AWARE with fp32 weights [B][H][n_new][d])."""
+    per-head counts, PRUNE_2_4, PRUNE_OUTPUT_AWARE with fp32 weights [B][H][n_new][d];
+    on per-channel caches PRUNE_CHANNEL, PRUNE_CHANNEL_OUTPUT_AWARE with fp32 token
+    weights [B][H][n_new])."""
     import torch
     n_new = int(x.shape[2])
     need = mustafar_compress_workspace_bytes(cache.desc.B, cache.desc.H, n_new)
@@ -395,6 +425,34 @@ def mustafar_window_decode_attn(q, Kc: CompressedCache, Vc: CompressedCache, win
         float(scale), _dptr(out), int(n_splits), _dptr(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
     return out
+
+
+def mustafar_window_decode_attn_scores(q, Kc: CompressedCache, Vc: CompressedCache,
+                                       win: DenseWindow, acc, scale: float = 0.0, out=None,
+                                       n_splits: int = 0, ws=None, stream=None):
+    """mustafar_window_decode_attn, then acc [B][H][W] (fp32, device) += the attention
+    probability, summed over each kv-head's query heads, of every window token
+    younger than 32 steps."""
+    import torch
+    B, Hq, d = (int(s) for s in q.shape)
+    if out is None:
+        out = torch.empty((B, Hq, d), dtype=torch.float16, device=q.device)
+    ws = _attn_ws(B, Hq, Kc.desc.H, d, Kc.n_tokens, n_splits, ws, q.device)
+    _check("mustafar_window_decode_attn_scores", lib().mustafar_window_decode_attn_scores(
+        _dptr(q), B, Hq, ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), ctypes.byref(win.desc),
+        _dptr(acc), float(scale), _dptr(out), int(n_splits), _dptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
+    return out
+
+
+def mustafar_window_step_grouped(win: DenseWindow, Kc: CompressedCache, Vc: CompressedCache,
+                                 k_new, v_new, active=None, acc=None, stream=None) -> None:
+    """One step of the grouped lifecycle: full windows first hand their oldest 32
+    tokens to Kc (per token) and the per-channel cache Vc (one group, scored by acc
+    [B][H][W] fp32, or by magnitude when acc is None)."""
+    _check("mustafar_window_step_grouped", lib().mustafar_window_step_grouped(
+        ctypes.byref(win.desc), ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), _dptr(k_new),
+        _dptr(v_new), _dptr(active), _dptr(acc), _stream(stream)))
 
 
 def mustafar_stream_read(buf, sink=None, stream=None):

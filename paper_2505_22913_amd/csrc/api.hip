@@ -30,11 +30,15 @@ int check_cache(const mustafar_ccache_t* c) {
   if (!head_dim_ok(c->d)) return MUSTAFAR_EINVAL;
   if (c->n_keep < 0 || c->n_keep > c->d) return MUSTAFAR_EINVAL;
   if (c->cap_tokens < 1 || c->n_tokens < 0 || c->n_tokens > c->cap_tokens) return MUSTAFAR_EINVAL;
-  if (c->val_stride % kPad != 0 ||
-      c->val_stride < mustafar_stream_capacity(c->d, c->n_keep, c->cap_tokens))
-    return MUSTAFAR_EINVAL;
+  if (c->group_keep < -1 || c->group_keep > mf::kGroup) return MUSTAFAR_EINVAL;
+  const int64_t need = c->group_keep >= 0
+                           ? mustafar_grouped_stream_capacity(c->d, c->group_keep, c->cap_tokens)
+                           : mustafar_stream_capacity(c->d, c->n_keep, c->cap_tokens);
+  if (c->val_stride % kPad != 0 || c->val_stride < need) return MUSTAFAR_EINVAL;
   return MUSTAFAR_OK;
 }
+
+bool grouped(const mustafar_ccache_t* c) { return c->group_keep >= 0; }
 
 mf::CacheView view_of(const mustafar_ccache_t* c) {
   mf::CacheView v;
@@ -47,6 +51,7 @@ mf::CacheView view_of(const mustafar_ccache_t* c) {
   v.n_keep = c->n_keep;
   v.cap_tokens = c->cap_tokens;
   v.val_stride = c->val_stride;
+  v.group_keep = c->group_keep;
   return v;
 }
 
@@ -58,6 +63,7 @@ mf::SparseSide side_of(const mustafar_ccache_t* c) {
   s.val_stride = c->val_stride;
   s.cap_tokens = c->cap_tokens;
   s.n_keep = c->n_keep;
+  s.group_keep = c->group_keep;
   return s;
 }
 
@@ -105,6 +111,17 @@ mf::WindowView window_view_of(const mustafar_window_t* w) {
   return wv;
 }
 
+// Grouped lifecycle windows: whole groups of 32 slots, at least two.
+bool grouped_window_ok(const mustafar_window_t* w) { return w->W >= 2 * mf::kGroup && w->W % mf::kGroup == 0; }
+
+// Tokens of a prompt of n tokens that the prefill leaves in the window: the
+// last min(n, W), or with a per-channel value cache the last 1 to 32 (the
+// compressed prefix is whole groups).
+int prefill_window_len(const mustafar_window_t* w, const mustafar_ccache_t* Vc, int n) {
+  if (Vc->group_keep >= 0) return n <= 0 ? 0 : n - (n - 1) / mf::kGroup * mf::kGroup;
+  return n < w->W ? n : w->W;
+}
+
 // The streams of batch entry b as a one-entry cache (same buffers).
 mustafar_ccache_t entry_view(const mustafar_ccache_t* c, int b) {
   mustafar_ccache_t v = *c;
@@ -129,6 +146,7 @@ int prune_opts_of(const mustafar_ccache_t* c, const mustafar_prune_opts_t* opts,
   if (opts->mode != MUSTAFAR_PRUNE_MAGNITUDE && opts->mode != MUSTAFAR_PRUNE_2_4 &&
       opts->mode != MUSTAFAR_PRUNE_OUTPUT_AWARE)
     return MUSTAFAR_EINVAL;
+  if (grouped(c)) return MUSTAFAR_EINVAL;  // per-token modes need a per-token cache
   o->mode = opts->mode;
   if (opts->mode == MUSTAFAR_PRUNE_2_4) {
     if (opts->head_keep || c->n_keep * 2 != c->d) return MUSTAFAR_EINVAL;
@@ -169,6 +187,12 @@ int64_t mustafar_token_max_elems(int d, int n_keep) {
   return m < d ? m : d;
 }
 
+int64_t mustafar_grouped_stream_capacity(int d, int group_keep, int cap_tokens) {
+  if (!head_dim_ok(d) || group_keep < 0 || group_keep > mf::kGroup || cap_tokens < 0) return -1;
+  const int64_t groups = ((int64_t)cap_tokens + mf::kGroup - 1) / mf::kGroup;
+  return groups * ((int64_t)group_keep * d + (int64_t)mf::kGroup * (d / kTile) * (kPad - 1));
+}
+
 int64_t mustafar_stream_capacity(int d, int n_keep, int cap_tokens) {
   const int64_t per = mustafar_token_max_elems(d, n_keep);
   if (per < 0 || cap_tokens < 0) return -1;
@@ -193,6 +217,32 @@ int mustafar_ccache_init(mustafar_ccache_t* c, void* bitmaps, void* offsets, voi
   t.cap_tokens = cap_tokens;
   t.n_tokens = 0;
   t.val_stride = val_stride;
+  t.group_keep = -1;
+  const int st = check_cache(&t);
+  if (st != MUSTAFAR_OK) return st;
+  *c = t;
+  return MUSTAFAR_OK;
+}
+
+int mustafar_ccache_init_grouped(mustafar_ccache_t* c, void* bitmaps, void* offsets, void* values,
+                                 void* stream_len, int B, int H, int d, float sparsity,
+                                 int cap_tokens, int64_t val_stride) {
+  if (!c) return MUSTAFAR_EINVAL;
+  const int gk = mustafar_keep_count(mf::kGroup, sparsity);
+  if (gk < 0 || !head_dim_ok(d)) return MUSTAFAR_EINVAL;
+  mustafar_ccache_t t;
+  t.bitmaps = (uint64_t*)bitmaps;
+  t.offsets = (uint32_t*)offsets;
+  t.values = (uint16_t*)values;
+  t.stream_len = (uint32_t*)stream_len;
+  t.B = B;
+  t.H = H;
+  t.d = d;
+  t.n_keep = d;
+  t.cap_tokens = cap_tokens;
+  t.n_tokens = 0;
+  t.val_stride = val_stride;
+  t.group_keep = gk;
   const int st = check_cache(&t);
   if (st != MUSTAFAR_OK) return st;
   *c = t;
@@ -212,9 +262,13 @@ int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void
   if (n_new < 1 || !aligned(x, 16)) return MUSTAFAR_EINVAL;
   if ((int64_t)c->n_tokens + n_new > c->cap_tokens) return MUSTAFAR_ECAPACITY;
   const size_t need = mustafar_compress_workspace_bytes(c->B, c->H, n_new);
+  if (grouped(c) && (n_new % mf::kGroup != 0 || c->n_tokens % mf::kGroup != 0)) return MUSTAFAR_EINVAL;
   if (!aligned(ws, 8) || ws_bytes < need) return MUSTAFAR_EWORKSPACE;
-  const hipError_t e = mf::launch_compress(view_of(c), (const uint16_t*)x, n_new, c->n_tokens,
-                                           (uint32_t*)ws, (hipStream_t)stream);
+  const hipError_t e =
+      grouped(c) ? mf::launch_compress_channel(view_of(c), (const uint16_t*)x, n_new, c->n_tokens,
+                                               (uint32_t*)ws, (hipStream_t)stream, nullptr)
+                 : mf::launch_compress(view_of(c), (const uint16_t*)x, n_new, c->n_tokens,
+                                       (uint32_t*)ws, (hipStream_t)stream);
   st = status_of(e);
   if (st == MUSTAFAR_OK) c->n_tokens += n_new;
   return st;
@@ -223,7 +277,7 @@ int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void
 int mustafar_append(mustafar_ccache_t* c, const void* x_new, void* stream) {
   int st = check_cache(c);
   if (st != MUSTAFAR_OK) return st;
-  if (!aligned(x_new, 16)) return MUSTAFAR_EINVAL;
+  if (!aligned(x_new, 16) || grouped(c)) return MUSTAFAR_EINVAL;
   if (c->n_tokens + 1 > c->cap_tokens) return MUSTAFAR_ECAPACITY;
   st = status_of(mf::launch_append(view_of(c), (const uint16_t*)x_new, c->n_tokens,
                                    (hipStream_t)stream));
@@ -238,6 +292,20 @@ int mustafar_prune_compress_ex(mustafar_ccache_t* c, const void* x, int n_new,
   int st = check_cache(c);
   if (st != MUSTAFAR_OK) return st;
   if (n_new < 1 || !aligned(x, 16)) return MUSTAFAR_EINVAL;
+  if (opts->mode == MUSTAFAR_PRUNE_CHANNEL || opts->mode == MUSTAFAR_PRUNE_CHANNEL_OUTPUT_AWARE) {
+    const bool scored = opts->mode == MUSTAFAR_PRUNE_CHANNEL_OUTPUT_AWARE;
+    if (!grouped(c) || opts->head_keep) return MUSTAFAR_EINVAL;
+    if (n_new % mf::kGroup != 0 || c->n_tokens % mf::kGroup != 0) return MUSTAFAR_EINVAL;
+    if (scored && (!opts->weights || !aligned(opts->weights, 4))) return MUSTAFAR_EINVAL;
+    if ((int64_t)c->n_tokens + n_new > c->cap_tokens) return MUSTAFAR_ECAPACITY;
+    if (!aligned(ws, 8) || ws_bytes < mustafar_compress_workspace_bytes(c->B, c->H, n_new))
+      return MUSTAFAR_EWORKSPACE;
+    st = status_of(mf::launch_compress_channel(view_of(c), (const uint16_t*)x, n_new, c->n_tokens,
+                                               (uint32_t*)ws, (hipStream_t)stream,
+                                               scored ? opts->weights : nullptr));
+    if (st == MUSTAFAR_OK) c->n_tokens += n_new;
+    return st;
+  }
   mf::PruneOpts o;
   if ((st = prune_opts_of(c, opts, &o)) != MUSTAFAR_OK) return st;
   if ((int64_t)c->n_tokens + n_new > c->cap_tokens) return MUSTAFAR_ECAPACITY;
@@ -254,7 +322,7 @@ int mustafar_append_ex(mustafar_ccache_t* c, const void* x_new, const mustafar_p
   if (!opts) return mustafar_append(c, x_new, stream);
   int st = check_cache(c);
   if (st != MUSTAFAR_OK) return st;
-  if (!aligned(x_new, 16)) return MUSTAFAR_EINVAL;
+  if (!aligned(x_new, 16) || grouped(c)) return MUSTAFAR_EINVAL;
   mf::PruneOpts o;
   if ((st = prune_opts_of(c, opts, &o)) != MUSTAFAR_OK) return st;
   if (c->n_tokens + 1 > c->cap_tokens) return MUSTAFAR_ECAPACITY;
@@ -292,7 +360,8 @@ size_t mustafar_attn_workspace_bytes(int B, int Hq, int Hkv, int d, int n_tokens
   const int64_t BHq = (int64_t)B * Hq;
   const int64_t parts = mf::merge_parts(n_seg, BHq);
   const int64_t rows = n_seg + (parts > 1 ? parts : 0);
-  return (size_t)(rows * BHq * (int64_t)(d + 2) * (int64_t)sizeof(float));
+  // ... then the per-query-head log-sum-exp of the scores-emitting calls.
+  return (size_t)(rows * BHq * (int64_t)(d + 2) * (int64_t)sizeof(float) + BHq * (int64_t)sizeof(float));
 }
 
 static int decode_common(const void* q, int B, int Hq, int Hkv, int d, int n_s, int n_dense,
@@ -402,10 +471,11 @@ int mustafar_window_prefill(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafa
   if (!window_matches(w, Kc) || !window_matches(w, Vc)) return MUSTAFAR_EINVAL;
   if (Kc->n_tokens != 0 || Vc->n_tokens != 0) return MUSTAFAR_EINVAL;
   if (n_max < 0 || !seq_len || !aligned(x_k, 16) || !aligned(x_v, 16)) return MUSTAFAR_EINVAL;
+  if (grouped(Kc) || (grouped(Vc) && !grouped_window_ok(w))) return MUSTAFAR_EINVAL;
   int max_comp = 0, max_len = 0;
   for (int b = 0; b < w->B; ++b) {
     if (seq_len[b] < 0 || seq_len[b] > n_max) return MUSTAFAR_EINVAL;
-    const int len = seq_len[b] < w->W ? seq_len[b] : w->W;
+    const int len = prefill_window_len(w, Vc, seq_len[b]);
     if (seq_len[b] - len > max_comp) max_comp = seq_len[b] - len;
     if (len > max_len) max_len = len;
   }
@@ -415,16 +485,18 @@ int mustafar_window_prefill(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafa
   const hipStream_t s = (hipStream_t)stream;
   const int64_t entry = (int64_t)w->H * n_max * w->d;  // fp16 elements per batch entry of x
   for (int b = 0; b < w->B; ++b) {
-    const int len = seq_len[b] < w->W ? seq_len[b] : w->W;
+    const int len = prefill_window_len(w, Vc, seq_len[b]);
     const int n_comp = seq_len[b] - len;
     const uint16_t* xk = (const uint16_t*)x_k + b * entry;
     const uint16_t* xv = (const uint16_t*)x_v + b * entry;
     if (n_comp > 0) {
       const mustafar_ccache_t kb = entry_view(Kc, b), vb = entry_view(Vc, b);
+      const hipError_t ev =
+          grouped(Vc) ? mf::launch_compress_channel(view_of(&vb), xv, n_comp, 0, (uint32_t*)ws, s, nullptr, n_max)
+                      : mf::launch_compress(view_of(&vb), xv, n_comp, 0, (uint32_t*)ws, s, n_max);
       if ((st = status_of(mf::launch_compress(view_of(&kb), xk, n_comp, 0, (uint32_t*)ws, s, n_max))) !=
               MUSTAFAR_OK ||
-          (st = status_of(mf::launch_compress(view_of(&vb), xv, n_comp, 0, (uint32_t*)ws, s, n_max))) !=
-              MUSTAFAR_OK)
+          (st = status_of(ev)) != MUSTAFAR_OK)
         return st;
     }
     if ((st = status_of(mf::launch_window_fill(window_view_of(w), b, w->d, xk, xv, n_max, n_comp, len,
@@ -443,6 +515,7 @@ int mustafar_window_step(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_c
   if (st != MUSTAFAR_OK) return st;
   if ((st = check_cache(Kc)) != MUSTAFAR_OK || (st = check_cache(Vc)) != MUSTAFAR_OK) return st;
   if (!window_matches(w, Kc) || !window_matches(w, Vc)) return MUSTAFAR_EINVAL;
+  if (grouped(Kc) || grouped(Vc)) return MUSTAFAR_EINVAL;  // see mustafar_window_step_grouped
   if (!aligned(k_new, 16) || !aligned(v_new, 16)) return MUSTAFAR_EINVAL;
   if (active && !aligned(active, 4)) return MUSTAFAR_EINVAL;
   const bool may_graduate = w->max_len >= w->W;
@@ -481,6 +554,67 @@ int mustafar_window_decode_attn(const void* q, int B, int Hq, const mustafar_cca
   sh.Hkv = Kc->H;
   return status_of(mf::launch_attention(sh, (const uint16_t*)q, side_of(Kc), side_of(Vc), w->k, w->v,
                                         ws_ml, ws_o, (uint16_t*)out, (hipStream_t)stream));
+}
+
+int mustafar_window_decode_attn_scores(const void* q, int B, int Hq, const mustafar_ccache_t* Kc,
+                                       const mustafar_ccache_t* Vc, const mustafar_window_t* w,
+                                       float* acc, float scale, void* out, int n_splits, void* ws,
+                                       size_t ws_bytes, void* stream) {
+  int st = check_window(w);
+  if (st != MUSTAFAR_OK) return st;
+  if ((st = check_cache(Kc)) != MUSTAFAR_OK || (st = check_cache(Vc)) != MUSTAFAR_OK) return st;
+  if (!window_matches(w, Kc) || !window_matches(w, Vc) || w->B != B) return MUSTAFAR_EINVAL;
+  if (Kc->n_tokens != Vc->n_tokens || !aligned(acc, 4)) return MUSTAFAR_EINVAL;
+  mf::AttnShape sh;
+  float *ws_ml, *ws_o;
+  st = decode_common(q, B, Hq, Kc->H, Kc->d, Kc->n_tokens, w->W, 1, n_splits, scale, out, ws,
+                     ws_bytes, &sh, &ws_ml, &ws_o);
+  if (st != MUSTAFAR_OK) return st;
+  if (n_splits <= 0) n_splits = mustafar_attn_default_splits(B, Kc->H, Kc->n_tokens > 0 ? Kc->n_tokens : 1);
+  const size_t need = mustafar_attn_workspace_bytes(B, Hq, Kc->H, Kc->d, Kc->n_tokens, n_splits);
+  float* lse2 = (float*)((char*)ws + need) - (int64_t)B * Hq;
+  sh.n_comp = w->n_comp;
+  sh.win_len = w->len;
+  sh.win_head = w->head;
+  sh.Hkv = Kc->H;
+  sh.lse2 = lse2;
+  const hipStream_t s = (hipStream_t)stream;
+  st = status_of(mf::launch_attention(sh, (const uint16_t*)q, side_of(Kc), side_of(Vc), w->k, w->v,
+                                      ws_ml, ws_o, (uint16_t*)out, s));
+  if (st != MUSTAFAR_OK) return st;
+  return status_of(mf::launch_window_scores(window_view_of(w), (const uint16_t*)q, sh.G, sh.T,
+                                            sh.scale_log2, lse2, acc, s));
+}
+
+int mustafar_window_step_grouped(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
+                                 const void* k_new, const void* v_new, const void* active,
+                                 float* acc, void* stream) {
+  int st = check_window(w);
+  if (st != MUSTAFAR_OK) return st;
+  if ((st = check_cache(Kc)) != MUSTAFAR_OK || (st = check_cache(Vc)) != MUSTAFAR_OK) return st;
+  if (!window_matches(w, Kc) || !window_matches(w, Vc)) return MUSTAFAR_EINVAL;
+  if (grouped(Kc) || !grouped(Vc) || !grouped_window_ok(w)) return MUSTAFAR_EINVAL;
+  if (Kc->n_tokens != Vc->n_tokens || Kc->n_tokens % mf::kGroup != 0) return MUSTAFAR_EINVAL;
+  if (!aligned(k_new, 16) || !aligned(v_new, 16) || (acc && !aligned(acc, 4))) return MUSTAFAR_EINVAL;
+  if (active && !aligned(active, 4)) return MUSTAFAR_EINVAL;
+  // Host bound of the entries' compressed counts: w->max_len follows an entry
+  // that holds the most tokens and is active on every step; no entry
+  // graduates before it, so n_tokens grows by a group whenever it does.
+  const bool may_graduate = w->max_len >= w->W;
+  if (may_graduate && (Kc->n_tokens + mf::kGroup > Kc->cap_tokens || Vc->n_tokens + mf::kGroup > Vc->cap_tokens))
+    return MUSTAFAR_ECAPACITY;
+  st = status_of(mf::launch_window_step_grouped(view_of(Kc), view_of(Vc), window_view_of(w),
+                                                (const uint16_t*)k_new, (const uint16_t*)v_new,
+                                                (const int32_t*)active, acc, (hipStream_t)stream));
+  if (st != MUSTAFAR_OK) return st;
+  if (may_graduate) {
+    Kc->n_tokens += mf::kGroup;
+    Vc->n_tokens += mf::kGroup;
+    w->max_len -= mf::kGroup - 1;
+  } else {
+    w->max_len += 1;
+  }
+  return MUSTAFAR_OK;
 }
 
 const char* mustafar_strerror(int status) {

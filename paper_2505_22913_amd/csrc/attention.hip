@@ -413,7 +413,8 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void k_merge(const float2* __r
                                                               int n_seg, int per, int BHq,
                                                               uint16_t* __restrict__ out,
                                                               float2* __restrict__ part_ml,
-                                                              float* __restrict__ part_o) {
+                                                              float* __restrict__ part_o,
+                                                              float* __restrict__ lse2) {
   constexpr int d = kTile * T;
   __shared__ float red[kMergeWaves];
   __shared__ float part[kMergeWaves][d];
@@ -449,6 +450,7 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void k_merge(const float2* __r
     const float inv = 1.f / L;
     const int64_t prow = (int64_t)blockIdx.y * BHq + r;
     if (!FINAL && lane == 0) part_ml[prow] = make_float2(M, L);
+    if (FINAL && lse2 != nullptr && lane == 0) lse2[r] = M + __builtin_log2f(L);
 #pragma unroll
     for (int tt = 0; tt < T; ++tt) {
       float v = part[0][lane + kTile * tt];
@@ -508,14 +510,14 @@ static hipError_t attention_TG(const AttnShape& sh, const AttnArgs& a, uint16_t*
     float2* part_ml = reinterpret_cast<float2*>(a.ws_o + (int64_t)n_seg * a.BHq * (kTile * T));
     float* part_o = reinterpret_cast<float*>(part_ml + (int64_t)parts * a.BHq);
     hipLaunchKernelGGL((k_merge<T, false>), dim3(a.BHq, parts), dim3(kMergeWaves * kWave), 0, s,
-                       a.ws_ml, a.ws_o, n_seg, kMergeSegsPerPart, a.BHq, nullptr, part_ml, part_o);
+                       a.ws_ml, a.ws_o, n_seg, kMergeSegsPerPart, a.BHq, nullptr, part_ml, part_o, nullptr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((k_merge<T, true>), dim3(a.BHq, 1), dim3(kMergeWaves * kWave), 0, s, part_ml,
-                       part_o, parts, parts, a.BHq, out, nullptr, nullptr);
+                       part_o, parts, parts, a.BHq, out, nullptr, nullptr, a.lse2);
     return hipGetLastError();
   }
   hipLaunchKernelGGL((k_merge<T, true>), dim3(a.BHq, 1), dim3(kMergeWaves * kWave), 0, s, a.ws_ml,
-                     a.ws_o, n_seg, n_seg, a.BHq, out, nullptr, nullptr);
+                     a.ws_o, n_seg, n_seg, a.BHq, out, nullptr, nullptr, a.lse2);
   return hipGetLastError();
 }
 
@@ -550,16 +552,91 @@ hipError_t launch_attention(const AttnShape& sh, const uint16_t* q, const Sparse
   a.ws_ml = reinterpret_cast<float2*>(ws_ml);
   a.ws_o = ws_o;
   a.BHq = sh.BHkv * sh.G;
-  a.kmaxK = K.bitmaps != nullptr ? token_max_elems_dev(d, K.n_keep) : 0;
-  a.kmaxV = V.bitmaps != nullptr ? token_max_elems_dev(d, V.n_keep) : 0;
+  a.kmaxK = side_token_bound(d, K);
+  a.kmaxV = side_token_bound(d, V);
   a.n_comp = sh.n_comp;
   a.win_len = sh.win_len;
   a.win_head = sh.win_head;
   a.Hkv = sh.Hkv;
+  a.lse2 = sh.lse2;
   switch (sh.T) {
     case 1: return attention_T<1>(sh, a, out, s);
     case 2: return attention_T<2>(sh, a, out, s);
     case 4: return attention_T<4>(sh, a, out, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// Output-aware scores of per-channel value pruning (Sec. 2): the attention
+// probability of every window token younger than 32 steps, summed over the G
+// query heads of its kv-head and added to its slot's score. One wave per
+// (batch entry, kv-head), lane = window position; q staged in LDS (every lane
+// reads the same address, a broadcast).
+// ------------------------------------------------------------------------------------------
+constexpr int kScoreSteps = 32;  // steps a token's score accumulates (the current and 31 more)
+
+template <int T, int G>
+__global__ __launch_bounds__(kWave) void k_window_scores(WindowView w, const uint16_t* __restrict__ q,
+                                                         float scale_log2, const float* __restrict__ lse2,
+                                                         float* __restrict__ acc) {
+  constexpr int d = kTile * T;
+  __shared__ __attribute__((aligned(16))) uint16_t qs[G * d];
+  const int bh = blockIdx.x;
+  const int b = bh / w.H;
+  const uint32_t lane = lane_id();
+  for (int i = (int)lane; i < G * d; i += kWave) qs[i] = q[(int64_t)bh * G * d + i];
+  __syncthreads();
+  const int len = w.len[b], head = w.head[b];
+  if (len <= 0 || len > w.W || head < 0 || head >= w.W) return;
+  float lse[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) lse[g] = lse2[(int64_t)bh * G + g];
+  const int p = max(0, len - kScoreSteps) + (int)lane;
+  if (p >= len) return;
+  const int slot = (head + p) % w.W;
+  const uint16_t* kr = w.k + ((int64_t)bh * w.W + slot) * d;
+  float s[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) s[g] = 0.f;
+#pragma unroll 4
+  for (int c = 0; c < d; c += 8) {
+    const u32x4 kk = *reinterpret_cast<const u32x4*>(kr + c);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const u32x4 qq = *reinterpret_cast<const u32x4*>(qs + g * d + c);
+      s[g] = __builtin_amdgcn_fdot2(as_h2(kk.x), as_h2(qq.x), s[g], false);
+      s[g] = __builtin_amdgcn_fdot2(as_h2(kk.y), as_h2(qq.y), s[g], false);
+      s[g] = __builtin_amdgcn_fdot2(as_h2(kk.z), as_h2(qq.z), s[g], false);
+      s[g] = __builtin_amdgcn_fdot2(as_h2(kk.w), as_h2(qq.w), s[g], false);
+    }
+  }
+  float sum = 0.f;
+#pragma unroll
+  for (int g = 0; g < G; ++g) sum += __builtin_amdgcn_exp2f(fmaf(s[g], scale_log2, -lse[g]));
+  acc[(int64_t)bh * w.W + slot] += sum;
+}
+
+template <int T>
+static hipError_t window_scores_T(const WindowView& w, const uint16_t* q, int G, float scale_log2,
+                                  const float* lse2, float* acc, hipStream_t s) {
+  const dim3 grid((uint32_t)(w.B * w.H));
+  switch (G) {
+    case 1: hipLaunchKernelGGL((k_window_scores<T, 1>), grid, dim3(kWave), 0, s, w, q, scale_log2, lse2, acc); break;
+    case 2: hipLaunchKernelGGL((k_window_scores<T, 2>), grid, dim3(kWave), 0, s, w, q, scale_log2, lse2, acc); break;
+    case 4: hipLaunchKernelGGL((k_window_scores<T, 4>), grid, dim3(kWave), 0, s, w, q, scale_log2, lse2, acc); break;
+    case 8: hipLaunchKernelGGL((k_window_scores<T, 8>), grid, dim3(kWave), 0, s, w, q, scale_log2, lse2, acc); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_window_scores(const WindowView& w, const uint16_t* q, int G, int T, float scale_log2,
+                                const float* lse2, float* acc, hipStream_t s) {
+  switch (T) {
+    case 1: return window_scores_T<1>(w, q, G, scale_log2, lse2, acc, s);
+    case 2: return window_scores_T<2>(w, q, G, scale_log2, lse2, acc, s);
+    case 4: return window_scores_T<4>(w, q, G, scale_log2, lse2, acc, s);
     default: return hipErrorInvalidValue;
   }
 }

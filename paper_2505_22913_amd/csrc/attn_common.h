@@ -43,6 +43,7 @@ struct AttnArgs {
   const int32_t* win_len;
   const int32_t* win_head;
   int Hkv;
+  float* lse2;  // optional: the final merge writes m + log2(l) per query head
 };
 
 // Compressed tokens of stream bh (its batch entry's count when ragged).
@@ -480,6 +481,25 @@ inline int token_max_elems_dev(int d, int k) {
   const int nonempty = k < T ? k : T;
   const int m = (k + (kPad - 1) * nonempty) / kPad * kPad;
   return m < d ? m : d;
+}
+
+// Worst-case fp16 elements per token of a per-channel cache (group_keep gk),
+// as the bound on the run of any block of NB = 64/T block-aligned tokens
+// divided by NB: a block of 32 or more tokens holds whole groups of 32 (gk * d
+// kept values and at most 7 pad slots per tile each); a 16-token block (T = 4)
+// holds at most min(16, gk) values per channel plus its pad slots.
+inline int grouped_token_bound(int d, int gk) {
+  const int T = d / kTile, NB = kWave / T;
+  const int64_t per_block =
+      NB >= kGroup ? (int64_t)(NB / kGroup) * ((int64_t)gk * d + (int64_t)kGroup * T * (kPad - 1))
+                   : (int64_t)d * (NB < gk ? NB : gk) + (int64_t)NB * T * (kPad - 1);
+  const int m = (int)((per_block + NB - 1) / NB);
+  return m < d ? m : d;
+}
+
+inline int side_token_bound(int d, const SparseSide& s) {
+  if (s.bitmaps == nullptr) return 0;
+  return s.group_keep >= 0 ? grouped_token_bound(d, s.group_keep) : token_max_elems_dev(d, s.n_keep);
 }
 
 // The MFMA kernel for grouped queries (attention_mfma.hip; G in {2, 4, 8}); the

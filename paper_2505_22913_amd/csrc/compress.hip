@@ -493,6 +493,82 @@ __global__ __launch_bounds__(256) void k_select(CacheView c, const uint16_t* __r
   }
 }
 
+// ---- Per-channel value pruning in groups of 32 tokens (Sec. 2) ---------------------------
+// The keep word of one channel over a group (bit j: token j kept): token j is
+// kept iff fewer than k tokens beat it (a larger key, or an equal key and a
+// lower index). Keys are 15-bit fp16 magnitudes or the bits of non-negative
+// fp32 scores; both order like the values.
+__device__ __forceinline__ uint32_t channel_keep_word(const uint32_t (&key)[kGroup], int k) {
+  uint32_t word = 0;
+#pragma unroll
+  for (int j = 0; j < kGroup; ++j) {
+    int beat = 0;
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      if (i < j) beat += key[i] >= key[j] ? 1 : 0;
+      else if (i > j) beat += key[i] > key[j] ? 1 : 0;
+    }
+    word |= (beat < k ? 1u : 0u) << j;
+  }
+  return word;
+}
+
+// Key of value x of token j: its fp16 magnitude, or (SCORED) the fp32 product
+// |x| * w_j rounded once.
+template <bool SCORED>
+__device__ __forceinline__ uint32_t channel_key(uint16_t x, float wj) {
+  if constexpr (SCORED) return __builtin_bit_cast(uint32_t, fabsf(half_bits_to_float(x)) * wj);
+  else return x & 0x7fffu;
+}
+
+// Lane (token j, tile t) of the group, j * T + t = r * 64 + lane, takes the
+// bitmap of that tile: ballots of bit j of each channel's keep word.
+template <int T>
+__device__ __forceinline__ void group_bitmaps(const uint32_t (&word)[T], uint32_t lane,
+                                              uint64_t (&mine)[(kGroup * T + kWave - 1) / kWave]) {
+#pragma unroll
+  for (int r = 0; r < (kGroup * T + kWave - 1) / kWave; ++r) mine[r] = 0;
+#pragma unroll
+  for (int j = 0; j < kGroup; ++j)
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const uint64_t bm = ballot(((word[t] >> j) & 1u) != 0u);
+      const int i = j * T + t;
+      if (lane == (uint32_t)(i % kWave)) mine[i / kWave] = bm;
+    }
+}
+
+// Bitmaps of tokens tok0 .. tok0+n_new-1 of every stream under per-channel
+// pruning: one wave per (stream, group of 32 tokens), lane = channel of a tile.
+template <int T, bool SCORED>
+__global__ __launch_bounds__(256) void k_select_channel(CacheView c, const uint16_t* __restrict__ x,
+                                                        int n_new, int64_t x_stride, int tok0,
+                                                        const float* __restrict__ w) {
+  constexpr int d = kTile * T;
+  constexpr int R = (kGroup * T + kWave - 1) / kWave;
+  const int groups = n_new / kGroup;
+  const int64_t wave = (int64_t)blockIdx.x * (256 / kWave) + threadIdx.x / kWave;
+  if (wave >= (int64_t)c.BH * groups) return;
+  const int bh = (int)(wave / groups), g = (int)(wave % groups);
+  const uint32_t lane = lane_id();
+  const int64_t row0 = (int64_t)bh * x_stride + (int64_t)g * kGroup;
+  uint32_t word[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    uint32_t key[kGroup];
+#pragma unroll
+    for (int j = 0; j < kGroup; ++j)
+      key[j] = channel_key<SCORED>(x[(row0 + j) * d + kTile * t + lane], SCORED ? w[row0 + j] : 0.f);
+    word[t] = channel_keep_word(key, c.group_keep);
+  }
+  uint64_t mine[R];
+  group_bitmaps<T>(word, lane, mine);
+  const int64_t tile0 = ((int64_t)bh * c.cap_tokens + tok0 + (int64_t)g * kGroup) * T;
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+    if (r * kWave + (int)lane < kGroup * T) c.bitmaps[tile0 + r * kWave + lane] = mine[r];
+}
+
 // Output-aware weights, one thread per (b, h, T, channel).
 __global__ __launch_bounds__(256) void k_query_lookahead(const uint16_t* __restrict__ q, int B, int Hq,
                                                          int Hkv, int n_q, int d, int L,
@@ -625,6 +701,100 @@ __global__ void k_window_commit(WindowView w, const int32_t* __restrict__ active
   }
 }
 
+// Grouped window step, one wave per stream (see mustafar_window_step_grouped):
+// if the entry's window is full, its oldest 32 tokens go to kc pruned per token
+// and to vc pruned per channel as one group, as tokens n_comp .. n_comp+31;
+// then the new token takes slot (head + len) % W (= head after a graduation)
+// and its score starts at 0. k_window_commit_grouped advances the entry.
+template <int T, bool SCORED>
+__global__ __launch_bounds__(256) void k_window_step_grouped(CacheView kc, CacheView vc, WindowView w,
+                                                             const uint16_t* __restrict__ k_new,
+                                                             const uint16_t* __restrict__ v_new,
+                                                             const int32_t* __restrict__ active,
+                                                             float* __restrict__ acc) {
+  constexpr int d = kTile * T;
+  const int bh = blockIdx.x * (256 / kWave) + threadIdx.x / kWave;
+  if (bh >= kc.BH) return;
+  const int b = bh / w.H;
+  if (active != nullptr && active[b] == 0) return;
+  const uint32_t lane = lane_id();
+  const int len = w.len[b], head = w.head[b];
+  if (len < 0 || len > w.W || head < 0 || head >= w.W) return;  // not a state these calls produce
+  uint16_t* kr = w.k + (int64_t)bh * w.W * d;
+  uint16_t* vr = w.v + (int64_t)bh * w.W * d;
+  float* ac = acc != nullptr ? acc + (int64_t)bh * w.W : nullptr;
+  const int slot = (head + len) % w.W;
+  const int tok = w.n_comp[b];
+  if (len >= w.W && tok >= 0 && tok + kGroup <= kc.cap_tokens && tok + kGroup <= vc.cap_tokens) {
+    // Keys, one token at a time (the selection of mustafar_append).
+    uint32_t base = tok > 0 ? kc.stream_len[bh] : 0u;
+    for (int u = 0; u < kGroup; ++u) {
+      uint16_t xv[T];
+      load_token<T>(kr + (int64_t)((head + u) % w.W) * d, lane, xv);
+      uint32_t mag[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) mag[t] = xv[t] & 0x7fffu;
+      uint64_t bm[T];
+      select_token<T>(mag, kc.n_keep, bm);
+      const int64_t tile0 = ((int64_t)bh * kc.cap_tokens + tok + u) * T;
+      uint64_t mine = bm[0];
+#pragma unroll
+      for (int t = 1; t < T; ++t) mine = (lane == (uint32_t)t) ? bm[t] : mine;
+      if (lane < (uint32_t)T) kc.bitmaps[tile0 + lane] = mine;
+      base += pack_token<T>(xv, bm, base, kc.values + (int64_t)bh * kc.val_stride, kc.offsets + tile0, lane);
+    }
+    if (lane == 0) kc.stream_len[bh] = base;
+    // Values: per-channel keep words over the group, then each token packed
+    // with its tile bitmaps.
+    uint32_t word[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      uint32_t key[kGroup];
+#pragma unroll
+      for (int j = 0; j < kGroup; ++j) {
+        const int sl = (head + j) % w.W;
+        key[j] = channel_key<SCORED>(vr[(int64_t)sl * d + kTile * t + lane], SCORED ? ac[sl] : 0.f);
+      }
+      word[t] = channel_keep_word(key, vc.group_keep);
+    }
+    base = tok > 0 ? vc.stream_len[bh] : 0u;
+    for (int u = 0; u < kGroup; ++u) {
+      uint16_t xv[T];
+      load_token<T>(vr + (int64_t)((head + u) % w.W) * d, lane, xv);
+      uint64_t bm[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) bm[t] = ballot(((word[t] >> u) & 1u) != 0u);
+      const int64_t tile0 = ((int64_t)bh * vc.cap_tokens + tok + u) * T;
+      uint64_t mine = bm[0];
+#pragma unroll
+      for (int t = 1; t < T; ++t) mine = (lane == (uint32_t)t) ? bm[t] : mine;
+      if (lane < (uint32_t)T) vc.bitmaps[tile0 + lane] = mine;
+      base += pack_token<T>(xv, bm, base, vc.values + (int64_t)bh * vc.val_stride, vc.offsets + tile0, lane);
+    }
+    if (lane == 0) vc.stream_len[bh] = base;
+  }
+  // The graduated tokens were consumed above, so their slots can be reused.
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    kr[(int64_t)slot * d + kTile * t + lane] = k_new[(int64_t)bh * d + kTile * t + lane];
+    vr[(int64_t)slot * d + kTile * t + lane] = v_new[(int64_t)bh * d + kTile * t + lane];
+  }
+  if (ac != nullptr && lane == 0) ac[slot] = 0.f;
+}
+
+__global__ void k_window_commit_grouped(WindowView w, const int32_t* __restrict__ active) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= w.B || (active != nullptr && active[b] == 0)) return;
+  if (w.len[b] < 0 || w.len[b] > w.W || w.head[b] < 0 || w.head[b] >= w.W) return;
+  if (w.len[b] >= w.W) {
+    w.head[b] = (w.head[b] + kGroup) % w.W;
+    w.n_comp[b] += kGroup;
+    w.len[b] -= kGroup - 1;
+  } else {
+    w.len[b] += 1;
+  }
+}
+
 // Prefill of one batch entry's window: tokens [first, first + count) of each of
 // its H streams (x: [H][x_stride][d]) into ring slots 0.., and its state.
 __global__ __launch_bounds__(256) void k_window_fill(WindowView w, int b, int d,
@@ -705,14 +875,11 @@ hipError_t launch_append(const CacheView& c, const uint16_t* x, int tok0, hipStr
   }
 }
 
+// Offsets and packing of tokens whose bitmaps are already in the cache.
 template <int T>
-static hipError_t compress_variant_T(const CacheView& c, const uint16_t* x, int n_new, int tok0,
-                                     uint32_t* ws, hipStream_t s, const PruneOpts& o) {
-  const int64_t waves = ((int64_t)c.BH * n_new + kTokPerWave - 1) / kTokPerWave;
-  hipLaunchKernelGGL(k_select<T>, dim3((uint32_t)((waves + 3) / 4)), dim3(256), 0, s, c, x, n_new,
-                     (int64_t)n_new, tok0, o);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+static hipError_t pack_preset_T(const CacheView& c, const uint16_t* x, int n_new, int64_t x_stride,
+                                int tok0, uint32_t* ws, hipStream_t s) {
+  hipError_t e;
   const int n_chunks = (n_new + compress_chunk_tokens(T) - 1) / compress_chunk_tokens(T);
   const int64_t n_wg = (int64_t)c.BH * n_chunks;
   uint64_t* flags = reinterpret_cast<uint64_t*>(ws);
@@ -723,8 +890,44 @@ static hipError_t compress_variant_T(const CacheView& c, const uint16_t* x, int 
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL((k_compress<T, true>), dim3((uint32_t)n_wg), dim3(kWave), 0, s, x, n_new, 0,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
-                     flags, ticket, n_chunks, (int64_t)n_new);
+                     flags, ticket, n_chunks, x_stride);
   return hipGetLastError();
+}
+
+template <int T>
+static hipError_t compress_channel_T(const CacheView& c, const uint16_t* x, int n_new, int tok0,
+                                     uint32_t* ws, hipStream_t s, const float* w, int64_t x_stride) {
+  const int64_t waves = (int64_t)c.BH * (n_new / kGroup);
+  const dim3 grid((uint32_t)((waves + 3) / 4));
+  if (w != nullptr)
+    hipLaunchKernelGGL((k_select_channel<T, true>), grid, dim3(256), 0, s, c, x, n_new, x_stride, tok0, w);
+  else
+    hipLaunchKernelGGL((k_select_channel<T, false>), grid, dim3(256), 0, s, c, x, n_new, x_stride, tok0, w);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return pack_preset_T<T>(c, x, n_new, x_stride, tok0, ws, s);
+}
+
+hipError_t launch_compress_channel(const CacheView& c, const uint16_t* x, int n_new, int tok0,
+                                   uint32_t* ws, hipStream_t s, const float* w, int64_t x_stride) {
+  if (x_stride <= 0) x_stride = n_new;
+  switch (c.T) {
+    case 1: return compress_channel_T<1>(c, x, n_new, tok0, ws, s, w, x_stride);
+    case 2: return compress_channel_T<2>(c, x, n_new, tok0, ws, s, w, x_stride);
+    case 4: return compress_channel_T<4>(c, x, n_new, tok0, ws, s, w, x_stride);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int T>
+static hipError_t compress_variant_T(const CacheView& c, const uint16_t* x, int n_new, int tok0,
+                                     uint32_t* ws, hipStream_t s, const PruneOpts& o) {
+  const int64_t waves = ((int64_t)c.BH * n_new + kTokPerWave - 1) / kTokPerWave;
+  hipLaunchKernelGGL(k_select<T>, dim3((uint32_t)((waves + 3) / 4)), dim3(256), 0, s, c, x, n_new,
+                     (int64_t)n_new, tok0, o);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return pack_preset_T<T>(c, x, n_new, (int64_t)n_new, tok0, ws, s);
 }
 
 hipError_t launch_compress_variant(const CacheView& c, const uint16_t* x, int n_new, int tok0,
@@ -767,6 +970,34 @@ hipError_t launch_window_fill(const WindowView& w, int b, int d, const uint16_t*
   hipLaunchKernelGGL(k_window_fill, dim3(blocks), dim3(256), 0, s, w, b, d, xk, xv, x_stride, first,
                      count);
   return hipGetLastError();
+}
+
+template <int T>
+static hipError_t window_step_grouped_T(const CacheView& kc, const CacheView& vc, const WindowView& w,
+                                        const uint16_t* k_new, const uint16_t* v_new,
+                                        const int32_t* active, float* acc, hipStream_t s) {
+  const dim3 grid((kc.BH + 3) / 4);
+  if (acc != nullptr)
+    hipLaunchKernelGGL((k_window_step_grouped<T, true>), grid, dim3(256), 0, s, kc, vc, w, k_new, v_new,
+                       active, acc);
+  else
+    hipLaunchKernelGGL((k_window_step_grouped<T, false>), grid, dim3(256), 0, s, kc, vc, w, k_new, v_new,
+                       active, acc);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_window_commit_grouped, dim3((w.B + 255) / 256), dim3(256), 0, s, w, active);
+  return hipGetLastError();
+}
+
+hipError_t launch_window_step_grouped(const CacheView& kc, const CacheView& vc, const WindowView& w,
+                                      const uint16_t* k_new, const uint16_t* v_new,
+                                      const int32_t* active, float* acc, hipStream_t s) {
+  switch (kc.T) {
+    case 1: return window_step_grouped_T<1>(kc, vc, w, k_new, v_new, active, acc, s);
+    case 2: return window_step_grouped_T<2>(kc, vc, w, k_new, v_new, active, acc, s);
+    case 4: return window_step_grouped_T<4>(kc, vc, w, k_new, v_new, active, acc, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_window_step(const CacheView& kc, const CacheView& vc, const WindowView& w,

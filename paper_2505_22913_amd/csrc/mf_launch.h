@@ -22,6 +22,7 @@ struct CacheView {
   int n_keep;        // kept channels per token
   int cap_tokens;    // token capacity per stream
   int64_t val_stride;
+  int group_keep;    // per-channel caches: tokens kept per channel and group of 32; else -1
 };
 
 // Compress n_new tokens per stream (x: [BH][x_stride][64T] fp16, x_stride = n_new
@@ -35,7 +36,8 @@ hipError_t launch_append(const CacheView& c, const uint16_t* x, int tok0, hipStr
 
 // Pruner variants of the same format (the magnitude top-k of k_compress is the
 // default): per-head kept counts, 2:4 per token, output-aware key scores.
-constexpr int kPruneMagnitude = 0, kPrune24 = 1, kPruneOutputAware = 2;
+constexpr int kPruneMagnitude = 0, kPrune24 = 1, kPruneOutputAware = 2, kPruneChannel = 3,
+              kPruneChannelOutputAware = 4;
 constexpr int kMaxPruneHeads = 256;
 struct PruneOpts {
   int mode;
@@ -50,6 +52,12 @@ hipError_t launch_compress_variant(const CacheView& c, const uint16_t* x, int n_
                                    uint32_t* ws, hipStream_t s, const PruneOpts& o);
 hipError_t launch_append_variant(const CacheView& c, const uint16_t* x, int tok0, hipStream_t s,
                                  const PruneOpts& o);
+// Per-channel pruning in groups of 32 tokens (n_new and tok0 multiples of 32):
+// selection (bitmaps, one wave per stream and group) then k_compress in its
+// preset mode. w: NULL (magnitude) or fp32 token weights [BH][n_new].
+constexpr int kGroup = 32;
+hipError_t launch_compress_channel(const CacheView& c, const uint16_t* x, int n_new, int tok0,
+                                   uint32_t* ws, hipStream_t s, const float* w, int64_t x_stride = 0);
 // Output-aware weights: w[b][h][T][c] = sum over t = T .. min(T+L, Nq)-1, then over
 // the G query heads of h, of |q[b][h*G+g][t][c]| (fp32, in that order).
 hipError_t launch_query_lookahead(const uint16_t* q, int B, int Hq, int Hkv, int n_q, int T, int L,
@@ -71,6 +79,16 @@ hipError_t launch_window_fill(const WindowView& w, int b, int d, const uint16_t*
 hipError_t launch_window_step(const CacheView& kc, const CacheView& vc, const WindowView& w,
                               const uint16_t* k_new, const uint16_t* v_new, const int32_t* active,
                               hipStream_t s);
+// Grouped lifecycle step (see mustafar_window_step_grouped): kc per token, vc
+// per channel; acc: fp32 [B][H][W] scores or NULL (magnitude).
+hipError_t launch_window_step_grouped(const CacheView& kc, const CacheView& vc, const WindowView& w,
+                                      const uint16_t* k_new, const uint16_t* v_new,
+                                      const int32_t* active, float* acc, hipStream_t s);
+// Scores of the window tokens younger than 32 steps: acc[b][h][slot] += sum over
+// the G query heads of h of exp2(scale_log2 * q.k - lse2[b][hq]) (lse2: the
+// log2-domain log-sum-exp the merge wrote).
+hipError_t launch_window_scores(const WindowView& w, const uint16_t* q, int G, int T,
+                                float scale_log2, const float* lse2, float* acc, hipStream_t s);
 
 struct SparseSide {
   const uint64_t* bitmaps;
@@ -79,6 +97,7 @@ struct SparseSide {
   int64_t val_stride;
   int cap_tokens;
   int n_keep;
+  int group_keep = -1;  // per-channel caches (see CacheView)
 };
 
 struct AttnShape {
@@ -97,6 +116,9 @@ struct AttnShape {
   const int32_t* win_len = nullptr;
   const int32_t* win_head = nullptr;
   int Hkv = 1;
+  // If set, the final merge also writes each query head's log-sum-exp of the
+  // scores in the log2 domain, m + log2(l), to lse2 [BHq].
+  float* lse2 = nullptr;
 };
 
 // Split-K merge in two levels when a single level would run on too few

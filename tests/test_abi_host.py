@@ -53,9 +53,10 @@ def test_struct_layout_matches_the_c_compiler(tmp_path):
     prog = tmp_path / "layout.c"
     prog.write_text(
         '#include <stddef.h>\n#include <stdio.h>\n#include "mustafar.h"\n'
-        "int main(void){printf(\"%zu %zu %zu %zu %zu\\n\", sizeof(mustafar_ccache_t),"
+        "int main(void){printf(\"%zu %zu %zu %zu %zu %zu\\n\", sizeof(mustafar_ccache_t),"
         " offsetof(mustafar_ccache_t, B), offsetof(mustafar_ccache_t, n_keep),"
-        " offsetof(mustafar_ccache_t, n_tokens), offsetof(mustafar_ccache_t, val_stride));"
+        " offsetof(mustafar_ccache_t, n_tokens), offsetof(mustafar_ccache_t, val_stride),"
+        " offsetof(mustafar_ccache_t, group_keep));"
         "return 0;}\n")
     exe = tmp_path / "layout"
     subprocess.run(["gcc", "-std=c11", f"-I{os.path.dirname(HEADER)}", "-o", str(exe), str(prog)],
@@ -64,7 +65,7 @@ def test_struct_layout_matches_the_c_compiler(tmp_path):
                                              check=True).stdout.split()]
     T = mf.ccache_t
     assert c_vals == [ctypes.sizeof(T), T.B.offset, T.n_keep.offset, T.n_tokens.offset,
-                      T.val_stride.offset]
+                      T.val_stride.offset, T.group_keep.offset]
 
 
 def test_keep_count_agrees_with_the_oracle_reading(lib):
@@ -290,3 +291,84 @@ def test_prune_variants_reject_before_launch(lib):
     assert lib.mustafar_query_lookahead(0x700000, 1, 6, 4, 10, 128, 32, 0x800000, None) == mf.EINVAL
     assert lib.mustafar_query_lookahead(0x700000, 1, 8, 4, 10, 128, 0, 0x800000, None) == mf.EINVAL
     assert lib.mustafar_query_lookahead(0x700008, 1, 8, 4, 10, 128, 32, 0x800000, None) == mf.EINVAL
+
+
+def _fake_grouped(B=2, H=4, d=128, s=0.7, cap=96, stride=None):
+    c = mf.ccache_t()
+    gk = mf.lib().mustafar_keep_count(32, s)
+    if stride is None:
+        stride = max(mf.lib().mustafar_grouped_stream_capacity(d, max(gk, 0), cap), 8)
+    st = mf.lib().mustafar_ccache_init_grouped(ctypes.byref(c), 0x100000, 0x200000, 0x300000,
+                                               0x400000, B, H, d, s, cap, stride)
+    return c, st
+
+
+def test_grouped_cache_init_and_capacity(lib):
+    import oracle
+    c, st = _fake_grouped()
+    assert st == mf.OK and c.group_keep == 10 and c.n_keep == 128
+    per, _ = _fake_cache()
+    assert per.group_keep == -1
+    # the bound matches the oracle's worst case per group
+    for d, gk, cap in ((64, 16, 64), (128, 10, 96), (256, 3, 32), (128, 0, 33)):
+        assert lib.mustafar_grouped_stream_capacity(d, gk, cap) == \
+            oracle.grouped_stream_capacity(d, gk, (cap + 31) // 32 * 32)
+    assert lib.mustafar_grouped_stream_capacity(96, 10, 32) == -1
+    assert lib.mustafar_grouped_stream_capacity(128, 33, 32) == -1
+    stride = lib.mustafar_grouped_stream_capacity(128, 10, 96)
+    assert _fake_grouped(stride=stride - 8)[1] == mf.EINVAL     # too small for the groups
+    assert _fake_grouped(s=1.5)[1] == mf.EINVAL
+
+
+def test_grouped_calls_reject_before_launch(lib):
+    c, _ = _fake_grouped(cap=96)
+    x, ws = 0x500000, 0x600000
+    need = lib.mustafar_compress_workspace_bytes(2, 4, 64)
+    comp = lambda n=64, **kw: lib.mustafar_prune_compress(  # noqa: E731
+        ctypes.byref(kw.get("c", c)), x, n, ws, need, None)
+    assert comp(n=40) == mf.EINVAL                    # not whole groups
+    assert comp(n=128) == mf.ECAPACITY
+    assert lib.mustafar_append(ctypes.byref(c), x, None) == mf.EINVAL   # groups are whole
+    o = mf.prune_opts_t()
+    ex = lambda opts, **kw: lib.mustafar_prune_compress_ex(  # noqa: E731
+        ctypes.byref(kw.get("c", c)), x, kw.get("n", 64), ctypes.byref(opts), ws, need, None)
+    o.mode = mf.PRUNE_MAGNITUDE
+    assert ex(o) == mf.EINVAL                         # per-token mode on a per-channel cache
+    o.mode = mf.PRUNE_CHANNEL_OUTPUT_AWARE
+    assert ex(o) == mf.EINVAL                         # no token weights
+    o.weights = 0x700002
+    assert ex(o) == mf.EINVAL                         # misaligned weights
+    per, _ = _fake_cache(cap=96)
+    o.mode = mf.PRUNE_CHANNEL
+    o.weights = None
+    assert ex(o, c=per) == mf.EINVAL                  # channel mode on a per-token cache
+    assert ex(o, n=33) == mf.EINVAL
+    assert c.n_tokens == 0
+    # Grouped window lifecycle.
+    w, _ = _fake_window(W=64)
+    K, _ = _fake_cache(B=2, H=4, cap=64)
+    V, _ = _fake_grouped(B=2, H=4, cap=64)
+    kn, vn, acc = 0xf00000, 0xf10000, 0xf30000
+    step = lambda **kw: lib.mustafar_window_step_grouped(  # noqa: E731
+        ctypes.byref(kw.get("w", w)), ctypes.byref(kw.get("K", K)), ctypes.byref(kw.get("V", V)),
+        kn, vn, None, kw.get("acc", acc), None)
+    assert step(V=per) == mf.EINVAL                   # values must be a per-channel cache
+    assert step(K=V) == mf.EINVAL                     # keys per token
+    w32, _ = _fake_window(W=32)
+    assert step(w=w32) == mf.EINVAL                   # at least two groups of slots
+    assert step(acc=acc + 2) == mf.EINVAL
+    wf, _ = _fake_window(W=64, max_len=64)
+    K.n_tokens = V.n_tokens = 64
+    assert step(w=wf) == mf.ECAPACITY                 # no room for a group
+    assert K.n_tokens == 64 and wf.max_len == 64
+    # the per-token step refuses per-channel caches
+    assert lib.mustafar_window_step(ctypes.byref(w), ctypes.byref(K), ctypes.byref(V), kn, vn,
+                                    None, None) == mf.EINVAL
+    # scores: workspace includes the log-sum-exp rows
+    K.n_tokens = V.n_tokens = 32
+    anb = lib.mustafar_attn_workspace_bytes(2, 8, 4, 128, 32, 0)
+    att = lambda **kw: lib.mustafar_window_decode_attn_scores(  # noqa: E731
+        0x700000, 2, 8, ctypes.byref(K), ctypes.byref(V), ctypes.byref(w), kw.get("acc", acc), 0.0,
+        0x800000, 0, 0xb00000, kw.get("ws_bytes", anb), None)
+    assert att(ws_bytes=anb - 4) == mf.EWORKSPACE
+    assert att(acc=acc + 1) == mf.EINVAL
