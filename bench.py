@@ -44,6 +44,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-window", action="store_true", help="skip the dense-window lifecycle leg")
     ap.add_argument("--no-variants", action="store_true", help="skip the pruner-variant leg")
+    ap.add_argument("--no-channel", action="store_true",
+                    help="skip the per-channel value-pruning leg")
+    ap.add_argument("--channel-only", action="store_true",
+                    help="only the per-channel value-pruning leg (for its kernel trace)")
     ap.add_argument("--cpu-sample-streams", type=int, default=256)
     ap.add_argument("--cpu-threads", type=int, default=0, help="0: min(16, cpu count)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -194,6 +198,99 @@ def main():
     torch.cuda.synchronize()
 
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+
+    # ---- per-channel value pruning in groups of 32 tokens: bulk compression of
+    # the prefill values (magnitude and output-aware), attention over per-token
+    # keys + per-channel values, and the grouped window lifecycle with scores ----
+    def channel_leg(v_len_ref):
+        torch.cuda.empty_cache()
+        Vg = mf.CompressedCache(w.B, w.Hkv, w.d, w.sV, cap, device=dev, grouped=True)
+        Kg = mf.CompressedCache(w.B, w.Hkv, w.d, w.sK, cap, device=dev)
+        gtw = torch.Generator(device=dev)
+        gtw.manual_seed(args.seed + 2)
+        tok_w = (torch.rand((w.B, w.Hkv, w.N), generator=gtw, device=dev) * 0.01).float()
+
+        def timed_v(fn, reps=3):
+            ts = []
+            for _ in range(reps):
+                Vg.desc.n_tokens = 0
+                a, b = ev(), ev()
+                a.record()
+                fn()
+                b.record()
+                torch.cuda.synchronize()
+                ts.append(a.elapsed_time(b) / 1e3)
+            return float(np.median(ts))
+
+        vtoks = w.B * w.Hkv * w.N
+        t_oa = timed_v(lambda: mf.mustafar_prune_compress_ex(
+            Vg, Vp, mode=mf.PRUNE_CHANNEL_OUTPUT_AWARE, weights=tok_w, ws=ws_c))
+        t_mag = timed_v(lambda: mf.mustafar_prune_compress(Vg, Vp, ws_c))
+        mf.mustafar_prune_compress(Kg, Kp, ws_c)
+        torch.cuda.synchronize()
+        kg_len = int(Kg.stream_len.to(torch.int64).sum().item())
+        vg_len = int(Vg.stream_len.to(torch.int64).sum().item())
+        for _ in range(3):
+            mf.mustafar_sparse_decode_attn(q, Kg, Vg, KL, VL, out=out, n_splits=args.splits, ws=ws_a)
+        a, b = ev(), ev()
+        reps = 10
+        a.record()
+        for _ in range(reps):
+            mf.mustafar_sparse_decode_attn(q, Kg, Vg, KL, VL, out=out, n_splits=args.splits, ws=ws_a)
+        b.record()
+        torch.cuda.synchronize()
+        t_ga = a.elapsed_time(b) / 1e3 / reps
+        g_bytes = attn_alg_bytes(w, kg_len, vg_len, w.N)
+        del Kg, Vg
+        torch.cuda.empty_cache()
+        # the grouped lifecycle: a 64-slot ring, 32 tokens per stream dense after the prefill
+        Kw = mf.CompressedCache(w.B, w.Hkv, w.d, w.sK, cap + 64, device=dev)
+        Vw = mf.CompressedCache(w.B, w.Hkv, w.d, w.sV, cap + 64, device=dev, grouped=True)
+        win = mf.DenseWindow(w.B, w.Hkv, w.d, 64, device=dev)
+        acc = torch.zeros((w.B, w.Hkv, 64), dtype=torch.float32, device=dev)
+        mf.mustafar_window_prefill(win, Kw, Vw, K, V, [w.N + w.n_tail] * w.B, ws_c)
+        gsteps = 96   # graduations after 33 and 65 steps: two per stream
+
+        def gstep(marks=None):
+            mf.mustafar_window_step_grouped(win, Kw, Vw, new_k, new_v, None, acc)
+            if marks is not None:
+                marks[0].record()
+            mf.mustafar_window_decode_attn_scores(q, Kw, Vw, win, acc, out=out,
+                                                  n_splits=args.splits, ws=ws_a)
+            if marks is not None:
+                marks[1].record()
+
+        torch.cuda.synchronize()
+        gmarks = [(ev(), ev()) for _ in range(gsteps)]
+        a, b = ev(), ev()
+        a.record()
+        for i in range(gsteps):
+            gstep(gmarks[i])
+        b.record()
+        torch.cuda.synchronize()
+        g_total = a.elapsed_time(b) / 1e3 / gsteps
+        g_attn = float(np.mean([m[0].elapsed_time(m[1]) for m in gmarks])) / 1e3
+        channel = {
+            "cache": f"V, {w.sV:.0%} per channel in groups of 32 (keys per token, {w.sK:.0%})",
+            "compress_magnitude_tokens_per_s": vtoks / t_mag,
+            "compress_output_aware_tokens_per_s": vtoks / t_oa,
+            "attention_us": t_ga * 1e6, "attention_gb_s": g_bytes / t_ga / 1e9,
+            "attention_frac": g_bytes / t_ga / 1e9 / HBM_PEAK_GBS, "attention_alg_bytes": g_bytes,
+            "values_stored_vs_per_token": None if v_len_ref is None else vg_len / max(1, v_len_ref),
+            "lifecycle_us_per_step": g_total * 1e6,
+            "lifecycle_attention_scores_us": g_attn * 1e6,
+            "lifecycle_window_step_us": (g_total - g_attn) * 1e6,
+            "how": "mustafar_window_step_grouped + mustafar_window_decode_attn_scores, "
+                   f"64-slot ring, {gsteps} steps, two graduations of 32 tokens per stream"}
+        del Kw, Vw, win, acc, tok_w
+        torch.cuda.empty_cache()
+        return channel
+
+
+    if args.channel_only:
+        print(json.dumps({"channel_pruning": channel_leg(None), "config": {"workload": w.name}}),
+              flush=True)
+        return
 
     # ---- bulk prune + compress of the prefill cache (K and V), timed ----
     pc_ms = []
@@ -352,6 +449,10 @@ def main():
         del Kv, qhist, wts
         torch.cuda.empty_cache()
 
+    channel = None
+    if not args.no_channel:
+        channel = channel_leg(v_len0)
+
     ceiling = read_ceiling_gbs()
 
     result = {
@@ -390,6 +491,7 @@ def main():
         "append_us_per_step": (total_s / steps - attn_s) * 1e6,
         "window_lifecycle": window,
         "prune_variants": variants,
+        "channel_pruning": channel,
         "compression_ratio": comp_kv / dense_kv,
         "wall_s_timed": wall,
     }
