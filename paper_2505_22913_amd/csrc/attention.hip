@@ -181,6 +181,11 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
       uint16_t* qt = reinterpret_cast<uint16_t*>(smem + L.qtab + tt * qtab_stride(1));
       qt[slot] = zero ? (uint16_t)0 : qsrc[kTile * tt + c];
     }
+    // The key region follows the value region, whose last 16 bytes the commits
+    // only ever fill with zeros: zero them once, so that the element before the
+    // first key tile (which the channel-31 product of a tile with an empty lower
+    // half reads, times 0) is never stale LDS content.
+    if (lane == 0) lds_store<u32x4>(lds_addr(smem) + L.kst - 16u, (u32x4){0u, 0u, 0u, 0u});
   }
 
   const int j0 = seg * a.sparse_seg_tokens;
