@@ -138,8 +138,9 @@ size_t mustafar_compress_workspace_bytes(int B, int H, int n_new);
  * compression of the prefill cache before decoding starts, Sec. 3).
  *   x   [B][H][n_new][d] fp16, 16-byte aligned: the dense new tokens
  *   ws  device workspace of at least mustafar_compress_workspace_bytes(),
- *       8-byte aligned; the call clears and uses it (per-chunk scan flags),
- *       so calls that share one workspace must not overlap
+ *       8-byte aligned; the call clears and uses it (per-chunk scan flags
+ *       and per-stream ticket counters), so calls that share one workspace
+ *       must not overlap
  * On success c->n_tokens += n_new. Errors: EINVAL (bad descriptor, n_new < 1,
  * misaligned x), ECAPACITY (n_tokens + n_new > cap_tokens), EWORKSPACE. */
 int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void* ws,

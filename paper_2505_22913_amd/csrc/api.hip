@@ -252,7 +252,8 @@ int mustafar_ccache_init_grouped(mustafar_ccache_t* c, void* bitmaps, void* offs
 size_t mustafar_compress_workspace_bytes(int B, int H, int n_new) {
   if (B < 1 || H < 1 || n_new < 1) return 0;
   const int64_t n_chunks = (n_new + mf::kMinCompressChunk - 1) / mf::kMinCompressChunk;
-  return (size_t)((int64_t)B * H * n_chunks * sizeof(uint64_t) + 16);
+  // per stream: a look-back flag per chunk and a ticket counter
+  return (size_t)((int64_t)B * H * (n_chunks * (int64_t)sizeof(uint64_t) + (int64_t)sizeof(uint32_t)) + 16);
 }
 
 int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void* ws,

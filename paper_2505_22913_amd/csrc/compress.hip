@@ -125,23 +125,29 @@ __global__ void k_clear(uint32_t* __restrict__ p, int64_t n) {
 // release would write back and invalidate the whole L2 of the XCD on every poll.
 //
 // Offset in the stream at which chunk `chunk` starts, computed by one whole
-// wave. The chunk's total is published first; then the wave reads the flags of
-// the 64 chunks before it at once and adds, from the nearest one back, the
-// totals up to and including the first known prefix, moving 64 chunks further
-// back while none is found. Chunks with lower tickets are already running and
+// wave after publish_total: the wave reads the flags of the 64 chunks before it
+// at once and adds, from the nearest one back, the totals up to and including
+// the first known prefix, moving 64 chunks further back while none is found.
+// Chunks with lower tickets (of the same stream) are already running and
 // publish their totals without waiting, so every poll is eventually answered;
 // the poll count is bounded anyway.
-__device__ uint32_t look_back(uint64_t* __restrict__ fl, int chunk, uint32_t total,
-                              uint32_t first_base, uint32_t lane) {
-  if (chunk == 0) {
-    if (lane == 0)
-      __hip_atomic_store(fl, kFlagPrefix | (uint64_t)(first_base + total), __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-    return first_base;
-  }
-  if (lane == 0)
+// The chunk's total (chunk 0: its prefix, first_base + total) is published as
+// soon as it is known, before the chunk packs, so that the chunks after it
+// rarely wait for it.
+__device__ void publish_total(uint64_t* __restrict__ fl, int chunk, uint32_t total, uint32_t first_base,
+                              uint32_t lane) {
+  if (lane != 0) return;
+  if (chunk == 0)
+    __hip_atomic_store(fl, kFlagPrefix | (uint64_t)(first_base + total), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  else
     __hip_atomic_store(fl + chunk, kFlagAgg | (uint64_t)total, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ uint32_t look_back(uint64_t* __restrict__ fl, int chunk, uint32_t total,
+                              uint32_t first_base, uint32_t lane) {
+  if (chunk == 0) return first_base;
   uint32_t acc = 0, polls = 0;
   for (int top = chunk - 1;;) {
     const int p = top - (int)lane;
@@ -244,10 +250,12 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
   __shared__ __align__(16) unsigned char s_rows[TPW * ROW];  // dense rows, then the packed run
 
   const uint32_t lane = lane_id();
+  // Workgroups take the streams in turn and, within a stream, ordered tickets
+  // from the stream's counter (one counter per stream keeps the atomics spread).
+  const int bh = (int)(blockIdx.x % (gridDim.x / (uint32_t)n_chunks));
   uint32_t tk = 0;
-  if (lane == 0) tk = atomicAdd(ticket_ctr, 1u);
-  const int ticket = __builtin_amdgcn_readfirstlane((int)tk);
-  const int bh = ticket / n_chunks, chunk = ticket % n_chunks;
+  if (lane == 0) tk = atomicAdd(ticket_ctr + bh, 1u);
+  const int chunk = __builtin_amdgcn_readfirstlane((int)tk);
   const int j0 = chunk * TPW;
   const int nt = min(TPW, n_new - j0);      // >= 1
   const uint32_t base_lds = (uint32_t)(uintptr_t)s_rows;
@@ -366,16 +374,21 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
   }
   const uint32_t lane_off = incl - lane_len;
   const uint32_t run = (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
+  const uint32_t first = (chunk == 0 && tok0 > 0) ? stream_len[bh] : 0u;
+  publish_total(flags + (int64_t)bh * n_chunks, chunk, run, first, lane);
 
   // Packing, one token at a time with lane = channel (tile bitmaps and offsets
   // read from the selecting lanes). The packed run is written over the rows in
   // place: a token packs into at most d values, so it never reaches the next
   // token's row.
-  uint16_t xn[T];
+  // The next token's values are loaded one iteration ahead, each into a 32-bit
+  // register of its own (two 16-bit values packed in one register would make
+  // the load's wait immediate).
+  uint32_t xn[T];
 #pragma unroll
   for (int t = 0; t < T; ++t) xn[t] = lds_ld<uint16_t>(base_lds + (kTile * t + lane) * 2);
   for (int i = 0; i < nt; ++i) {
-    uint16_t xv[T];
+    uint32_t xv[T];
 #pragma unroll
     for (int t = 0; t < T; ++t) {
       xv[t] = xn[t];
@@ -396,12 +409,11 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
       const bool kept = (bm >> lane) & 1ull;
       const uint32_t slot = kept ? below : cnt + (lane - below);  // dropped lane r fills pad slot r
       if (kept || slot < pad8(cnt))
-        lds_st<uint16_t>(base_lds + (pos + slot) * 2, kept ? xv[t] : (uint16_t)0);
+        lds_st<uint16_t>(base_lds + (pos + slot) * 2, kept ? (uint16_t)xv[t] : (uint16_t)0);
       pos += pad8(cnt);
     }
   }
 
-  const uint32_t first = (chunk == 0 && tok0 > 0) ? stream_len[bh] : 0u;
   const uint32_t base = look_back(flags + (int64_t)bh * n_chunks, chunk, run, first, lane);
   if (lane == 0 && chunk == n_chunks - 1) stream_len[bh] = base == kBadBase ? kBadBase : base + run;
   if (base == kBadBase) return;  // look-back gave up: nothing is written
@@ -824,8 +836,8 @@ static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, i
   const int n_chunks = (n_new + compress_chunk_tokens(T) - 1) / compress_chunk_tokens(T);
   const int64_t n_wg = (int64_t)c.BH * n_chunks;
   uint64_t* flags = reinterpret_cast<uint64_t*>(ws);
-  uint32_t* ticket = reinterpret_cast<uint32_t*>(flags + n_wg);
-  const int64_t words = 2 * n_wg + 1;
+  uint32_t* ticket = reinterpret_cast<uint32_t*>(flags + n_wg);  // [BH]
+  const int64_t words = 2 * n_wg + c.BH;
   const int clear_blocks = (int)((words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024);
   hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, words);
   hipError_t e = hipGetLastError();
@@ -883,8 +895,8 @@ static hipError_t pack_preset_T(const CacheView& c, const uint16_t* x, int n_new
   const int n_chunks = (n_new + compress_chunk_tokens(T) - 1) / compress_chunk_tokens(T);
   const int64_t n_wg = (int64_t)c.BH * n_chunks;
   uint64_t* flags = reinterpret_cast<uint64_t*>(ws);
-  uint32_t* ticket = reinterpret_cast<uint32_t*>(flags + n_wg);
-  const int64_t words = 2 * n_wg + 1;
+  uint32_t* ticket = reinterpret_cast<uint32_t*>(flags + n_wg);  // [BH]
+  const int64_t words = 2 * n_wg + c.BH;
   const int clear_blocks = (int)((words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024);
   hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, words);
   if ((e = hipGetLastError()) != hipSuccess) return e;
