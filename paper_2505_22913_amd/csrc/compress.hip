@@ -36,6 +36,18 @@ __device__ __forceinline__ void lds_st(uint32_t byte_addr, V v) {
   *reinterpret_cast<__attribute__((address_space(3))) V*>(byte_addr) = v;
 }
 
+__device__ __forceinline__ uint32_t ffbl_u32(uint32_t x) {  // 0xffffffff when x == 0
+  uint32_t r;
+  asm("v_ffbl_b32 %0, %1" : "=v"(r) : "v"(x));
+  return r;
+}
+
+__device__ __forceinline__ int wave_max_int(int v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o, kWave));
+  return __builtin_amdgcn_readfirstlane(v);
+}
+
 // Keep-mask of one token. mag[t] is the key of this lane's channel in tile t:
 // the fp16 magnitude (bits & 0x7fff, 15 bits) or a non-negative fp32 score
 // (its bits, 31 bits, order like the values). Sets bm[t] (wave-uniform) so that
@@ -241,13 +253,14 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
                                                     uint32_t* __restrict__ ticket_ctr, int n_chunks,
                                                     int64_t x_stride) {
   constexpr int d = kTile * T;
-  constexpr int LPT = T >= 4 ? 2 : 1;      // lanes per token in the threshold search
+  constexpr int LPT = T >= 2 ? 2 : 1;      // lanes per token (selection and packing)
   constexpr int TPW = kWave / LPT;          // tokens per chunk
   constexpr int CPL = d / LPT;              // channels per lane
   constexpr int NR = CPL / 2;               // packed registers per lane
   constexpr int ROW = d * 2 + 16;           // LDS bytes per token row (pad: conflict-free row reads)
   constexpr int P16 = d / 8;                // 16-byte pieces per row
-  __shared__ __align__(16) unsigned char s_rows[TPW * ROW];  // dense rows, then the packed run
+  __shared__ __align__(16) unsigned char s_rows[TPW * ROW];  // dense rows
+  extern __shared__ __align__(16) unsigned char s_out[];     // the packed run, then a trash slot
 
   const uint32_t lane = lane_id();
   // Workgroups take the streams in turn and, within a stream, ordered tickets
@@ -377,40 +390,40 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
   const uint32_t first = (chunk == 0 && tok0 > 0) ? stream_len[bh] : 0u;
   publish_total(flags + (int64_t)bh * n_chunks, chunk, run, first, lane);
 
-  // Packing, one token at a time with lane = channel (tile bitmaps and offsets
-  // read from the selecting lanes). The packed run is written over the rows in
-  // place: a token packs into at most d values, so it never reaches the next
-  // token's row.
-  // The next token's values are loaded one iteration ahead, each into a 32-bit
-  // register of its own (two 16-bit values packed in one register would make
-  // the load's wait immediate).
-  uint32_t xn[T];
+  // Packing, lane = its tiles: the lane walks the set bits of each tile's mask
+  // in channel order (lower half, then upper half), reads the kept values from
+  // its row and writes them to the chunk's packed run, value r of a tile at
+  // r; the tile's last group of 8 is zeroed first, so its pad slots hold +0.0.
+  // The trip counts are the wave's busiest lane; a lane whose bits are used up
+  // (x - 1 borrows) writes to the trash slot instead.
+  {
+    const uint32_t out_lds = (uint32_t)(uintptr_t)s_out;
+    const uint32_t trash = out_lds + 2u * run;
+    const bool live = (int)lane < nt * LPT;
+    const uint32_t row = base_lds + (uint32_t)(min((int)lane / LPT, nt - 1) * ROW + ((int)lane % LPT) * CPL * 2);
 #pragma unroll
-  for (int t = 0; t < T; ++t) xn[t] = lds_ld<uint16_t>(base_lds + (kTile * t + lane) * 2);
-  for (int i = 0; i < nt; ++i) {
-    uint32_t xv[T];
+    for (int t = 0; t < TPL; ++t) {
+      const uint32_t lo = live ? keep[2 * t] : 0u, hi = live ? keep[2 * t + 1] : 0u;
+      const uint32_t nlo = (uint32_t)__popc(lo), cnt = nlo + (uint32_t)__popc(hi);
+      const uint32_t out = out_lds + 2u * (lane_off + tile_pos[t]);
+      if (cnt & 7u) lds_st<u32x4_t>(out + 16u * (cnt / 8u), (u32x4_t){0u, 0u, 0u, 0u});
 #pragma unroll
-    for (int t = 0; t < T; ++t) {
-      xv[t] = xn[t];
-      if (i + 1 < nt) xn[t] = lds_ld<uint16_t>(base_lds + (i + 1) * ROW + (kTile * t + lane) * 2);
-    }
-    uint32_t pos = (uint32_t)__builtin_amdgcn_readlane((int)lane_off, i * LPT);
+      for (int h = 0; h < 2; ++h) {
+        uint32_t x = h == 0 ? lo : hi;
+        const uint32_t dst = out + (h == 0 ? 0u : 2u * nlo);
+        const uint32_t src = row + (uint32_t)(kTile * t + 32 * h) * 2u;
+        const int n8 = (wave_max_int((int)__popc(x)) + 7) >> 3;
+        for (int g = 0; g < n8; ++g) {
 #pragma unroll
-    for (int t = 0; t < T; ++t) {
-      const int src = i * LPT + t / TPL;         // lane holding tile t of token i
-      const int w0 = 2 * (t % TPL);              // its word pair
-      const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)keep[w0], src);
-      const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)keep[w0 + 1], src);
-      const uint64_t bm = (uint64_t)lo | ((uint64_t)hi << 32);
-      if (LPT == 2 && t == TPL)
-        pos = (uint32_t)__builtin_amdgcn_readlane((int)lane_off, i * LPT + 1);
-      const uint32_t cnt = (uint32_t)__popcll(bm);
-      const uint32_t below = mbcnt(bm, 0u);
-      const bool kept = (bm >> lane) & 1ull;
-      const uint32_t slot = kept ? below : cnt + (lane - below);  // dropped lane r fills pad slot r
-      if (kept || slot < pad8(cnt))
-        lds_st<uint16_t>(base_lds + (pos + slot) * 2, kept ? (uint16_t)xv[t] : (uint16_t)0);
-      pos += pad8(cnt);
+          for (int u = 0; u < 8; ++u) {
+            const uint32_t f = ffbl_u32(x);
+            const bool used_up = x == 0u;
+            x &= x - 1u;
+            const uint16_t v = lds_ld<uint16_t>(src + 2u * (f & 31u));
+            lds_st<uint16_t>(used_up ? trash : dst + 16u * (uint32_t)g + 2u * (uint32_t)u, v);
+          }
+        }
+      }
     }
   }
 
@@ -422,7 +435,7 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
   {
     u32x4_t* dst = reinterpret_cast<u32x4_t*>(values + (int64_t)bh * val_stride + base);
     for (uint32_t c = lane; c < run / 8; c += kWave)
-      __builtin_nontemporal_store(*reinterpret_cast<const u32x4_t*>(s_rows + 16 * c), &dst[c]);
+      __builtin_nontemporal_store(*reinterpret_cast<const u32x4_t*>(s_out + 16 * c), &dst[c]);
   }
   // Bitmaps and offsets of this lane's tiles (tile index = token * T + t).
   if ((int)lane < nt * LPT) {
@@ -830,6 +843,20 @@ __global__ __launch_bounds__(256) void k_window_fill(WindowView w, int b, int d,
   }
 }
 
+// Dynamic LDS of k_compress: the chunk's packed run (tokens of at most `tok`
+// values each) and a 16-byte trash slot.
+inline size_t packed_run_lds(int T, int tok) {
+  return (size_t)compress_chunk_tokens(T) * (size_t)tok * 2u + 16u;
+}
+
+// Worst-case fp16 elements of one token keeping k of d channels (every
+// non-empty tile padded to 8).
+inline int token_max_values(int d, int k) {
+  const int T = d / kTile, nonempty = k < T ? k : T;
+  const int m = (k + 7 * nonempty) / 8 * 8;
+  return m < d ? m : d;
+}
+
 template <int T>
 static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, int64_t x_stride,
                              int tok0, uint32_t* ws, hipStream_t s) {
@@ -842,7 +869,8 @@ static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, i
   hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, words);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_compress<T>, dim3((uint32_t)n_wg), dim3(kWave), 0, s, x, n_new, c.n_keep,
+  hipLaunchKernelGGL(k_compress<T>, dim3((uint32_t)n_wg), dim3(kWave),
+                     packed_run_lds(T, token_max_values(kTile * T, c.n_keep)), s, x, n_new, c.n_keep,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
                      flags, ticket, n_chunks, x_stride);
   return hipGetLastError();
@@ -900,7 +928,8 @@ static hipError_t pack_preset_T(const CacheView& c, const uint16_t* x, int n_new
   const int clear_blocks = (int)((words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024);
   hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, words);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL((k_compress<T, true>), dim3((uint32_t)n_wg), dim3(kWave), 0, s, x, n_new, 0,
+  hipLaunchKernelGGL((k_compress<T, true>), dim3((uint32_t)n_wg), dim3(kWave), packed_run_lds(T, kTile * T),
+                     s, x, n_new, 0,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
                      flags, ticket, n_chunks, x_stride);
   return hipGetLastError();

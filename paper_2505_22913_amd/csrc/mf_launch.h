@@ -6,9 +6,9 @@
 
 namespace mf {
 
-// Tokens per one-wave workgroup of the bulk compression (one lane per token,
-// two lanes per token when d = 256).
-constexpr int compress_chunk_tokens(int T) { return T >= 4 ? 32 : 64; }
+// Tokens per one-wave workgroup of the bulk compression (one lane per token at
+// d = 64, two lanes per token from d = 128 on).
+constexpr int compress_chunk_tokens(int T) { return T >= 2 ? 32 : 64; }
 // Smallest chunk over the supported head sizes (T = 4), for workspace sizing.
 constexpr int kMinCompressChunk = 32;
 
