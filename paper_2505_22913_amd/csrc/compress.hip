@@ -519,23 +519,41 @@ __global__ __launch_bounds__(256) void k_select(CacheView c, const uint16_t* __r
 }
 
 // ---- Per-channel value pruning in groups of 32 tokens (Sec. 2) ---------------------------
-// The keep word of one channel over a group (bit j: token j kept): token j is
-// kept iff fewer than k tokens beat it (a larger key, or an equal key and a
-// lower index). Keys are 15-bit fp16 magnitudes or the bits of non-negative
-// fp32 scores; both order like the values.
+// The keep word of one channel over a group (bit j: token j kept): the k
+// tokens with the largest keys, equal keys to the lower token. Keys are 15-bit
+// fp16 magnitudes (NBITS 15) or the bits of non-negative fp32 scores (NBITS
+// 31); both order like the values. Bit-sliced like the token selection of
+// k_compress: the 32 keys become bit planes of 32-token words (two 16x16
+// transposes of key pairs per 16 bits of key), searched most significant bit
+// first; the threshold ties are then taken lowest token first.
+template <int NBITS>
 __device__ __forceinline__ uint32_t channel_keep_word(const uint32_t (&key)[kGroup], int k) {
-  uint32_t word = 0;
+  if (k <= 0) return 0u;
+  if (k >= kGroup) return 0xffffffffu;
+  constexpr int NP = NBITS > 16 ? 2 : 1;  // 16-bit slices of the key
+  uint32_t pl[NP][16];
 #pragma unroll
-  for (int j = 0; j < kGroup; ++j) {
-    int beat = 0;
+  for (int h = 0; h < NP; ++h) {
 #pragma unroll
-    for (int i = 0; i < kGroup; ++i) {
-      if (i < j) beat += key[i] >= key[j] ? 1 : 0;
-      else if (i > j) beat += key[i] > key[j] ? 1 : 0;
+    for (int r = 0; r < 16; ++r) {
+      const uint32_t a = (key[2 * r] >> (16 * h)) & 0xffffu, c = (key[2 * r + 1] >> (16 * h)) & 0xffffu;
+      pl[h][r] = a | (c << 16);
     }
-    word |= (beat < k ? 1u : 0u) << j;
+    transpose16x2(pl[h]);  // pl[h][b]: bit r = bit 16h+b of key 2r, bit 16+r = of key 2r+1
   }
-  return word;
+  uint32_t cand = 0xffffffffu, above = 0u;
+  int n_above = 0;
+#pragma unroll
+  for (int b = NBITS - 1; b >= 0; --b) {
+    const uint32_t plane = pl[b / 16][b % 16];
+    const uint32_t ones = cand & plane;
+    const int c1 = (int)__popc(ones);
+    const bool take = n_above + c1 >= k;
+    above = take ? above : (above | ones);
+    cand = take ? ones : (cand & ~plane);
+    n_above += take ? 0 : c1;
+  }
+  return interleave_halves(above) | lowest_bits(interleave_halves(cand), k - n_above);
 }
 
 // Key of value x of token j: its fp16 magnitude, or (SCORED) the fp32 product
@@ -584,7 +602,7 @@ __global__ __launch_bounds__(256) void k_select_channel(CacheView c, const uint1
 #pragma unroll
     for (int j = 0; j < kGroup; ++j)
       key[j] = channel_key<SCORED>(x[(row0 + j) * d + kTile * t + lane], SCORED ? w[row0 + j] : 0.f);
-    word[t] = channel_keep_word(key, c.group_keep);
+    word[t] = channel_keep_word<SCORED ? 31 : 15>(key, c.group_keep);
   }
   uint64_t mine[R];
   group_bitmaps<T>(word, lane, mine);
@@ -780,7 +798,7 @@ __global__ __launch_bounds__(256) void k_window_step_grouped(CacheView kc, Cache
         const int sl = (head + j) % w.W;
         key[j] = channel_key<SCORED>(vr[(int64_t)sl * d + kTile * t + lane], SCORED ? ac[sl] : 0.f);
       }
-      word[t] = channel_keep_word(key, vc.group_keep);
+      word[t] = channel_keep_word<SCORED ? 31 : 15>(key, vc.group_keep);
     }
     base = tok > 0 ? vc.stream_len[bh] : 0u;
     for (int u = 0; u < kGroup; ++u) {
