@@ -243,7 +243,7 @@ __device__ __forceinline__ uint32_t lowest_bits(uint32_t w, int n) {
 // PRESET: the keep-masks are the bitmaps already in the cache for these tokens
 // (a pruner variant selected them); only the scan and the packing run.
 template <int T, bool PRESET = false>
-__global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__ x, int n_new, int k,
+__global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__ x, int n_new, int k_all,
                                                     uint64_t* __restrict__ bitmaps,
                                                     uint32_t* __restrict__ offsets,
                                                     uint16_t* __restrict__ values,
@@ -251,7 +251,7 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
                                                     int cap_tokens, int tok0, int64_t val_stride,
                                                     uint64_t* __restrict__ flags,
                                                     uint32_t* __restrict__ ticket_ctr, int n_chunks,
-                                                    int64_t x_stride) {
+                                                    int64_t x_stride, PruneOpts o) {
   constexpr int d = kTile * T;
   constexpr int LPT = T >= 2 ? 2 : 1;      // lanes per token (selection and packing)
   constexpr int TPW = kWave / LPT;          // tokens per chunk
@@ -269,6 +269,7 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
   uint32_t tk = 0;
   if (lane == 0) tk = atomicAdd(ticket_ctr + bh, 1u);
   const int chunk = __builtin_amdgcn_readfirstlane((int)tk);
+  const int k = o.per_head ? o.head_keep[bh % o.H] : k_all;  // kept channels of this stream
   const int j0 = chunk * TPW;
   const int nt = min(TPW, n_new - j0);      // >= 1
   const uint32_t base_lds = (uint32_t)(uintptr_t)s_rows;
@@ -633,6 +634,47 @@ __global__ __launch_bounds__(256) void k_query_lookahead(const uint16_t* __restr
   }
 }
 
+// The same weights for L = 32, 32 consecutive positions per thread: the thread
+// reads the |q| of the 63 positions its windows cover once (zeros past the
+// end, which leave an fp32 sum unchanged) and adds each into the windows that
+// contain it, position by position and query head by query head, so every
+// output gets exactly the additions, in the order, of the one-thread form.
+constexpr int kLookRun = 32;
+
+template <int G>
+__global__ __launch_bounds__(256) void k_query_lookahead32(const uint16_t* __restrict__ q, int B, int Hkv,
+                                                           int n_q, int d, float* __restrict__ w) {
+  constexpr int L = 32;
+  const int runs = (n_q + kLookRun - 1) / kLookRun;
+  const int64_t n = (int64_t)B * Hkv * runs * d;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int c = (int)(i % d);
+  const int run = (int)((i / d) % runs);
+  const int64_t bh = i / ((int64_t)d * runs);
+  const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
+  const int T0 = run * kLookRun;
+  const uint16_t* qb = q + ((int64_t)b * Hkv * G + (int64_t)h * G) * n_q * d + c;
+  float acc[kLookRun];
+#pragma unroll
+  for (int k = 0; k < kLookRun; ++k) acc[k] = 0.f;
+#pragma unroll
+  for (int s = 0; s < kLookRun + L - 1; ++s) {
+    const int t = T0 + s;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float v = t < n_q ? fabsf(half_bits_to_float(qb[((int64_t)g * n_q + t) * d])) : 0.f;
+#pragma unroll
+      for (int k = 0; k < kLookRun; ++k)
+        if (s >= k && s < k + L) acc[k] += v;   // window of output T0 + k: positions k .. k+L-1
+    }
+  }
+  float* wb = w + (bh * n_q + T0) * (int64_t)d + c;
+#pragma unroll
+  for (int k = 0; k < kLookRun; ++k)
+    if (T0 + k < n_q) wb[(int64_t)k * d] = acc[k];
+}
+
 // Prune, compress and append one token (d fp16 at src) to stream bh as token
 // tok: the token's bitmaps and offsets, its packed values after the stream's
 // stream_len values (none when tok == 0), then the new stream_len. One wave.
@@ -877,7 +919,7 @@ inline int token_max_values(int d, int k) {
 
 template <int T>
 static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, int64_t x_stride,
-                             int tok0, uint32_t* ws, hipStream_t s) {
+                             int tok0, uint32_t* ws, hipStream_t s, const PruneOpts& o = PruneOpts{}) {
   const int n_chunks = (n_new + compress_chunk_tokens(T) - 1) / compress_chunk_tokens(T);
   const int64_t n_wg = (int64_t)c.BH * n_chunks;
   uint64_t* flags = reinterpret_cast<uint64_t*>(ws);
@@ -890,7 +932,7 @@ static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, i
   hipLaunchKernelGGL(k_compress<T>, dim3((uint32_t)n_wg), dim3(kWave),
                      packed_run_lds(T, token_max_values(kTile * T, c.n_keep)), s, x, n_new, c.n_keep,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
-                     flags, ticket, n_chunks, x_stride);
+                     flags, ticket, n_chunks, x_stride, o);
   return hipGetLastError();
 }
 
@@ -949,7 +991,7 @@ static hipError_t pack_preset_T(const CacheView& c, const uint16_t* x, int n_new
   hipLaunchKernelGGL((k_compress<T, true>), dim3((uint32_t)n_wg), dim3(kWave), packed_run_lds(T, kTile * T),
                      s, x, n_new, 0,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
-                     flags, ticket, n_chunks, x_stride);
+                     flags, ticket, n_chunks, x_stride, PruneOpts{});
   return hipGetLastError();
 }
 
@@ -981,6 +1023,9 @@ hipError_t launch_compress_channel(const CacheView& c, const uint16_t* x, int n_
 template <int T>
 static hipError_t compress_variant_T(const CacheView& c, const uint16_t* x, int n_new, int tok0,
                                      uint32_t* ws, hipStream_t s, const PruneOpts& o) {
+  // Magnitude pruning with a kept count per head is the bulk compressor with
+  // its stream's count.
+  if (o.mode == kPruneMagnitude) return compress_T<T>(c, x, n_new, (int64_t)n_new, tok0, ws, s, o);
   const int64_t waves = ((int64_t)c.BH * n_new + kTokPerWave - 1) / kTokPerWave;
   hipLaunchKernelGGL(k_select<T>, dim3((uint32_t)((waves + 3) / 4)), dim3(256), 0, s, c, x, n_new,
                      (int64_t)n_new, tok0, o);
@@ -1013,6 +1058,19 @@ hipError_t launch_append_variant(const CacheView& c, const uint16_t* x, int tok0
 
 hipError_t launch_query_lookahead(const uint16_t* q, int B, int Hq, int Hkv, int n_q, int T, int L,
                                   float* w, hipStream_t s) {
+  const int G = Hq / Hkv;
+  if (L == 32 && (G == 1 || G == 2 || G == 4 || G == 8)) {
+    const int64_t n = (int64_t)B * Hkv * ((n_q + kLookRun - 1) / kLookRun) * kTile * T;
+    const dim3 grid((uint32_t)((n + 255) / 256));
+    const int d = kTile * T;
+    switch (G) {
+      case 1: hipLaunchKernelGGL(k_query_lookahead32<1>, grid, dim3(256), 0, s, q, B, Hkv, n_q, d, w); break;
+      case 2: hipLaunchKernelGGL(k_query_lookahead32<2>, grid, dim3(256), 0, s, q, B, Hkv, n_q, d, w); break;
+      case 4: hipLaunchKernelGGL(k_query_lookahead32<4>, grid, dim3(256), 0, s, q, B, Hkv, n_q, d, w); break;
+      default: hipLaunchKernelGGL(k_query_lookahead32<8>, grid, dim3(256), 0, s, q, B, Hkv, n_q, d, w); break;
+    }
+    return hipGetLastError();
+  }
   const int64_t n = (int64_t)B * Hkv * n_q * kTile * T;
   int blocks = (int)((n + 255) / 256);
   blocks = blocks < 1 ? 1 : (blocks > 65536 ? 65536 : blocks);

@@ -40,11 +40,11 @@ constexpr int kPruneMagnitude = 0, kPrune24 = 1, kPruneOutputAware = 2, kPruneCh
               kPruneChannelOutputAware = 4;
 constexpr int kMaxPruneHeads = 256;
 struct PruneOpts {
-  int mode;
-  int H;                      // kv-heads: stream s is head s % H
-  int per_head;               // head_keep holds each head's kept count
-  const float* weights;       // output-aware: fp32 [BH][x_stride][64T] channel weights
-  int32_t head_keep[kMaxPruneHeads];
+  int mode = 0;
+  int H = 1;                  // kv-heads: stream s is head s % H
+  int per_head = 0;           // head_keep holds each head's kept count
+  const float* weights = nullptr;  // output-aware: fp32 [BH][x_stride][64T] channel weights
+  int32_t head_keep[kMaxPruneHeads] = {};
 };
 // Selection (bitmaps of tokens tok0.., one wave per token) then packing with the
 // given bitmaps (k_compress in its preset mode).

@@ -69,7 +69,7 @@ def test_magnitude_through_the_variant_path_equals_the_default():
     compare_format(ga, gb, N, all_pairs(B, H))
 
 
-@pytest.mark.parametrize("G,L", [(1, 32), (4, 32), (2, 5)])
+@pytest.mark.parametrize("G,L", [(1, 32), (4, 32), (2, 5), (2, 32), (8, 32)])
 def test_query_lookahead_bit_exact(G, L):
     announce(f"lookahead G={G} L={L}")
     rng = np.random.default_rng(13 + G)
