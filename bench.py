@@ -471,7 +471,7 @@ def main():
         "config": {"workload": w.name, "batch": w.B, "q_heads": w.Hq, "kv_heads": w.Hkv,
                    "context": w.N, "head_dim": w.d, "window": w.n_tail, "k_sparsity": w.sK,
                    "v_sparsity": w.sV, "splits": args.splits or
-                   mf.mustafar_attn_default_splits(w.B, w.Hkv, n_s_end)},
+                   mf.mustafar_attn_default_splits(w.B, w.Hq, w.Hkv, n_s_end)},
         "attention": {"us": attn_s * 1e6, "tokens_per_s": w.B / attn_s,
                       "kv_tokens_per_s": w.B * w.Hkv * (n_s_end + w.n_tail) / attn_s,
                       "alg_bytes": alg_bytes, "gb_s": attn_gbs},

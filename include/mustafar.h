@@ -218,13 +218,27 @@ int mustafar_append_ex(mustafar_ccache_t* c, const void* x_new, const mustafar_p
 int mustafar_query_lookahead(const void* q, int B, int Hq, int Hkv, int n_q, int d, int L,
                              void* w, void* stream);
 
-/* Split-K segment count chosen when a decode call passes n_splits <= 0. */
-int mustafar_attn_default_splits(int B, int Hkv, int n_tokens);
+/* Kernels behind the decode calls, for mustafar_attn_default_splits:
+ * MUSTAFAR_ATTN_SPARSE for the calls over compressed caches, MUSTAFAR_ATTN_DENSE
+ * for mustafar_dense_decode_attn. */
+enum mustafar_attn_kind {
+    MUSTAFAR_ATTN_SPARSE = 0,
+    MUSTAFAR_ATTN_DENSE = 1
+};
+
+/* Split-K segment count a decode call of the given kind picks when it is
+ * passed n_splits <= 0, for B*Hkv streams of n_tokens tokens (the compressed
+ * tokens for the sparse calls). It depends on the kernel that runs: with one
+ * query head per kv-head, many segments down to one 64-token block; with
+ * grouped queries, about 2048 (sparse) or 4096 (dense) workgroups of at least
+ * 128 tokens. Returns 1 for invalid arguments or kind. */
+int mustafar_attn_default_splits(int B, int Hq, int Hkv, int n_tokens, int kind);
 
 /* Device workspace for the decode-attention calls: fp32 partial results
  * (running max, running sum, d accumulators) for n_splits token ranges plus
  * one dense-window segment, for each of the B*Hq query heads. n_splits <= 0
- * selects mustafar_attn_default_splits(B, Hkv, n_tokens). */
+ * sizes for the larger of the two kinds' default split counts, so the result
+ * serves any decode call over n_tokens tokens that also passes n_splits <= 0. */
 size_t mustafar_attn_workspace_bytes(int B, int Hq, int Hkv, int d, int n_tokens, int n_splits);
 
 /* Decode attention over compressed caches plus a dense local window

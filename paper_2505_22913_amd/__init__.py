@@ -57,6 +57,7 @@ class prune_opts_t(ctypes.Structure):
 
 PRUNE_MAGNITUDE, PRUNE_2_4, PRUNE_OUTPUT_AWARE = 0, 1, 2
 PRUNE_CHANNEL, PRUNE_CHANNEL_OUTPUT_AWARE = 3, 4
+ATTN_SPARSE, ATTN_DENSE = 0, 1
 GROUP = 32  # tokens per group of per-channel value pruning
 
 _SIGS = {
@@ -78,7 +79,7 @@ _SIGS = {
                                                ctypes.c_void_p]),
     "mustafar_append": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
                                        ctypes.c_void_p]),
-    "mustafar_attn_default_splits": (ctypes.c_int, [ctypes.c_int] * 3),
+    "mustafar_attn_default_splits": (ctypes.c_int, [ctypes.c_int] * 5),
     "mustafar_attn_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int] * 6),
     "mustafar_sparse_decode_attn": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
                                                    ctypes.POINTER(ccache_t),
@@ -194,8 +195,9 @@ def mustafar_compress_workspace_bytes(B: int, H: int, n_new: int) -> int:
     return lib().mustafar_compress_workspace_bytes(int(B), int(H), int(n_new))
 
 
-def mustafar_attn_default_splits(B: int, Hkv: int, n_tokens: int) -> int:
-    return lib().mustafar_attn_default_splits(int(B), int(Hkv), int(n_tokens))
+def mustafar_attn_default_splits(B: int, Hq: int, Hkv: int, n_tokens: int,
+                                 kind: int = ATTN_SPARSE) -> int:
+    return lib().mustafar_attn_default_splits(int(B), int(Hq), int(Hkv), int(n_tokens), int(kind))
 
 
 def mustafar_attn_workspace_bytes(B: int, Hq: int, Hkv: int, d: int, n_tokens: int,

@@ -12,8 +12,15 @@ namespace {
 constexpr int kTile = MUSTAFAR_TILE;
 constexpr int kPad = MUSTAFAR_PAD;
 constexpr int kMaxGrid = 65535;            // grid.y limit for the stream index
-constexpr int kTargetWaves = 32768;        // decode: ~10 rounds of ~13 resident waves on 256 CUs
-constexpr int kMinSegTokens = 128;         // decode: smallest useful segment
+// Default decode splits, from split sweeps over the decode workloads. The walk
+// kernel (one query head per kv-head, one wave per segment) wants ~10 rounds of
+// ~13 resident waves on 256 CUs and gains from segments as short as one block;
+// the grouped-query kernels want fewer, longer segments.
+constexpr int kWalkTargetGroups = 32768;
+constexpr int kWalkMinSegTokens = 64;
+constexpr int kMfmaTargetGroups = 2048;
+constexpr int kDenseGroupedTargetGroups = 4096;
+constexpr int kGroupedMinSegTokens = 128;
 constexpr int kSegAlign = 64;              // segments are whole 64-token blocks
 
 bool aligned(const void* p, uintptr_t a) { return p && ((uintptr_t)p % a) == 0; }
@@ -342,11 +349,17 @@ int mustafar_query_lookahead(const void* q, int B, int Hq, int Hkv, int n_q, int
                                               (float*)w, (hipStream_t)stream));
 }
 
-int mustafar_attn_default_splits(int B, int Hkv, int n_tokens) {
-  if (B < 1 || Hkv < 1 || n_tokens < 1) return 1;
+int mustafar_attn_default_splits(int B, int Hq, int Hkv, int n_tokens, int kind) {
+  if (B < 1 || Hkv < 1 || Hq < Hkv || n_tokens < 1) return 1;
+  if (kind != MUSTAFAR_ATTN_SPARSE && kind != MUSTAFAR_ATTN_DENSE) return 1;
+  const bool grouped_q = Hq / Hkv >= 2;
+  const int64_t target = !grouped_q ? kWalkTargetGroups
+                         : kind == MUSTAFAR_ATTN_DENSE ? kDenseGroupedTargetGroups
+                                                       : kMfmaTargetGroups;
+  const int min_seg = grouped_q ? kGroupedMinSegTokens : kWalkMinSegTokens;
   const int64_t streams = (int64_t)B * Hkv;
-  int64_t want = (kTargetWaves + streams - 1) / streams;
-  const int64_t most = (n_tokens + kMinSegTokens - 1) / kMinSegTokens;
+  int64_t want = (target + streams - 1) / streams;
+  const int64_t most = (n_tokens + min_seg - 1) / min_seg;
   if (want > most) want = most;
   if (want < 1) want = 1;
   return (int)want;
@@ -354,7 +367,11 @@ int mustafar_attn_default_splits(int B, int Hkv, int n_tokens) {
 
 size_t mustafar_attn_workspace_bytes(int B, int Hq, int Hkv, int d, int n_tokens, int n_splits) {
   if (B < 1 || Hq < 1 || Hkv < 1 || d < 1 || n_tokens < 0) return 0;
-  if (n_splits <= 0) n_splits = mustafar_attn_default_splits(B, Hkv, n_tokens);
+  if (n_splits <= 0) {
+    const int sp = mustafar_attn_default_splits(B, Hq, Hkv, n_tokens, MUSTAFAR_ATTN_SPARSE);
+    const int dn = mustafar_attn_default_splits(B, Hq, Hkv, n_tokens, MUSTAFAR_ATTN_DENSE);
+    n_splits = sp > dn ? sp : dn;
+  }
   // Segments actually launched never exceed n_splits over the tokens plus one window
   // segment; a two-level merge adds its first-level parts.
   const int64_t n_seg = (int64_t)n_splits + 1;
@@ -376,7 +393,9 @@ static int decode_common(const void* q, int B, int Hq, int Hkv, int d, int n_s, 
   const int G = Hq / Hkv;
   if (G != 1 && G != 2 && G != 4 && G != 8) return MUSTAFAR_EUNSUPPORTED;
   const int n_main = dense_is_window ? n_s : n_dense;
-  if (n_splits <= 0) n_splits = mustafar_attn_default_splits(B, Hkv, n_main > 0 ? n_main : 1);
+  if (n_splits <= 0)
+    n_splits = mustafar_attn_default_splits(B, Hq, Hkv, n_main > 0 ? n_main : 1,
+                                            dense_is_window ? MUSTAFAR_ATTN_SPARSE : MUSTAFAR_ATTN_DENSE);
   if (n_splits > (1 << 20)) return MUSTAFAR_EINVAL;
   const size_t need = mustafar_attn_workspace_bytes(B, Hq, Hkv, d, n_main, n_splits);
   if (!aligned(ws, 16) || ws_bytes < need) return MUSTAFAR_EWORKSPACE;
@@ -571,7 +590,9 @@ int mustafar_window_decode_attn_scores(const void* q, int B, int Hq, const musta
   st = decode_common(q, B, Hq, Kc->H, Kc->d, Kc->n_tokens, w->W, 1, n_splits, scale, out, ws,
                      ws_bytes, &sh, &ws_ml, &ws_o);
   if (st != MUSTAFAR_OK) return st;
-  if (n_splits <= 0) n_splits = mustafar_attn_default_splits(B, Kc->H, Kc->n_tokens > 0 ? Kc->n_tokens : 1);
+  if (n_splits <= 0)
+    n_splits = mustafar_attn_default_splits(B, Hq, Kc->H, Kc->n_tokens > 0 ? Kc->n_tokens : 1,
+                                            MUSTAFAR_ATTN_SPARSE);
   const size_t need = mustafar_attn_workspace_bytes(B, Hq, Kc->H, Kc->d, Kc->n_tokens, n_splits);
   float* lse2 = (float*)((char*)ws + need) - (int64_t)B * Hq;
   sh.n_comp = w->n_comp;

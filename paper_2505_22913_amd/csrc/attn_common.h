@@ -175,7 +175,10 @@ __device__ __forceinline__ void dense_body(const AttnArgs& a, int dseg, int bh, 
       m_run[g] = mnew;
 #pragma unroll
       for (int tt = 0; tt < T; ++tt) o[g][tt] *= alpha;
-      if (t == 0 && valid) ps[j * G + g] = pj;
+      // Every slot's p is stored (0 for a skipped ring slot): the p.V loop below
+      // reads all of the block's slots, and LDS left by an earlier workgroup may
+      // hold non-finite bits.
+      if (t == 0) ps[j * G + g] = pj;
     }
     __syncthreads();
     for (int jj = 0; jj < nb; ++jj) {

@@ -179,6 +179,32 @@ def test_decode_attention_rejects_before_launch(lib):
     assert dense(ws_bytes=16) == mf.EWORKSPACE
 
 
+def test_default_splits_follow_the_kernel(lib):
+    S, D = mf.ATTN_SPARSE, mf.ATTN_DENSE
+    ds = lib.mustafar_attn_default_splits
+    # one query head per kv-head: ~32768 workgroups, segments down to one 64-token block
+    assert ds(16, 32, 32, 32768, S) == 64
+    assert ds(1, 32, 32, 4096, S) == 64
+    assert ds(1, 8, 8, 1024, S) == 16
+    assert ds(1, 8, 8, 1024, D) == 16
+    # grouped queries: ~2048 (sparse) or ~4096 (dense) workgroups of at least 128 tokens
+    assert ds(1, 32, 8, 131072, S) == 256
+    assert ds(1, 32, 8, 131072, D) == 512
+    assert ds(4, 32, 8, 16384, S) == 64
+    assert ds(4, 32, 8, 16384, D) == 128
+    assert ds(1, 32, 8, 300, S) == 3
+    # invalid arguments
+    assert ds(1, 32, 8, 4096, 2) == 1
+    assert ds(0, 32, 8, 4096, S) == 1
+    assert ds(1, 4, 8, 4096, S) == 1
+    assert ds(1, 32, 8, 0, S) == 1
+    # the default workspace covers both kinds' default split counts
+    for B, Hq, Hkv, n in ((1, 32, 8, 131072), (2, 16, 16, 5000), (3, 8, 2, 700)):
+        want = max(lib.mustafar_attn_workspace_bytes(B, Hq, Hkv, 128, n, ds(B, Hq, Hkv, n, k))
+                   for k in (S, D))
+        assert lib.mustafar_attn_workspace_bytes(B, Hq, Hkv, 128, n, 0) == want
+
+
 def test_strerror_covers_every_status(lib):
     for code in (mf.OK, mf.EINVAL, mf.ECAPACITY, mf.EWORKSPACE, mf.ELAUNCH, mf.EUNSUPPORTED):
         assert mf.strerror(code) not in ("", "unknown status")
