@@ -252,32 +252,37 @@ __host__ __device__ inline uint32_t run_region_elems(uint32_t max_run) {
 // past the end returns zeros and reads no memory.
 // The arguments are wave-uniform; readfirstlane states it, so the descriptor
 // stays in scalar registers.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t run_rsrc(const uint16_t* p, uint32_t elems) {
-  const uint64_t a = (uint64_t)(uintptr_t)p;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t run_rsrc_at(uint64_t a, uint32_t elems) {
   const uint64_t u = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(a >> 32)) << 32) |
                      (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
   const int bytes = __builtin_amdgcn_readfirstlane((int)(elems * 2u));
   return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(u), (short)0, bytes, 0x00020000);
 }
 
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t run_rsrc(const uint16_t* p, uint32_t elems) {
+  return run_rsrc_at((uint64_t)(uintptr_t)p, elems);
+}
+
 constexpr int kLoadNT = 2;  // non-temporal: the compressed streams are read once per call
 
-// Chunk c of the block's key run, then of its value run. Every chunk is loaded
-// (no divergent register writes); the descriptors bound each run, so the lanes
-// past its end get zeros.
+// Slot c holds chunk c of the block's key run for c < nck, else chunk c - nck
+// of its value run. Every slot is loaded (no divergent register writes), at
+// byte offset 16 lane + 1 KiB c of one of two descriptors: the key run's, and
+// one that starts nck chunks before the value run and spans those chunks too,
+// so that the same slot offsets land on the value chunks. The hardware bounds
+// each load by its descriptor's size, immediate and scalar offsets included,
+// so the lanes past a run's end get zeros and read no memory.
 template <int STAGE>
 __device__ __forceinline__ void stage_issue(u32x4 (&r)[STAGE], const uint16_t* kv, const uint16_t* vv,
                                             const Runs& rn, uint32_t lane) {
   const uint32_t nck = (rn.kn + kChunk - 1) / kChunk;
+  const __amdgpu_buffer_rsrc_t rk = run_rsrc(kv + rn.kstart, rn.kn);
+  const __amdgpu_buffer_rsrc_t rv =
+      run_rsrc_at((uint64_t)(uintptr_t)(vv + rn.vstart) - 2ull * kChunk * nck, rn.vn + kChunk * nck);
 #pragma unroll
-  for (int c = 0; c < STAGE; ++c) {
-    const bool is_k = (uint32_t)c < nck;
-    const uint32_t first = kChunk * (is_k ? (uint32_t)c : (uint32_t)c - nck);
-    const uint32_t n = is_k ? rn.kn : rn.vn;
-    const uint16_t* src = (is_k ? kv + rn.kstart : vv + rn.vstart) + first;
-    const uint32_t rest = (uint32_t)max((int)n - (int)first, 0);  // scalar max (no VALU saturation)
-    r[c] = __builtin_amdgcn_raw_buffer_load_b128(run_rsrc(src, rest), 16u * lane, 0, kLoadNT);
-  }
+  for (int c = 0; c < STAGE; ++c)
+    r[c] = __builtin_amdgcn_raw_buffer_load_b128((uint32_t)c < nck ? rk : rv, 16u * lane,
+                                                 2u * kChunk * (uint32_t)c, kLoadNT);
 }
 
 // Whole chunks go to LDS (zeros past each run's end), then kMargin zeros after
