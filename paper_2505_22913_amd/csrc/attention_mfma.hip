@@ -150,6 +150,8 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
         const uint32_t slot = (c / 4) * kMSlots + 4u + (ch >= 32u ? 36u : 0u) + (ch % 32u);
         const half4_t ka = lds_load<half4_t>(row + 2u * slot);
         sc[g] = __builtin_amdgcn_mfma_f32_16x16x16f16(ka, qb[c], sc[g], 0, 0, 0);
+        // At most four operand loads ahead of their products (register budget).
+        if (c % 4 == 3) __builtin_amdgcn_sched_barrier(0);
       }
     }
 
@@ -219,6 +221,7 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
         const half4_t vb = lds_load<half4_t>(base + L.vdt + row * Geo::VD_ROW + (16u * g + 4u * q4) * 2u);
         o[c] = __builtin_amdgcn_mfma_f32_16x16x16f16(pa[g], vb, o[c], 0, 0, 0);
       }
+      if (c % 2 == 1) __builtin_amdgcn_sched_barrier(0);
     }
 
     if (has_next) {
@@ -232,9 +235,22 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
   }
 }
 
+// Waves per SIMD that an instance's register budget is set for: three (168
+// VGPRs) where its registers fit without spilling, else two (256), and one for
+// the largest staging at d = 256. Unbounded, the compiler took 196-260 VGPRs at
+// d = 128 (two waves) and 272-353 at d = 256 (one wave); with the operand loads
+// of the two products kept a few MFMAs ahead (the scheduling barriers above)
+// these bounds need no spills.
+template <int T, int G, int STAGE>
+constexpr int mfma_waves() {
+  if ((T == 1 && (STAGE <= 6 || (STAGE == 8 && G <= 4))) || (T == 2 && (STAGE == 4 || (STAGE == 6 && G >= 4))))
+    return 3;
+  return (T == 4 && STAGE == 16) ? 1 : 2;
+}
+
 // Sparse call with G >= 2: grid (n_sparse_segs + n_dense_segs, BHkv).
 template <int T, int G, int STAGE>
-__global__ __launch_bounds__(64) void k_sparse_attn_mfma(AttnArgs a) {
+__global__ __launch_bounds__(64, (mfma_waves<T, G, STAGE>())) void k_sparse_attn_mfma(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int seg = blockIdx.x, bh = blockIdx.y;
   if (seg >= a.n_sparse_segs) {
