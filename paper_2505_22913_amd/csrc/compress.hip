@@ -239,11 +239,18 @@ __device__ __forceinline__ uint32_t lowest_bits(uint32_t w, int n) {
   return w & (p >= 31u ? 0xffffffffu : ((2u << p) - 1u));
 }
 
-// One wave per workgroup; a chunk is 64 tokens (32 when d = 256) of one stream.
+// compress_waves() waves per workgroup; a chunk is that many runs of 64 tokens
+// (32 from d = 128 on) of one stream, one run per wave. The waves select and
+// pack their runs side by side and share the chunk's ticket, scan total and
+// look-back, so those cost once per chunk (two waves: 4% off the bulk
+// compression of a 50% cache against one; four measured the same).
 // PRESET: the keep-masks are the bitmaps already in the cache for these tokens
 // (a pruner variant selected them); only the scan and the packing run.
+template <int T>
+constexpr int compress_waves() { return 2; }
+
 template <int T, bool PRESET = false>
-__global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__ x, int n_new, int k_all,
+__global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const uint16_t* __restrict__ x, int n_new, int k_all,
                                                     uint64_t* __restrict__ bitmaps,
                                                     uint32_t* __restrict__ offsets,
                                                     uint16_t* __restrict__ values,
@@ -253,32 +260,38 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
                                                     uint32_t* __restrict__ ticket_ctr, int n_chunks,
                                                     int64_t x_stride, PruneOpts o) {
   constexpr int d = kTile * T;
+  constexpr int kCompressWaves = compress_waves<T>();
   constexpr int LPT = T >= 2 ? 2 : 1;      // lanes per token (selection and packing)
-  constexpr int TPW = kWave / LPT;          // tokens per chunk
+  constexpr int TPW = kWave / LPT;          // tokens per wave
   constexpr int CPL = d / LPT;              // channels per lane
   constexpr int NR = CPL / 2;               // packed registers per lane
   constexpr int ROW = d * 2 + 16;           // LDS bytes per token row (pad: conflict-free row reads)
   constexpr int P16 = d / 8;                // 16-byte pieces per row
-  __shared__ __align__(16) unsigned char s_rows[TPW * ROW];  // dense rows
+  __shared__ __align__(16) unsigned char s_rows_all[kCompressWaves][TPW * ROW];  // dense rows
+  __shared__ uint32_t s_share[kCompressWaves + 2];  // ticket, the waves' run lengths, the chunk's base
   extern __shared__ __align__(16) unsigned char s_out[];     // the packed run, then a trash slot
 
   const uint32_t lane = lane_id();
+  const int wave = (int)(threadIdx.x / kWave);
+  unsigned char* s_rows = s_rows_all[wave];
   // Workgroups take the streams in turn and, within a stream, ordered tickets
   // from the stream's counter (one counter per stream keeps the atomics spread).
   const int bh = (int)(blockIdx.x % (gridDim.x / (uint32_t)n_chunks));
-  uint32_t tk = 0;
-  if (lane == 0) tk = atomicAdd(ticket_ctr + bh, 1u);
-  const int chunk = __builtin_amdgcn_readfirstlane((int)tk);
+  if (threadIdx.x == 0) s_share[0] = atomicAdd(ticket_ctr + bh, 1u);
+  __syncthreads();
+  const int chunk = __builtin_amdgcn_readfirstlane((int)s_share[0]);
   const int k = o.per_head ? o.head_keep[bh % o.H] : k_all;  // kept channels of this stream
-  const int j0 = chunk * TPW;
-  const int nt = min(TPW, n_new - j0);      // >= 1
+  const int jc = chunk * (kCompressWaves * TPW);                // the chunk's first token
+  const int j0 = jc + wave * TPW;                               // this wave's first token
+  const int nt = min(TPW, n_new - j0);      // <= 0: the chunk ends before this wave's half
   const uint32_t base_lds = (uint32_t)(uintptr_t)s_rows;
 
-  // Stage the chunk's dense rows: 16-byte coalesced non-temporal loads (every
-  // load issued; lanes past the chunk re-read its first piece and store nothing).
+  // Stage the wave's dense rows: 16-byte coalesced non-temporal loads (every
+  // load issued; lanes past the rows re-read the chunk's first piece and store
+  // nothing).
   {
-    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(x + ((int64_t)bh * x_stride + j0) * d);
-    const int n16 = nt * P16;
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(x + ((int64_t)bh * x_stride + (nt > 0 ? j0 : jc)) * d);
+    const int n16 = max(nt, 0) * P16;
     constexpr int kIt = TPW * P16 / kWave;
     u32x4_t r[kIt];
 #pragma unroll
@@ -298,7 +311,7 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
   constexpr int NW = NR / 16;
   uint32_t keep[NW];
   if constexpr (PRESET) {
-    const int jt = min((int)lane / LPT, nt - 1);
+    const int jt = min((int)lane / LPT, max(nt, 1) - 1);
     const int64_t tb = ((int64_t)bh * cap_tokens + tok0 + j0 + jt) * T + ((int)lane % LPT) * (T / LPT);
 #pragma unroll
     for (int t = 0; t < NW / 2; ++t) {
@@ -307,7 +320,7 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
       keep[2 * t + 1] = (uint32_t)(bm >> 32);
     }
   } else {
-    const int jt = min((int)lane / LPT, nt - 1);
+    const int jt = min((int)lane / LPT, max(nt, 1) - 1);
     const unsigned char* row = s_rows + jt * ROW + ((int)lane % LPT) * CPL * 2;
     uint32_t pl[NR];
 #pragma unroll
@@ -386,10 +399,18 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
     const uint32_t v = (uint32_t)__shfl_up((int)incl, o, kWave);
     if ((int)lane >= o) incl += v;
   }
-  const uint32_t lane_off = incl - lane_len;
-  const uint32_t run = (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
+  const uint32_t wave_run = (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
+  if (lane == 0) s_share[1 + wave] = wave_run;
+  __syncthreads();
+  uint32_t run = 0, wave_off = 0;           // the chunk's run: the waves' runs in order
+#pragma unroll
+  for (int w = 0; w < kCompressWaves; ++w) {
+    wave_off = w == wave ? run : wave_off;
+    run += s_share[1 + w];
+  }
+  const uint32_t lane_off = incl - lane_len + wave_off;
   const uint32_t first = (chunk == 0 && tok0 > 0) ? stream_len[bh] : 0u;
-  publish_total(flags + (int64_t)bh * n_chunks, chunk, run, first, lane);
+  if (wave == 0) publish_total(flags + (int64_t)bh * n_chunks, chunk, run, first, lane);
 
   // Packing, lane = its tiles: the lane walks the set bits of each tile's mask
   // in channel order (lower half, then upper half), reads the kept values from
@@ -401,7 +422,7 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
     const uint32_t out_lds = (uint32_t)(uintptr_t)s_out;
     const uint32_t trash = out_lds + 2u * run;
     const bool live = (int)lane < nt * LPT;
-    const uint32_t row = base_lds + (uint32_t)(min((int)lane / LPT, nt - 1) * ROW + ((int)lane % LPT) * CPL * 2);
+    const uint32_t row = base_lds + (uint32_t)(min((int)lane / LPT, max(nt, 1) - 1) * ROW + ((int)lane % LPT) * CPL * 2);
 #pragma unroll
     for (int t = 0; t < TPL; ++t) {
       const uint32_t lo = live ? keep[2 * t] : 0u, hi = live ? keep[2 * t + 1] : 0u;
@@ -428,14 +449,19 @@ __global__ __launch_bounds__(kWave) void k_compress(const uint16_t* __restrict__
     }
   }
 
-  const uint32_t base = look_back(flags + (int64_t)bh * n_chunks, chunk, run, first, lane);
-  if (lane == 0 && chunk == n_chunks - 1) stream_len[bh] = base == kBadBase ? kBadBase : base + run;
+  if (wave == 0) {
+    const uint32_t b = look_back(flags + (int64_t)bh * n_chunks, chunk, run, first, lane);
+    if (lane == 0) s_share[kCompressWaves + 1] = b;
+    if (lane == 0 && chunk == n_chunks - 1) stream_len[bh] = b == kBadBase ? kBadBase : b + run;
+  }
+  __syncthreads();  // the packed run of both waves and the chunk's base
+  const uint32_t base = __builtin_amdgcn_readfirstlane((int)s_share[kCompressWaves + 1]);
   if (base == kBadBase) return;  // look-back gave up: nothing is written
 
   // Packed run (a multiple of 8 values, 16-byte aligned in the stream).
   {
     u32x4_t* dst = reinterpret_cast<u32x4_t*>(values + (int64_t)bh * val_stride + base);
-    for (uint32_t c = lane; c < run / 8; c += kWave)
+    for (uint32_t c = threadIdx.x; c < run / 8; c += kCompressWaves * kWave)
       __builtin_nontemporal_store(*reinterpret_cast<const u32x4_t*>(s_out + 16 * c), &dst[c]);
   }
   // Bitmaps and offsets of this lane's tiles (tile index = token * T + t).
@@ -929,7 +955,7 @@ static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, i
   hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, words);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_compress<T>, dim3((uint32_t)n_wg), dim3(kWave),
+  hipLaunchKernelGGL(k_compress<T>, dim3((uint32_t)n_wg), dim3(compress_waves<T>() * kWave),
                      packed_run_lds(T, token_max_values(kTile * T, c.n_keep)), s, x, n_new, c.n_keep,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
                      flags, ticket, n_chunks, x_stride, o);
@@ -988,7 +1014,7 @@ static hipError_t pack_preset_T(const CacheView& c, const uint16_t* x, int n_new
   const int clear_blocks = (int)((words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024);
   hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, words);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL((k_compress<T, true>), dim3((uint32_t)n_wg), dim3(kWave), packed_run_lds(T, kTile * T),
+  hipLaunchKernelGGL((k_compress<T, true>), dim3((uint32_t)n_wg), dim3(compress_waves<T>() * kWave), packed_run_lds(T, kTile * T),
                      s, x, n_new, 0,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
                      flags, ticket, n_chunks, x_stride, PruneOpts{});

@@ -6,11 +6,11 @@
 
 namespace mf {
 
-// Tokens per one-wave workgroup of the bulk compression (one lane per token at
+// Tokens per two-wave workgroup of the bulk compression (one lane per token at
 // d = 64, two lanes per token from d = 128 on).
-constexpr int compress_chunk_tokens(int T) { return T >= 2 ? 32 : 64; }
-// Smallest chunk over the supported head sizes (T = 4), for workspace sizing.
-constexpr int kMinCompressChunk = 32;
+constexpr int compress_chunk_tokens(int T) { return T >= 2 ? 64 : 128; }
+// Smallest chunk over the supported head sizes, for workspace sizing.
+constexpr int kMinCompressChunk = 64;
 
 struct CacheView {
   uint64_t* bitmaps;

@@ -118,9 +118,9 @@ def test_ccache_init_validates(lib):
 def test_compress_and_append_reject_before_launch(lib):
     c, _ = _fake_cache(B=2, H=4, cap=100)
     ws_need = lib.mustafar_compress_workspace_bytes(2, 4, 50)
-    # per stream: one 8-byte scan flag per 32-token chunk and a 4-byte ticket counter
-    assert ws_need == 2 * 4 * (2 * 8 + 4) + 16
-    assert lib.mustafar_compress_workspace_bytes(1, 1, 65) == 3 * 8 + 4 + 16
+    # per stream: one 8-byte scan flag per 64-token chunk and a 4-byte ticket counter
+    assert ws_need == 2 * 4 * (1 * 8 + 4) + 16
+    assert lib.mustafar_compress_workspace_bytes(1, 1, 65) == 2 * 8 + 4 + 16
     x = 0x500000
     assert lib.mustafar_prune_compress(ctypes.byref(c), x, 0, 0x600000, ws_need, None) == mf.EINVAL
     assert lib.mustafar_prune_compress(ctypes.byref(c), x + 2, 50, 0x600000, ws_need,
