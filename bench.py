@@ -404,6 +404,43 @@ def main():
                   "how": "mustafar_window_step + mustafar_window_decode_attn, ring of "
                          f"{w.n_tail} tokens per stream"}
         del Kw, Vw, win
+        torch.cuda.empty_cache()
+
+        # The same steps with output-aware keys: the leaving key is pruned with the
+        # weights its window slot gathered from the queries of its 32 steps.
+        Kw = mf.CompressedCache(w.B, w.Hkv, w.d, w.sK, cap, device=dev)
+        Vw = mf.CompressedCache(w.B, w.Hkv, w.d, w.sV, cap, device=dev)
+        win = mf.DenseWindow(w.B, w.Hkv, w.d, w.n_tail, device=dev)
+        kacc = torch.zeros((w.B, w.Hkv, w.n_tail, w.d), dtype=torch.float32, device=dev)
+        mf.mustafar_window_prefill(win, Kw, Vw, K, V, [w.N + w.n_tail] * w.B, ws_c)
+
+        def kstep(marks=None):
+            mf.mustafar_window_step_weighted(win, Kw, Vw, new_k, new_v, kacc)
+            mf.mustafar_window_decode_attn(q, Kw, Vw, win, out=out, n_splits=args.splits, ws=ws_a)
+            if marks is not None:
+                marks[0].record()
+            mf.mustafar_window_key_weights(q, win, kacc)
+            if marks is not None:
+                marks[1].record()
+
+        for _ in range(warm):
+            kstep()
+        torch.cuda.synchronize()
+        kmarks = [(ev(), ev()) for _ in range(steps)]
+        a, b = ev(), ev()
+        a.record()
+        for i in range(steps):
+            kstep(kmarks[i])
+        b.record()
+        torch.cuda.synchronize()
+        k_total = a.elapsed_time(b) / 1e3 / steps
+        k_kw = float(np.mean([m[0].elapsed_time(m[1]) for m in kmarks])) / 1e3
+        window["output_aware_keys"] = {
+            "us_per_step": k_total * 1e6, "key_weights_us": k_kw * 1e6,
+            "tokens_per_s": w.B / k_total,
+            "how": "mustafar_window_step_weighted + mustafar_window_decode_attn + "
+                   "mustafar_window_key_weights (|q| of the step into the newest 32 slots)"}
+        del Kw, Vw, win, kacc
 
     # ---- pruner variants on the same prefill cache (K: N tokens per stream) ----
     variants = None

@@ -329,6 +329,34 @@ int mustafar_window_prefill(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafa
 int mustafar_window_step(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
                          const void* k_new, const void* v_new, const void* active, void* stream);
 
+/* Output-aware key pruning in the window lifecycle (Sec. 2: a key's channels
+ * are scored by |K| times the L1 sum of the query at its position and the 31
+ * after it, summed over the query heads of its kv-head). kacc [B][H][W][d] is
+ * fp32 device memory, 16-byte aligned, owned by the caller and zeroed by it
+ * before the window's prefill; window slot s of (b, h) holds the weights of the
+ * token in that slot. Each call adds |q[b][h*G+g][c]| (fp16 q [B][Hq][d],
+ * 16-byte aligned; G = Hq/H), for g = 0, 1, ..., G-1 one after the other in
+ * fp32, to kacc[b][h][s][c] for every batch entry b, kv-head h and slot s
+ * holding one of the newest min(len[b], 32) window tokens. Called once per
+ * decode step with that step's queries, after the step's
+ * mustafar_window_step_weighted, it leaves a token that leaves the window 32
+ * steps after it arrived with the weights mustafar_query_lookahead (L = 32)
+ * computes from the same queries, bit for bit. Errors: EINVAL, EUNSUPPORTED
+ * (G > 8). */
+int mustafar_window_key_weights(const void* q, int B, int Hq, const mustafar_window_t* w,
+                                float* kacc, void* stream);
+
+/* mustafar_window_step whose leaving key (the oldest token of a full window)
+ * is pruned output-aware: channel score fl32(|k_c| x kacc[b][h][slot][c]), the
+ * larger first, ties to the lower channel (the selection of
+ * MUSTAFAR_PRUNE_OUTPUT_AWARE); its value is pruned by magnitude as before. The
+ * slot that takes the new token gets weights 0. Needs W >= 32, so that a key
+ * leaves with the weights of 32 steps. Errors as mustafar_window_step, and
+ * EINVAL for W < 32 or a misaligned kacc. */
+int mustafar_window_step_weighted(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
+                                  const void* k_new, const void* v_new, const void* active,
+                                  float* kacc, void* stream);
+
 /* Decode attention of Algorithm 1 per batch entry b over its n_comp[b]
  * compressed tokens and the len[b] tokens of its window (the window is
  * Algorithm 1's dense local part). Every batch entry must hold at least one

@@ -23,21 +23,41 @@ from __future__ import annotations
 import numpy as np
 
 from . import (GROUP, attention_probs, compress, decode_attention, decompress, encode,
-               keep_count, prune_channel_group, prune_token, sparse_decode_attention)
+               keep_count, prune_channel_group, prune_token, prune_token_scored,
+               sparse_decode_attention)
+
+# Output-aware keys: a key's weights sum the query at its position and the 31
+# after it (Sec. 2).
+KEY_WEIGHT_STEPS = 32
 
 
 class WindowOracle:
     """Token history of a batch of B entries with H kv-heads of dimension d.
 
     ``sk`` and ``sv`` are the K and V sparsities, ``W`` the window length.
+
+    With ``output_aware_keys`` the keys that leave the window are pruned by the
+    output-aware score of Sec. 2 instead of by magnitude: every call of
+    ``accumulate_key_weights`` (one per decode step, with that step's queries)
+    adds |q| of each query head of a kv-head, one head after the other in
+    float32, to the channel weights of each of the entry's newest 32 window
+    tokens, and a key leaves with channels ranked by fl32(|k_c| * w_c). A token
+    that leaves 32 steps after it arrived thus carries the sum over the query
+    of its own step and the 31 after it, as ``query_lookahead`` adds them. The
+    tokens a prefill compresses at once have no decode queries and are pruned
+    by magnitude.
     """
 
-    def __init__(self, B: int, H: int, d: int, W: int, sk: float, sv: float):
+    def __init__(self, B: int, H: int, d: int, W: int, sk: float, sv: float,
+                 output_aware_keys: bool = False):
         self.B, self.H, self.d, self.W = B, H, d, W
         self.sk, self.sv = sk, sv
         # hist_k[b] is a list of [H][d] uint16 arrays, one per arrived token.
         self.hist_k = [[] for _ in range(B)]
         self.hist_v = [[] for _ in range(B)]
+        self.output_aware_keys = output_aware_keys
+        self.key_w = [dict() for _ in range(B)]   # token index -> float32 [H][d]
+        self.n_prefill = [0] * B                  # tokens the prefill compressed
 
     # ---- arrivals ------------------------------------------------------------------------
     def prefill(self, xk, xv, seq_len) -> None:
@@ -48,6 +68,31 @@ class WindowOracle:
             for j in range(int(seq_len[b])):
                 self.hist_k[b].append(np.array(xk[b, :, j]))
                 self.hist_v[b].append(np.array(xv[b, :, j]))
+            self.n_prefill[b] = self.n_comp(b)
+
+    def accumulate_key_weights(self, q) -> None:
+        """One decode step's queries q [B][Hq][d] (fp16) into the key weights of the
+        newest KEY_WEIGHT_STEPS window tokens of every entry."""
+        qa = np.abs(np.asarray(q).view(np.float16).astype(np.float32))
+        G = qa.shape[1] // self.H
+        for b in range(self.B):
+            n, L = self.n_comp(b), self.window_len(b)
+            for p in range(max(0, L - KEY_WEIGHT_STEPS), L):
+                w = self.key_w[b].setdefault(n + p, np.zeros((self.H, self.d), dtype=np.float32))
+                for h in range(self.H):
+                    for g in range(G):
+                        w[h] = w[h] + qa[b, h * G + g]
+
+    def key_weights(self, b: int, j: int) -> np.ndarray:
+        """float32 [H][d] weights of token j of entry b (zeros if it has none)."""
+        return self.key_w[b].get(j, np.zeros((self.H, self.d), dtype=np.float32))
+
+    def _key_keep(self, b: int, j: int, h: int) -> np.ndarray:
+        x = self.hist_k[b][j][h]
+        k = _keep_count(self.d, self.sk)
+        if self.output_aware_keys and j >= self.n_prefill[b]:
+            return prune_token_scored(x, self.key_weights(b, j)[h], k)
+        return prune_token(x, k)
 
     def step(self, k_new, v_new, active=None) -> None:
         """Active entries receive one token each: k_new, v_new [B][H][d]."""
@@ -84,7 +129,13 @@ class WindowOracle:
         n = self.n_comp(b)
         k = self._tokens(self.hist_k, b, 0, n)[None]
         v = self._tokens(self.hist_v, b, 0, n)[None]
-        return compress(k, self.sk), compress(v, self.sv)
+        if not self.output_aware_keys:
+            return compress(k, self.sk), compress(v, self.sv)
+        keep = np.zeros((1, self.H, n, self.d), dtype=bool)
+        for j in range(n):
+            for h in range(self.H):
+                keep[0, h, j] = self._key_keep(b, j, h)
+        return encode(k, keep), compress(v, self.sv)
 
     # ---- attention -----------------------------------------------------------------------
     def attention(self, q, b: int, scale: float = 0.0) -> np.ndarray:
@@ -104,11 +155,10 @@ class WindowOracle:
         kk = np.ascontiguousarray(self._tokens(self.hist_k, b, 0, self.arrived(b)))
         vv = np.ascontiguousarray(self._tokens(self.hist_v, b, 0, self.arrived(b)))
         kk, vv = kk.copy(), vv.copy()
-        kkeep = _keep_count(self.d, self.sk)
         vkeep = _keep_count(self.d, self.sv)
         for h in range(self.H):
             for j in range(n):
-                kk[h, j][~prune_token(kk[h, j], kkeep)] = 0
+                kk[h, j][~self._key_keep(b, j, h)] = 0
                 vv[h, j][~prune_token(vv[h, j], vkeep)] = 0
         return decode_attention(q, kk[None], vv[None], None, None, scale)[0]
 

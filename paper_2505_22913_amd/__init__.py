@@ -102,6 +102,13 @@ _SIGS = {
     "mustafar_window_step": (ctypes.c_int, [ctypes.POINTER(window_t), ctypes.POINTER(ccache_t),
                                             ctypes.POINTER(ccache_t), ctypes.c_void_p,
                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "mustafar_window_step_weighted": (ctypes.c_int, [ctypes.POINTER(window_t), ctypes.POINTER(ccache_t),
+                                                     ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                                     ctypes.c_void_p]),
+    "mustafar_window_key_weights": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                                   ctypes.POINTER(window_t), ctypes.c_void_p,
+                                                   ctypes.c_void_p]),
     "mustafar_window_decode_attn": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
                                                    ctypes.POINTER(ccache_t),
                                                    ctypes.POINTER(ccache_t),
@@ -411,6 +418,24 @@ def mustafar_window_step(win: DenseWindow, Kc: CompressedCache, Vc: CompressedCa
     _check("mustafar_window_step", lib().mustafar_window_step(
         ctypes.byref(win.desc), ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), _dptr(k_new),
         _dptr(v_new), _dptr(active), _stream(stream)))
+
+
+def mustafar_window_step_weighted(win: DenseWindow, Kc: CompressedCache, Vc: CompressedCache, k_new,
+                                  v_new, kacc, active=None, stream=None) -> None:
+    """mustafar_window_step whose leaving key is pruned output-aware with its window
+    slot's weights in kacc [B][H][W][d] (fp32, device); the new token's weights start
+    at 0."""
+    _check("mustafar_window_step_weighted", lib().mustafar_window_step_weighted(
+        ctypes.byref(win.desc), ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), _dptr(k_new),
+        _dptr(v_new), _dptr(active), _dptr(kacc), _stream(stream)))
+
+
+def mustafar_window_key_weights(q, win: DenseWindow, kacc, stream=None) -> None:
+    """kacc[b][h][slot] += |q| of the query heads of kv-head h (one after the other, in
+    fp32) for the newest 32 window tokens of every entry; q [B][Hq][d] fp16."""
+    B, Hq, _ = (int(s) for s in q.shape)
+    _check("mustafar_window_key_weights", lib().mustafar_window_key_weights(
+        _dptr(q), B, Hq, ctypes.byref(win.desc), _dptr(kacc), _stream(stream)))
 
 
 def mustafar_window_decode_attn(q, Kc: CompressedCache, Vc: CompressedCache, win: DenseWindow,

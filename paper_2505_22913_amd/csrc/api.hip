@@ -22,6 +22,7 @@ constexpr int kMfmaTargetGroups = 2048;
 constexpr int kDenseGroupedTargetGroups = 4096;
 constexpr int kGroupedMinSegTokens = 128;
 constexpr int kSegAlign = 64;              // segments are whole 64-token blocks
+constexpr int kKeyWeightSteps = 32;        // output-aware keys: the current and 31 next queries
 
 bool aligned(const void* p, uintptr_t a) { return p && ((uintptr_t)p % a) == 0; }
 bool head_dim_ok(int d) { return d == 64 || d == 128 || d == 256; }
@@ -529,8 +530,38 @@ int mustafar_window_prefill(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafa
   return MUSTAFAR_OK;
 }
 
+static int window_step_common(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
+                              const void* k_new, const void* v_new, const void* active, float* kacc,
+                              void* stream);
+
 int mustafar_window_step(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
                          const void* k_new, const void* v_new, const void* active, void* stream) {
+  return window_step_common(w, Kc, Vc, k_new, v_new, active, nullptr, stream);
+}
+
+int mustafar_window_step_weighted(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
+                                  const void* k_new, const void* v_new, const void* active,
+                                  float* kacc, void* stream) {
+  int st = check_window(w);
+  if (st != MUSTAFAR_OK) return st;
+  if (w->W < kKeyWeightSteps || !aligned(kacc, 16)) return MUSTAFAR_EINVAL;
+  return window_step_common(w, Kc, Vc, k_new, v_new, active, kacc, stream);
+}
+
+int mustafar_window_key_weights(const void* q, int B, int Hq, const mustafar_window_t* w, float* kacc,
+                                void* stream) {
+  int st = check_window(w);
+  if (st != MUSTAFAR_OK) return st;
+  if (B != w->B || Hq < 1 || Hq % w->H != 0) return MUSTAFAR_EINVAL;
+  if (Hq / w->H > 8) return MUSTAFAR_EUNSUPPORTED;
+  if (!aligned(q, 16) || !aligned(kacc, 16)) return MUSTAFAR_EINVAL;
+  return status_of(mf::launch_window_key_weights(window_view_of(w), (const uint16_t*)q, Hq / w->H,
+                                                 w->d / kTile, kacc, (hipStream_t)stream));
+}
+
+static int window_step_common(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
+                              const void* k_new, const void* v_new, const void* active, float* kacc,
+                              void* stream) {
   int st = check_window(w);
   if (st != MUSTAFAR_OK) return st;
   if ((st = check_cache(Kc)) != MUSTAFAR_OK || (st = check_cache(Vc)) != MUSTAFAR_OK) return st;
@@ -543,7 +574,7 @@ int mustafar_window_step(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_c
     return MUSTAFAR_ECAPACITY;
   st = status_of(mf::launch_window_step(view_of(Kc), view_of(Vc), window_view_of(w), (const uint16_t*)k_new,
                                         (const uint16_t*)v_new, (const int32_t*)active,
-                                        (hipStream_t)stream));
+                                        (hipStream_t)stream, kacc));
   if (st != MUSTAFAR_OK) return st;
   if (may_graduate) {
     Kc->n_tokens += 1;

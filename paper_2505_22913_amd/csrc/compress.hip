@@ -475,6 +475,22 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
   }
 }
 
+// Output-aware keep-mask of one token, lane = channel: the score |x| * w in
+// fp32 (one rounding) of channel 64 t + lane, w the token's fp32 channel
+// weights; non-negative, so its bits order like its value (31 significant bits).
+template <int T>
+__device__ __forceinline__ void select_output_aware(int k, const uint16_t (&xv)[T],
+                                                    const float* __restrict__ w, uint32_t lane,
+                                                    uint64_t (&bm)[T]) {
+  uint32_t key[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const float m = fabsf(half_bits_to_float(xv[t]));
+    key[t] = __builtin_bit_cast(uint32_t, m * w[kTile * t + lane]);
+  }
+  select_token<T, 31>(key, k, bm);
+}
+
 // Keep-mask of one token under a pruner variant, lane = channel; xv[t] is the
 // lane's fp16 bits in tile t, w the token's fp32 channel weights (output-aware).
 template <int T>
@@ -497,15 +513,7 @@ __device__ __forceinline__ void select_variant(const PruneOpts& o, int k, const 
       bm[t] = ballot(wins >= 2);
     }
   } else if (o.mode == kPruneOutputAware) {
-    // Score |x| * w in fp32 (one rounding); non-negative, so its bits order
-    // like its value (31 significant bits).
-    uint32_t key[T];
-#pragma unroll
-    for (int t = 0; t < T; ++t) {
-      const float m = fabsf(half_bits_to_float(xv[t]));
-      key[t] = __builtin_bit_cast(uint32_t, m * w[kTile * t + lane]);
-    }
-    select_token<T, 31>(key, k, bm);
+    select_output_aware<T>(k, xv, w, lane, bm);
   } else {
     uint32_t mag[T];
 #pragma unroll
@@ -762,16 +770,39 @@ __global__ __launch_bounds__(256) void k_append(CacheView c, const uint16_t* __r
   append_one<T>(c, bh, tok0, x + (int64_t)bh * kTile * T, lane_id());
 }
 
+// append_one with output-aware selection: w the token's fp32 channel weights.
+template <int T>
+__device__ __forceinline__ void append_one_weighted(const CacheView& c, int bh, int tok,
+                                                    const uint16_t* __restrict__ src,
+                                                    const float* __restrict__ w, uint32_t lane) {
+  const uint32_t base = tok > 0 ? c.stream_len[bh] : 0u;
+  uint16_t xv[T];
+  load_token<T>(src, lane, xv);
+  uint64_t bm[T];
+  select_output_aware<T>(c.n_keep, xv, w, lane, bm);
+  const int64_t tile0 = ((int64_t)bh * c.cap_tokens + tok) * T;
+  uint64_t mine = bm[0];
+#pragma unroll
+  for (int t = 1; t < T; ++t) mine = (lane == (uint32_t)t) ? bm[t] : mine;
+  if (lane < (uint32_t)T) c.bitmaps[tile0 + lane] = mine;
+  const uint32_t used =
+      pack_token<T>(xv, bm, base, c.values + (int64_t)bh * c.val_stride, c.offsets + tile0, lane);
+  if (lane == 0) c.stream_len[bh] = base + used;
+}
+
 // Window step, one wave per stream: if the batch entry's window is full, its
 // oldest token (slot head) goes to both compressed caches as token n_comp and
 // the new token takes its slot; otherwise the new token goes to slot
 // (head + len) % W. The per-entry counters advance in k_window_commit, after
-// every stream of the entry has read them.
-template <int T>
+// every stream of the entry has read them. WEIGHTED: the leaving key is pruned
+// output-aware with its slot's accumulated weights kacc [BH][W][d], and the
+// new token's weights start at 0.
+template <int T, bool WEIGHTED = false>
 __global__ __launch_bounds__(256) void k_window_step(CacheView kc, CacheView vc, WindowView w,
                                                      const uint16_t* __restrict__ k_new,
                                                      const uint16_t* __restrict__ v_new,
-                                                     const int32_t* __restrict__ active) {
+                                                     const int32_t* __restrict__ active,
+                                                     float* __restrict__ kacc = nullptr) {
   constexpr int d = kTile * T;
   const int bh = blockIdx.x * (256 / kWave) + threadIdx.x / kWave;
   if (bh >= kc.BH) return;
@@ -787,7 +818,11 @@ __global__ __launch_bounds__(256) void k_window_step(CacheView kc, CacheView vc,
     slot = head;
     const int tok = w.n_comp[b];
     if (tok >= 0 && tok < kc.cap_tokens && tok < vc.cap_tokens) {  // guaranteed by the host's bound
-      append_one<T>(kc, bh, tok, kr + (int64_t)slot * d, lane);
+      if constexpr (WEIGHTED)
+        append_one_weighted<T>(kc, bh, tok, kr + (int64_t)slot * d, kacc + ((int64_t)bh * w.W + slot) * d,
+                               lane);
+      else
+        append_one<T>(kc, bh, tok, kr + (int64_t)slot * d, lane);
       append_one<T>(vc, bh, tok, vr + (int64_t)slot * d, lane);
     }
   }
@@ -797,6 +832,62 @@ __global__ __launch_bounds__(256) void k_window_step(CacheView kc, CacheView vc,
   for (int t = 0; t < T; ++t) {
     kr[(int64_t)slot * d + kTile * t + lane] = k_new[(int64_t)bh * d + kTile * t + lane];
     vr[(int64_t)slot * d + kTile * t + lane] = v_new[(int64_t)bh * d + kTile * t + lane];
+    if constexpr (WEIGHTED) kacc[((int64_t)bh * w.W + slot) * d + kTile * t + lane] = 0.f;
+  }
+}
+
+// Output-aware key weights of the window (see mustafar_window_key_weights): a
+// 256-thread block per (entry, kv-head); a thread owns four channels of some of
+// the newest kKeyWeightSteps slots, loads all of them before it adds and
+// stores (no load waits on a store), and adds the |q| of the G query heads one
+// by one, head order.
+constexpr int kKeyWeightSteps = 32;
+
+template <int T>
+__global__ __launch_bounds__(256) void k_window_key_weights(WindowView w, const uint16_t* __restrict__ q,
+                                                            int G, float* __restrict__ kacc) {
+  constexpr int d = kTile * T;
+  constexpr int C4 = d / 4;                  // four-channel columns per slot
+  constexpr int ROWS = 256 / C4;             // slots per pass of the block
+  constexpr int PASSES = kKeyWeightSteps / ROWS;
+  const int bh = blockIdx.x;
+  const int b = bh / w.H;
+  const int len = w.len[b], head = w.head[b];
+  if (len <= 0 || len > w.W || head < 0 || head >= w.W) return;
+  const int c4 = (int)threadIdx.x % C4, r0 = (int)threadIdx.x / C4;
+  const int n = min(len, kKeyWeightSteps), p0 = len - n;
+  float aq[8][4];
+#pragma unroll
+  for (int g = 0; g < 8; ++g) {
+    uint2 h2 = {0u, 0u};
+    if (g < G) h2 = *reinterpret_cast<const uint2*>(q + ((int64_t)bh * G + g) * d + 4 * c4);
+    aq[g][0] = fabsf(half_bits_to_float((uint16_t)h2.x));
+    aq[g][1] = fabsf(half_bits_to_float((uint16_t)(h2.x >> 16)));
+    aq[g][2] = fabsf(half_bits_to_float((uint16_t)h2.y));
+    aq[g][3] = fabsf(half_bits_to_float((uint16_t)(h2.y >> 16)));
+  }
+  float4 v[PASSES];
+  float4* a[PASSES];
+#pragma unroll
+  for (int i = 0; i < PASSES; ++i) {
+    const int r = r0 + ROWS * i;
+    a[i] = r < n ? reinterpret_cast<float4*>(kacc + ((int64_t)bh * w.W + (head + p0 + r) % w.W) * d) + c4
+                 : nullptr;
+    if (a[i]) v[i] = *a[i];
+  }
+#pragma unroll
+  for (int i = 0; i < PASSES; ++i) {
+    if (!a[i]) continue;
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      if (g < G) {
+        v[i].x += aq[g][0];
+        v[i].y += aq[g][1];
+        v[i].z += aq[g][2];
+        v[i].w += aq[g][3];
+      }
+    }
+    *a[i] = v[i];
   }
 }
 
@@ -972,9 +1063,13 @@ static hipError_t append_T(const CacheView& c, const uint16_t* x, int tok0, hipS
 template <int T>
 static hipError_t window_step_T(const CacheView& kc, const CacheView& vc, const WindowView& w,
                                 const uint16_t* k_new, const uint16_t* v_new, const int32_t* active,
-                                hipStream_t s) {
-  hipLaunchKernelGGL(k_window_step<T>, dim3((kc.BH + 3) / 4), dim3(256), 0, s, kc, vc, w, k_new, v_new,
-                     active);
+                                hipStream_t s, float* kacc) {
+  if (kacc != nullptr)
+    hipLaunchKernelGGL((k_window_step<T, true>), dim3((kc.BH + 3) / 4), dim3(256), 0, s, kc, vc, w, k_new,
+                       v_new, active, kacc);
+  else
+    hipLaunchKernelGGL((k_window_step<T, false>), dim3((kc.BH + 3) / 4), dim3(256), 0, s, kc, vc, w, k_new,
+                       v_new, active, nullptr);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_window_commit, dim3((w.B + 255) / 256), dim3(256), 0, s, w, active);
@@ -1145,13 +1240,25 @@ hipError_t launch_window_step_grouped(const CacheView& kc, const CacheView& vc, 
 
 hipError_t launch_window_step(const CacheView& kc, const CacheView& vc, const WindowView& w,
                               const uint16_t* k_new, const uint16_t* v_new, const int32_t* active,
-                              hipStream_t s) {
+                              hipStream_t s, float* kacc) {
   switch (kc.T) {
-    case 1: return window_step_T<1>(kc, vc, w, k_new, v_new, active, s);
-    case 2: return window_step_T<2>(kc, vc, w, k_new, v_new, active, s);
-    case 4: return window_step_T<4>(kc, vc, w, k_new, v_new, active, s);
+    case 1: return window_step_T<1>(kc, vc, w, k_new, v_new, active, s, kacc);
+    case 2: return window_step_T<2>(kc, vc, w, k_new, v_new, active, s, kacc);
+    case 4: return window_step_T<4>(kc, vc, w, k_new, v_new, active, s, kacc);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_window_key_weights(const WindowView& w, const uint16_t* q, int G, int T, float* kacc,
+                                     hipStream_t s) {
+  const dim3 grid((uint32_t)(w.B * w.H));
+  switch (T) {
+    case 1: hipLaunchKernelGGL(k_window_key_weights<1>, grid, dim3(256), 0, s, w, q, G, kacc); break;
+    case 2: hipLaunchKernelGGL(k_window_key_weights<2>, grid, dim3(256), 0, s, w, q, G, kacc); break;
+    case 4: hipLaunchKernelGGL(k_window_key_weights<4>, grid, dim3(256), 0, s, w, q, G, kacc); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace mf

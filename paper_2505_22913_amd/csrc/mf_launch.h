@@ -76,9 +76,14 @@ struct WindowView {
 hipError_t launch_window_fill(const WindowView& w, int b, int d, const uint16_t* xk,
                               const uint16_t* xv, int64_t x_stride, int first, int count,
                               hipStream_t s);
+// kacc: null for magnitude keys, else the window's output-aware key weights
+// [BH][W][64T] fp32 (the leaving key is pruned with its slot's weights).
 hipError_t launch_window_step(const CacheView& kc, const CacheView& vc, const WindowView& w,
                               const uint16_t* k_new, const uint16_t* v_new, const int32_t* active,
-                              hipStream_t s);
+                              hipStream_t s, float* kacc = nullptr);
+// kacc[bh][slot] += |q| of the G query heads of bh, for the newest 32 window tokens.
+hipError_t launch_window_key_weights(const WindowView& w, const uint16_t* q, int G, int T, float* kacc,
+                                     hipStream_t s);
 // Grouped lifecycle step (see mustafar_window_step_grouped): kc per token, vc
 // per channel; acc: fp32 [B][H][W] scores or NULL (magnitude).
 hipError_t launch_window_step_grouped(const CacheView& kc, const CacheView& vc, const WindowView& w,

@@ -290,6 +290,23 @@ def test_window_calls_reject_before_launch(lib):
     assert att(B=3) == mf.EINVAL
     assert att(Hq=12) == mf.EUNSUPPORTED
     assert att(ws_bytes=anb - 4) == mf.EWORKSPACE
+    # Output-aware keys in the window.
+    kacc = 0x4000000
+    wstep = lambda **kw: lib.mustafar_window_step_weighted(  # noqa: E731
+        ctypes.byref(kw.get("w", w)), ctypes.byref(K), ctypes.byref(V), kn, vn, act,
+        kw.get("kacc", kacc), None)
+    assert wstep(kacc=kacc + 8) == mf.EINVAL         # misaligned weights
+    assert wstep(kacc=None) == mf.EINVAL
+    w16, _ = _fake_window(W=16)
+    assert wstep(w=w16) == mf.EINVAL                 # a key must see 32 steps in the window
+    kw_ = lambda **kw: lib.mustafar_window_key_weights(  # noqa: E731
+        kw.get("q", 0x700000), kw.get("B", 2), kw.get("Hq", 8), ctypes.byref(w), kw.get("kacc", kacc),
+        None)
+    assert kw_(B=3) == mf.EINVAL
+    assert kw_(Hq=6) == mf.EINVAL                    # not a multiple of H
+    assert kw_(Hq=64) == mf.EUNSUPPORTED             # 16 query heads per kv-head
+    assert kw_(q=0x700002) == mf.EINVAL
+    assert kw_(kacc=kacc + 4) == mf.EINVAL
 
 
 def test_prune_variants_reject_before_launch(lib):

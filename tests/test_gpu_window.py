@@ -10,7 +10,8 @@ entries' compressed and window lengths differ throughout. At checkpoints:
 * every stream's compressed format equals the oracle's one-shot compression of
   the entry's tokens before its window, bit for bit (Sec. 3; the incremental
   graduation must reproduce it exactly);
-* the attention output of every entry is within 2e-3 of the oracle's Algorithm 1.
+* the attention output of every entry is within 2e-3 of the oracle's Algorithm 1;
+* with output-aware keys, the window's key weights equal the oracle's bit for bit.
 """
 import numpy as np
 import pytest
@@ -126,3 +127,55 @@ def test_window_step_without_mask_and_long_prefill_splits():
     err = max(attn_error(out[b], o.attention(q.cpu().numpy()[b], b)) for b in range(B))
     announce(f"window long prefill: attention error {err:.2e}")
     assert err <= ATTN_TOL
+
+
+@pytest.mark.parametrize("W,G", [(32, 1), (48, 4)])
+def test_window_lifecycle_output_aware_keys(W, G):
+    """The lifecycle with output-aware keys (Sec. 2): mustafar_window_key_weights
+    after every step's attention, mustafar_window_step_weighted for the step. The
+    key weights of every window slot equal the oracle's, bit for bit (fp32 adds in
+    the same order), and so do the caches; attention within the tolerance."""
+    import torch
+    announce(f"window lifecycle output-aware keys W={W} G={G}")
+    rng = np.random.default_rng(300 + W + G)
+    B, H, d = 3, 2, 128
+    seq = [1, 20, W + 30]
+    n_max = max(seq)
+    steps = W + 50
+    xk = rng.standard_normal((B, H, n_max, d)).astype(np.float16)
+    xv = rng.standard_normal((B, H, n_max, d)).astype(np.float16)
+    cap = n_max + steps
+    Kc = mf.CompressedCache(B, H, d, 0.5, cap)
+    Vc = mf.CompressedCache(B, H, d, 0.7, cap)
+    win = mf.DenseWindow(B, H, d, W)
+    kacc = torch.zeros((B, H, W, d), dtype=torch.float32, device="cuda")
+    mf.mustafar_window_prefill(win, Kc, Vc, torch.from_numpy(xk).cuda(), torch.from_numpy(xv).cuda(),
+                               seq)
+    o = WindowOracle(B, H, d, W, 0.5, 0.7, output_aware_keys=True)
+    o.prefill(xk, xv, seq)
+    graduated = 0
+    for s in range(steps):
+        act = np.array([1, (s % 4) != 2, 1], dtype=np.int32)
+        kn = rng.standard_normal((B, H, d)).astype(np.float16)
+        vn = rng.standard_normal((B, H, d)).astype(np.float16)
+        mf.mustafar_window_step_weighted(win, Kc, Vc, torch.from_numpy(kn).cuda(),
+                                         torch.from_numpy(vn).cuda(), kacc,
+                                         torch.from_numpy(act).cuda())
+        o.step(kn, vn, act)
+        q = torch.from_numpy(rng.standard_normal((B, H * G, d)).astype(np.float16)).cuda()
+        if s % 10 == 9 or s == steps - 1:
+            _check_state(o, win, Kc, Vc, B, H, W)
+            _check_attention(o, win, Kc, Vc, q, B, G, f"output-aware keys W={W} G={G} step {s + 1}")
+        mf.mustafar_window_key_weights(q, win, kacc)
+        o.accumulate_key_weights(q.cpu().numpy())
+        if s % 10 == 9 or s == steps - 1:
+            torch.cuda.synchronize()
+            a = kacc.cpu().numpy()
+            lens, heads = win.len.cpu().numpy(), win.head.cpu().numpy()
+            for b in range(B):
+                n = o.n_comp(b)
+                for p in range(int(lens[b])):
+                    slot = (int(heads[b]) + p) % W
+                    assert np.array_equal(a[b, :, slot], o.key_weights(b, n + p)), (s, b, p)
+            graduated = sum(o.n_comp(b) - o.n_prefill[b] for b in range(B))
+    assert graduated >= 40

@@ -100,6 +100,79 @@ def test_attention_equals_the_direct_computation(G):
         np.testing.assert_allclose(a, r, rtol=0, atol=1e-12)
 
 
+# ---- output-aware keys in the lifecycle (Sec. 2) -------------------------------------------
+def _output_aware_run(W, S, G, inactive=()):
+    rng = np.random.default_rng(40 + W + G)
+    B, H, d = 1, 2, 64
+    o = WindowOracle(B, H, d, W, 0.5, 0.5, output_aware_keys=True)
+    x0 = rng.standard_normal((B, H, 1, d)).astype(np.float16)
+    o.prefill(x0, x0, [1])
+    keys, qs = [x0[0, :, 0]], []
+    for s in range(S):
+        k = rng.standard_normal((B, H, d)).astype(np.float16)
+        act = [0 if s in inactive else 1]
+        o.step(k, rng.standard_normal((B, H, d)).astype(np.float16), act)
+        if act[0]:
+            keys.append(k[0])
+        q = rng.standard_normal((B, H * G, d)).astype(np.float16)
+        o.accumulate_key_weights(q)
+        qs.append(q[0])
+    return o, np.stack(keys, axis=1)[None], np.stack(qs, axis=1)[None]
+
+
+@pytest.mark.parametrize("W,G", [(32, 1), (48, 2)])
+def test_output_aware_key_weights_equal_the_bulk_lookahead(W, G):
+    """A continuously active entry whose prompt is one token: key j >= 1 arrives in
+    step j - 1 and leaves with the lookahead weights of the queries of steps
+    j - 1 .. j + 30 (query_lookahead with L = 32, bit for bit); the prompt token
+    missed its own (prefill) query and carries those of steps 0 .. 30. The
+    compressed keys equal compress_variant's output-aware compression with those
+    weights, bit for bit."""
+    S = 90
+    o, K, Q = _output_aware_run(W, S, G)
+    H, d = 2, 64
+    look = oracle.query_lookahead(Q, H, 32)
+    n = o.n_comp(0)
+    assert n == S + 1 - W
+    want_w = np.stack([oracle.query_lookahead(Q, H, 31)[0, :, 0]] +
+                      [look[0, :, j - 1] for j in range(1, n)], axis=1)       # [H][n][d]
+    for j in range(n):
+        assert np.array_equal(o.key_weights(0, j), want_w[:, j]), j
+    want = oracle.compress_variant(K[:, :, :n], "output_aware", k=oracle.keep_count(d, 0.5),
+                                   weights=want_w[None])
+    got, _ = o.compressed(0)
+    for key in ("bitmaps", "offsets", "stream_len"):
+        assert np.array_equal(got[key], want[key]), key
+    L = int(want["stream_len"][0, 0])
+    assert np.array_equal(got["values"][:, :, :L], want["values"][:, :, :L])
+    # and the weights matter: some key differs from its magnitude pruning
+    mag = oracle.compress(K[:, :, :n], 0.5)
+    assert not np.array_equal(got["bitmaps"], mag["bitmaps"])
+
+
+def test_output_aware_keys_of_a_paused_entry_gather_every_query():
+    """While an entry receives no tokens its newest window tokens keep adding the
+    queries of every step: a token's weights are the sum over the steps in which it
+    was among the newest 32 window tokens."""
+    W, S, G = 32, 60, 1
+    pause = set(range(10, 15))
+    o, K, Q = _output_aware_run(W, S, G, inactive=pause)
+    # token j arrived in step a_j; it stays among the newest 32 until 32 newer
+    # tokens have arrived
+    arrive = [-1]
+    for s in range(S):
+        if s not in pause:
+            arrive.append(s)
+    qa = np.abs(Q[0].astype(np.float32))        # [Hq][S][d]
+    for j in range(o.n_comp(0)):
+        first = max(arrive[j], 0)
+        last = arrive[j + 32] if j + 32 < len(arrive) else S    # the step the 32nd newer token came
+        w = np.zeros((2, 64), dtype=np.float32)
+        for s in range(first, last):
+            w = w + qa[:, s]
+        assert np.array_equal(o.key_weights(0, j), w), j
+
+
 # ---- the grouped lifecycle (per-channel value pruning in groups of 32) -------------------
 from oracle.window import GroupedWindowOracle  # noqa: E402
 
