@@ -150,6 +150,36 @@ def test_output_aware_key_weights_equal_the_bulk_lookahead(W, G):
     assert not np.array_equal(got["bitmaps"], mag["bitmaps"])
 
 
+def test_output_aware_key_pins_reject_planted_mistakes(monkeypatch):
+    """The lookahead pin fails when the window oracle gathers one step too few or
+    adds the query heads of a step in the other order."""
+    import oracle.window as ow
+
+    def weights_match(W=32, G=2):
+        o, K, Q = _output_aware_run(W, 90, G)
+        look = oracle.query_lookahead(Q, 2, 32)
+        return all(np.array_equal(o.key_weights(0, j), look[0, :, j - 1]) for j in range(1, o.n_comp(0)))
+
+    assert weights_match()
+    monkeypatch.setattr(ow, "KEY_WEIGHT_STEPS", 31)
+    assert not weights_match()
+    monkeypatch.undo()
+
+    def reversed_heads(self, q):
+        qa = np.abs(np.asarray(q).view(np.float16).astype(np.float32))
+        G = qa.shape[1] // self.H
+        for b in range(self.B):
+            n, L = self.n_comp(b), self.window_len(b)
+            for p in range(max(0, L - ow.KEY_WEIGHT_STEPS), L):
+                w = self.key_w[b].setdefault(n + p, np.zeros((self.H, self.d), dtype=np.float32))
+                for h in range(self.H):
+                    for g in reversed(range(G)):
+                        w[h] = w[h] + qa[b, h * G + g]
+
+    monkeypatch.setattr(ow.WindowOracle, "accumulate_key_weights", reversed_heads)
+    assert not weights_match()
+
+
 def test_output_aware_keys_of_a_paused_entry_gather_every_query():
     """While an entry receives no tokens its newest window tokens keep adding the
     queries of every step: a token's weights are the sum over the steps in which it
