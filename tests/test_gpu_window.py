@@ -129,16 +129,16 @@ def test_window_step_without_mask_and_long_prefill_splits():
     assert err <= ATTN_TOL
 
 
-@pytest.mark.parametrize("W,G", [(32, 1), (48, 4)])
-def test_window_lifecycle_output_aware_keys(W, G):
+@pytest.mark.parametrize("W,G,d", [(32, 1, 128), (48, 4, 128), (40, 2, 64), (32, 8, 256)])
+def test_window_lifecycle_output_aware_keys(W, G, d):
     """The lifecycle with output-aware keys (Sec. 2): mustafar_window_key_weights
     after every step's attention, mustafar_window_step_weighted for the step. The
     key weights of every window slot equal the oracle's, bit for bit (fp32 adds in
     the same order), and so do the caches; attention within the tolerance."""
     import torch
-    announce(f"window lifecycle output-aware keys W={W} G={G}")
-    rng = np.random.default_rng(300 + W + G)
-    B, H, d = 3, 2, 128
+    announce(f"window lifecycle output-aware keys W={W} G={G} d={d}")
+    rng = np.random.default_rng(300 + W + G + d)
+    B, H = 3, 2
     seq = [1, 20, W + 30]
     n_max = max(seq)
     steps = W + 50
