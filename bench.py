@@ -36,8 +36,10 @@ HBM_PEAK_GBS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    # Long enough for the GPU clocks to settle under this load (the first few
+    # dozen calls after an idle period run slower); no idle gap follows it.
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--workload", default="mha-b16-32k")
     ap.add_argument("--splits", type=int, default=0, help="split-K segments (0: library default)")
     ap.add_argument("--seed", type=int, default=4)
@@ -311,11 +313,11 @@ def main():
     # ---- dense baseline over the same tokens ----
     ws_d = torch.empty(mf.mustafar_attn_workspace_bytes(w.B, w.Hq, w.Hkv, w.d, w.N + w.n_tail,
                                                         args.splits), dtype=torch.uint8, device=dev)
-    for _ in range(3):
+    a, b = ev(), ev()
+    n_dense_reps = 20
+    for _ in range(20):
         mf.mustafar_dense_decode_attn(q, K, V, out=out, n_splits=args.splits, ws=ws_d)
     torch.cuda.synchronize()
-    a, b = ev(), ev()
-    n_dense_reps = 10
     a.record()
     for _ in range(n_dense_reps):
         mf.mustafar_dense_decode_attn(q, K, V, out=out, n_splits=args.splits, ws=ws_d)
@@ -334,13 +336,12 @@ def main():
         if marks is not None:
             marks[1].record()
 
+    marks = [(ev(), ev()) for _ in range(steps)]
+    t_start, t_end = ev(), ev()
     for _ in range(warm):
         step()
     torch.cuda.synchronize()
     n_s_start = Kc.n_tokens
-    marks = [(ev(), ev()) for _ in range(steps)]
-    t_start, t_end = ev(), ev()
-    torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t_start.record()
     for i in range(steps):
@@ -387,11 +388,11 @@ def main():
             if marks is not None:
                 marks[1].record()
 
+        wmarks = [(ev(), ev()) for _ in range(steps)]
+        a, b = ev(), ev()
         for _ in range(warm):
             wstep()
         torch.cuda.synchronize()
-        wmarks = [(ev(), ev()) for _ in range(steps)]
-        a, b = ev(), ev()
         a.record()
         for i in range(steps):
             wstep(wmarks[i])
@@ -423,11 +424,11 @@ def main():
             if marks is not None:
                 marks[1].record()
 
+        kmarks = [(ev(), ev()) for _ in range(steps)]
+        a, b = ev(), ev()
         for _ in range(warm):
             kstep()
         torch.cuda.synchronize()
-        kmarks = [(ev(), ev()) for _ in range(steps)]
-        a, b = ev(), ev()
         a.record()
         for i in range(steps):
             kstep(kmarks[i])

@@ -130,7 +130,7 @@ struct AttnShape {
 // workgroups (many segments, few query heads): the number of first-level parts
 // of 32 segments, or 1 for a single-level merge.
 inline int merge_parts(int64_t n_seg, int64_t BHq) {
-  return (n_seg > 64 && BHq < 256) ? (int)((n_seg + 31) / 32) : 1;
+  return (n_seg > 128 && BHq < 256) ? (int)((n_seg + 31) / 32) : 1;
 }
 
 // Partial results of every segment into ws_ml [n_seg][BHq] (max, sum) and
