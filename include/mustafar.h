@@ -74,7 +74,9 @@ typedef struct mustafar_ccache {
     uint32_t* stream_len; /* [B*H], 4-byte aligned                              */
     int32_t B, H, d;      /* batch, kv-heads, head dimension (64, 128 or 256)   */
     int32_t n_keep;       /* channels kept per token                            */
-    int32_t cap_tokens;   /* tokens each stream can hold                        */
+    int32_t cap_tokens;   /* tokens each stream can hold (a multiple of 64 keeps
+                             each stream's bitmaps and offsets line-aligned,
+                             which the attention reads block by block)      */
     int32_t n_tokens;     /* tokens compressed so far (same for every stream)   */
     int64_t val_stride;   /* fp16 elements reserved per stream, multiple of 8   */
     int32_t group_keep;   /* -1: per-token cache (n_keep channels per token);   */

@@ -219,12 +219,18 @@ class CompressedCache:
 
     bitmaps u64 [B][H][cap][d/64], offsets u32 [B][H][cap][d/64],
     values fp16 bits [B][H][val_stride], stream_len u32 [B][H].
+
+    The capacity is rounded up to a multiple of ``align`` tokens (64 by default),
+    so that every stream's bitmaps and offsets start on a 256-byte boundary: the
+    attention kernels read them in 32-token blocks, and a block that straddles
+    an extra 128-byte line costs 5% more traffic.
     """
 
     def __init__(self, B: int, H: int, d: int, sparsity: float, cap_tokens: int, device="cuda",
-                 grouped: bool = False):
+                 grouped: bool = False, align: int = 64):
         import torch
         T = d // TILE
+        cap_tokens = (int(cap_tokens) + align - 1) // align * align
         if grouped:   # per-channel pruning in groups of 32 tokens
             stride = lib().mustafar_grouped_stream_capacity(d, mustafar_keep_count(GROUP, sparsity),
                                                             cap_tokens)

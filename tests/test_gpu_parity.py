@@ -104,7 +104,7 @@ def test_append_into_empty_cache_and_capacity_error():
     announce("append empty + capacity")
     B, H, d = 1, 2, 64
     K, _ = synth.make_kv(B, H, 3, d, seed=8)
-    cache = mf.CompressedCache(B, H, d, 0.5, 3)
+    cache = mf.CompressedCache(B, H, d, 0.5, 3, align=1)
     for j in range(3):
         mf.mustafar_append(cache, to_dev(np.ascontiguousarray(K[:, :, j])))
     compare_format(read_cache(cache), oracle.compress(K, 0.5), 3, all_pairs(B, H))
