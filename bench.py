@@ -328,8 +328,7 @@ def main():
 
     # ---- decode steps: append (prune+compress one token per stream) + attention ----
     def step(marks=None):
-        mf.mustafar_append(Kc, new_k)
-        mf.mustafar_append(Vc, new_v)
+        mf.mustafar_append_kv(Kc, Vc, new_k, new_v)
         if marks is not None:
             marks[0].record()
         mf.mustafar_sparse_decode_attn(q, Kc, Vc, KL, VL, out=out, n_splits=args.splits, ws=ws_a)

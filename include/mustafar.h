@@ -155,6 +155,13 @@ int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void
  * one mustafar_prune_compress call. */
 int mustafar_append(mustafar_ccache_t* c, const void* x_new, void* stream);
 
+/* mustafar_append of a decode step's key (into Kc) and value (into Vc) in one
+ * launch. The caches must have the same B, H, d and n_tokens (their
+ * sparsities may differ). Errors: EINVAL (descriptors, shapes, alignment,
+ * per-channel caches), ECAPACITY; on any error neither cache changes. */
+int mustafar_append_kv(mustafar_ccache_t* Kc, mustafar_ccache_t* Vc, const void* k_new,
+                       const void* v_new, void* stream);
+
 /* PRUNER VARIANTS in the same compressed format (the decode attention reads
  * any bitmaps):
  *   MUSTAFAR_PRUNE_MAGNITUDE     per-token magnitude top-k (the default above),

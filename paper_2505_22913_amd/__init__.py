@@ -77,6 +77,8 @@ _SIGS = {
     "mustafar_prune_compress": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
                                                ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t,
                                                ctypes.c_void_p]),
+    "mustafar_append_kv": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.POINTER(ccache_t),
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "mustafar_append": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
                                        ctypes.c_void_p]),
     "mustafar_attn_default_splits": (ctypes.c_int, [ctypes.c_int] * 5),
@@ -275,6 +277,12 @@ def mustafar_prune_compress(cache: CompressedCache, x, ws=None, stream=None) -> 
     _check("mustafar_prune_compress", lib().mustafar_prune_compress(
         ctypes.byref(cache.desc), _dptr(x), n_new, _dptr(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
+
+
+def mustafar_append_kv(Kc: CompressedCache, Vc: CompressedCache, k_new, v_new, stream=None) -> None:
+    """Append one decode step's key and value per stream, [B][H][d] fp16 each, in one launch."""
+    _check("mustafar_append_kv", lib().mustafar_append_kv(ctypes.byref(Kc.desc), ctypes.byref(Vc.desc),
+                                                          _dptr(k_new), _dptr(v_new), _stream(stream)))
 
 
 def mustafar_append(cache: CompressedCache, x_new, stream=None) -> None:

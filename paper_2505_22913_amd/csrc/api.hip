@@ -294,6 +294,23 @@ int mustafar_append(mustafar_ccache_t* c, const void* x_new, void* stream) {
   return st;
 }
 
+int mustafar_append_kv(mustafar_ccache_t* Kc, mustafar_ccache_t* Vc, const void* k_new,
+                       const void* v_new, void* stream) {
+  int st;
+  if ((st = check_cache(Kc)) != MUSTAFAR_OK || (st = check_cache(Vc)) != MUSTAFAR_OK) return st;
+  if (Kc->B != Vc->B || Kc->H != Vc->H || Kc->d != Vc->d || Kc->n_tokens != Vc->n_tokens)
+    return MUSTAFAR_EINVAL;
+  if (!aligned(k_new, 16) || !aligned(v_new, 16) || grouped(Kc) || grouped(Vc)) return MUSTAFAR_EINVAL;
+  if (Kc->n_tokens + 1 > Kc->cap_tokens || Vc->n_tokens + 1 > Vc->cap_tokens) return MUSTAFAR_ECAPACITY;
+  st = status_of(mf::launch_append_kv(view_of(Kc), view_of(Vc), (const uint16_t*)k_new,
+                                      (const uint16_t*)v_new, Kc->n_tokens, (hipStream_t)stream));
+  if (st == MUSTAFAR_OK) {
+    Kc->n_tokens += 1;
+    Vc->n_tokens += 1;
+  }
+  return st;
+}
+
 int mustafar_prune_compress_ex(mustafar_ccache_t* c, const void* x, int n_new,
                                const mustafar_prune_opts_t* opts, void* ws, size_t ws_bytes,
                                void* stream) {

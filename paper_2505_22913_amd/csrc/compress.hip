@@ -770,6 +770,18 @@ __global__ __launch_bounds__(256) void k_append(CacheView c, const uint16_t* __r
   append_one<T>(c, bh, tok0, x + (int64_t)bh * kTile * T, lane_id());
 }
 
+// The keys and values of one decode step in one launch: waves 0 .. BH-1 append
+// to kc, the next BH to vc (the caches have the same shape and token count).
+template <int T>
+__global__ __launch_bounds__(256) void k_append_kv(CacheView kc, CacheView vc, const uint16_t* __restrict__ k,
+                                                   const uint16_t* __restrict__ v, int tok0) {
+  const int i = blockIdx.x * (256 / kWave) + threadIdx.x / kWave;
+  if (i >= 2 * kc.BH) return;
+  const bool is_v = i >= kc.BH;
+  const int bh = is_v ? i - kc.BH : i;
+  append_one<T>(is_v ? vc : kc, bh, tok0, (is_v ? v : k) + (int64_t)bh * kTile * T, lane_id());
+}
+
 // append_one with output-aware selection: w the token's fp32 channel weights.
 template <int T>
 __device__ __forceinline__ void append_one_weighted(const CacheView& c, int bh, int tok,
@@ -1094,6 +1106,18 @@ hipError_t launch_append(const CacheView& c, const uint16_t* x, int tok0, hipStr
     case 4: return append_T<4>(c, x, tok0, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_append_kv(const CacheView& kc, const CacheView& vc, const uint16_t* k, const uint16_t* v,
+                            int tok0, hipStream_t s) {
+  const dim3 grid((2 * kc.BH + 3) / 4);
+  switch (kc.T) {
+    case 1: hipLaunchKernelGGL(k_append_kv<1>, grid, dim3(256), 0, s, kc, vc, k, v, tok0); break;
+    case 2: hipLaunchKernelGGL(k_append_kv<2>, grid, dim3(256), 0, s, kc, vc, k, v, tok0); break;
+    case 4: hipLaunchKernelGGL(k_append_kv<4>, grid, dim3(256), 0, s, kc, vc, k, v, tok0); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 // Offsets and packing of tokens whose bitmaps are already in the cache.

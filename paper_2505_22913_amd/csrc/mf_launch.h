@@ -33,6 +33,9 @@ hipError_t launch_compress(const CacheView& c, const uint16_t* x, int n_new, int
                            hipStream_t s, int64_t x_stride = 0);
 // Compress one token per stream (x: [BH][64T]) as token tok0.
 hipError_t launch_append(const CacheView& c, const uint16_t* x, int tok0, hipStream_t s);
+// launch_append of the keys and the values of one step in one launch (same shapes).
+hipError_t launch_append_kv(const CacheView& kc, const CacheView& vc, const uint16_t* k, const uint16_t* v,
+                            int tok0, hipStream_t s);
 
 // Pruner variants of the same format (the magnitude top-k of k_compress is the
 // default): per-head kept counts, 2:4 per token, output-aware key scores.

@@ -142,6 +142,23 @@ def test_compress_and_append_reject_before_launch(lib):
     assert c.n_tokens == 101                                             # nothing changed
 
 
+def test_append_kv_rejects_before_launch(lib):
+    K, _ = _fake_cache(B=2, H=4, cap=10)
+    V, _ = _fake_cache(B=2, H=4, s=0.7, cap=10)
+    kn, vn = 0xf00000, 0xf10000
+    call = lambda **kw: lib.mustafar_append_kv(  # noqa: E731
+        ctypes.byref(kw.get("K", K)), ctypes.byref(kw.get("V", V)), kw.get("kn", kn), kw.get("vn", vn), None)
+    assert call(kn=kn + 2) == mf.EINVAL
+    assert call(vn=None) == mf.EINVAL
+    V3, _ = _fake_cache(B=2, H=3, s=0.7, cap=10)
+    assert call(V=V3) == mf.EINVAL                   # shapes differ
+    V.n_tokens = 1
+    assert call() == mf.EINVAL                       # token counts differ
+    K.n_tokens = V.n_tokens = 10
+    assert call() == mf.ECAPACITY
+    assert K.n_tokens == 10 and V.n_tokens == 10
+
+
 def test_decode_attention_rejects_before_launch(lib):
     K, _ = _fake_cache(B=2, H=4)
     V, _ = _fake_cache(B=2, H=4, s=0.7)

@@ -100,6 +100,22 @@ def test_compress_in_pieces_and_append_equal_compress_all():
         compare_format(read_cache(cache), oracle.compress(K, s), n0 + n1 + n2, all_pairs(B, H))
 
 
+def test_append_kv_equals_the_oracle():
+    announce("append_kv")
+    B, H, d, n0, n1 = 2, 3, 128, 70, 9
+    K, V = synth.make_kv(B, H, n0 + n1, d, seed=12)
+    Kc = mf.CompressedCache(B, H, d, 0.5, n0 + n1)
+    Vc = mf.CompressedCache(B, H, d, 0.7, n0 + n1)
+    mf.mustafar_prune_compress(Kc, to_dev(np.ascontiguousarray(K[:, :, :n0])))
+    mf.mustafar_prune_compress(Vc, to_dev(np.ascontiguousarray(V[:, :, :n0])))
+    for j in range(n0, n0 + n1):
+        mf.mustafar_append_kv(Kc, Vc, to_dev(np.ascontiguousarray(K[:, :, j])),
+                              to_dev(np.ascontiguousarray(V[:, :, j])))
+    assert Kc.n_tokens == Vc.n_tokens == n0 + n1
+    compare_format(read_cache(Kc), oracle.compress(K, 0.5), n0 + n1, all_pairs(B, H))
+    compare_format(read_cache(Vc), oracle.compress(V, 0.7), n0 + n1, all_pairs(B, H))
+
+
 def test_append_into_empty_cache_and_capacity_error():
     announce("append empty + capacity")
     B, H, d = 1, 2, 64
