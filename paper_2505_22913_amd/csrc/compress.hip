@@ -311,11 +311,13 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
   constexpr int NW = NR / 16;
   uint32_t keep[NW];
   if constexpr (PRESET) {
+    // (a wave whose run lies past the chunk's end reads nothing: its tokens
+    // are past n_new, possibly past the cache's capacity)
     const int jt = min((int)lane / LPT, max(nt, 1) - 1);
     const int64_t tb = ((int64_t)bh * cap_tokens + tok0 + j0 + jt) * T + ((int)lane % LPT) * (T / LPT);
 #pragma unroll
     for (int t = 0; t < NW / 2; ++t) {
-      const uint64_t bm = bitmaps[tb + t];
+      const uint64_t bm = nt > 0 ? bitmaps[tb + t] : 0ull;
       keep[2 * t] = (uint32_t)bm;
       keep[2 * t + 1] = (uint32_t)(bm >> 32);
     }
