@@ -530,6 +530,12 @@ def main():
         "prune_variants": variants,
         "channel_pruning": channel,
         "compression_ratio": comp_kv / dense_kv,
+        "paper_reference": {
+            "hardware": "NVIDIA RTX 6000 Ada (Sec. 4.3), against cuBLAS dense batched MV",
+            "workload": "Llama-2-7B MHA, 2048 input + 1024 generated tokens",
+            "speedup_vs_dense_k50_v50": 1 / 0.8107, "speedup_vs_dense_k70_v70": 1 / 0.6187,
+            "compression_ratio_k50_v50": 0.65, "compression_ratio_k70_v70": 0.45,
+            "note": "context only: other hardware, other dense baseline, no absolute throughput given"},
         "wall_s_timed": wall,
     }
     if not args.no_cpu_baseline:
