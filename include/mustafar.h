@@ -156,9 +156,10 @@ int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void
 int mustafar_append(mustafar_ccache_t* c, const void* x_new, void* stream);
 
 /* mustafar_append of a decode step's key (into Kc) and value (into Vc) in one
- * launch. The caches must have the same B, H, d and n_tokens (their
- * sparsities may differ). Errors: EINVAL (descriptors, shapes, alignment,
- * per-channel caches), ECAPACITY; on any error neither cache changes. */
+ * launch. The caches must be two different caches with the same B, H, d and
+ * n_tokens (their sparsities may differ). Errors: EINVAL (descriptors, one
+ * cache twice, shapes, alignment, per-channel caches), ECAPACITY; on any
+ * error neither cache changes. */
 int mustafar_append_kv(mustafar_ccache_t* Kc, mustafar_ccache_t* Vc, const void* k_new,
                        const void* v_new, void* stream);
 

@@ -298,6 +298,7 @@ int mustafar_append_kv(mustafar_ccache_t* Kc, mustafar_ccache_t* Vc, const void*
                        const void* v_new, void* stream) {
   int st;
   if ((st = check_cache(Kc)) != MUSTAFAR_OK || (st = check_cache(Vc)) != MUSTAFAR_OK) return st;
+  if (Kc == Vc) return MUSTAFAR_EINVAL;
   if (Kc->B != Vc->B || Kc->H != Vc->H || Kc->d != Vc->d || Kc->n_tokens != Vc->n_tokens)
     return MUSTAFAR_EINVAL;
   if (!aligned(k_new, 16) || !aligned(v_new, 16) || grouped(Kc) || grouped(Vc)) return MUSTAFAR_EINVAL;

@@ -150,6 +150,7 @@ def test_append_kv_rejects_before_launch(lib):
         ctypes.byref(kw.get("K", K)), ctypes.byref(kw.get("V", V)), kw.get("kn", kn), kw.get("vn", vn), None)
     assert call(kn=kn + 2) == mf.EINVAL
     assert call(vn=None) == mf.EINVAL
+    assert call(V=K) == mf.EINVAL                    # the same cache twice
     V3, _ = _fake_cache(B=2, H=3, s=0.7, cap=10)
     assert call(V=V3) == mf.EINVAL                   # shapes differ
     V.n_tokens = 1
