@@ -92,8 +92,11 @@ def measured_traffic(kernel: str, workload: str, key: str = "bytes_per_launch"):
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    src = open(os.path.join(ROOT, rec["source"]), "rb").read()
-    if hashlib.sha256(src).hexdigest()[:16] != rec["source_sha256_prefix"]:
+    # the kernel's source and every file it includes, hashed in the listed order
+    h = hashlib.sha256()
+    for rel in rec.get("sources", [rec.get("source")]):
+        h.update(open(os.path.join(ROOT, rel), "rb").read())
+    if h.hexdigest()[:16] != rec["source_sha256_prefix"]:
         return None
     return rec.get(key)
 
