@@ -153,6 +153,8 @@ def test_append_kv_rejects_before_launch(lib):
     assert call(V=K) == mf.EINVAL                    # the same cache twice
     V3, _ = _fake_cache(B=2, H=3, s=0.7, cap=10)
     assert call(V=V3) == mf.EINVAL                   # shapes differ
+    Vg, _ = _fake_grouped(B=2, H=4, cap=64)
+    assert call(V=Vg) == mf.EINVAL                   # per-channel groups take no single token
     V.n_tokens = 1
     assert call() == mf.EINVAL                       # token counts differ
     K.n_tokens = V.n_tokens = 10
