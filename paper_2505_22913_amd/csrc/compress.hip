@@ -269,7 +269,6 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
   constexpr int P16 = d / 8;                // 16-byte pieces per row
   __shared__ __align__(16) unsigned char s_rows_all[kCompressWaves][TPW * ROW];  // dense rows
   __shared__ uint32_t s_share[kCompressWaves + 2];  // ticket, the waves' run lengths, the chunk's base
-  extern __shared__ __align__(16) unsigned char s_out[];     // the packed run, then a trash slot
 
   const uint32_t lane = lane_id();
   const int wave = (int)(threadIdx.x / kWave);
@@ -410,43 +409,40 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
     wave_off = w == wave ? run : wave_off;
     run += s_share[1 + w];
   }
-  const uint32_t lane_off = incl - lane_len + wave_off;
+  const uint32_t lane_off = incl - lane_len;  // in the wave's run
   const uint32_t first = (chunk == 0 && tok0 > 0) ? stream_len[bh] : 0u;
   if (wave == 0) publish_total(flags + (int64_t)bh * n_chunks, chunk, run, first, lane);
 
-  // Packing, lane = its tiles: the lane walks the set bits of each tile's mask
-  // in channel order (lower half, then upper half), reads the kept values from
-  // its row and writes them to the chunk's packed run, value r of a tile at
-  // r; the tile's last group of 8 is zeroed first, so its pad slots hold +0.0.
-  // The trip counts are the wave's busiest lane; a lane whose bits are used up
-  // (x - 1 borrows) writes to the trash slot instead.
+  // Packing, lane = its tiles: the lane reloads its row into registers, then
+  // writes the kept values of each tile in channel order, value r of a tile
+  // at r, over the wave's own rows (a wave's LDS operations run in program
+  // order, so every row is read before the first write). The run is at most
+  // d values per token, so it ends before the last row's pad, the trash slot
+  // of the dropped channels. The tile's last group of 8 is zeroed first, so
+  // its pad slots hold +0.0.
   {
-    const uint32_t out_lds = (uint32_t)(uintptr_t)s_out;
-    const uint32_t trash = out_lds + 2u * run;
+    const uint32_t trash = base_lds + (uint32_t)(TPW * ROW - 16);
     const bool live = (int)lane < nt * LPT;
     const uint32_t row = base_lds + (uint32_t)(min((int)lane / LPT, max(nt, 1) - 1) * ROW + ((int)lane % LPT) * CPL * 2);
+    uint32_t v[NR];
+#pragma unroll
+    for (int i = 0; i < NR / 4; ++i) {
+      const u32x4_t w = lds_ld<u32x4_t>(row + 16u * (uint32_t)i);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[4 * i + e] = w[e];
+    }
 #pragma unroll
     for (int t = 0; t < TPL; ++t) {
       const uint32_t lo = live ? keep[2 * t] : 0u, hi = live ? keep[2 * t + 1] : 0u;
-      const uint32_t nlo = (uint32_t)__popc(lo), cnt = nlo + (uint32_t)__popc(hi);
-      const uint32_t out = out_lds + 2u * (lane_off + tile_pos[t]);
-      if (cnt & 7u) lds_st<u32x4_t>(out + 16u * (cnt / 8u), (u32x4_t){0u, 0u, 0u, 0u});
+      const uint32_t cnt = (uint32_t)(__popc(lo) + __popc(hi));
+      uint32_t pos = base_lds + 2u * (lane_off + tile_pos[t]);
+      if (cnt & 7u) lds_st<u32x4_t>(pos + 16u * (cnt / 8u), (u32x4_t){0u, 0u, 0u, 0u});
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        uint32_t x = h == 0 ? lo : hi;
-        const uint32_t dst = out + (h == 0 ? 0u : 2u * nlo);
-        const uint32_t src = row + (uint32_t)(kTile * t + 32 * h) * 2u;
-        const int n8 = (wave_max_int((int)__popc(x)) + 7) >> 3;
-        for (int g = 0; g < n8; ++g) {
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            const uint32_t f = ffbl_u32(x);
-            const bool used_up = x == 0u;
-            x &= x - 1u;
-            const uint16_t v = lds_ld<uint16_t>(src + 2u * (f & 31u));
-            lds_st<uint16_t>(used_up ? trash : dst + 16u * (uint32_t)g + 2u * (uint32_t)u, v);
-          }
-        }
+      for (int c = 0; c < kTile; ++c) {
+        const uint32_t bit = ((c < 32 ? lo : hi) >> (c & 31)) & 1u;
+        const uint32_t pair = v[(kTile / 2) * t + c / 2];
+        lds_st<uint16_t>(bit ? pos : trash, (uint16_t)(c & 1 ? pair >> 16 : pair));
+        pos += bit << 1;
       }
     }
   }
@@ -456,15 +452,17 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
     if (lane == 0) s_share[kCompressWaves + 1] = b;
     if (lane == 0 && chunk == n_chunks - 1) stream_len[bh] = b == kBadBase ? kBadBase : b + run;
   }
-  __syncthreads();  // the packed run of both waves and the chunk's base
+  __syncthreads();  // the chunk's base
   const uint32_t base = __builtin_amdgcn_readfirstlane((int)s_share[kCompressWaves + 1]);
   if (base == kBadBase) return;  // look-back gave up: nothing is written
 
-  // Packed run (a multiple of 8 values, 16-byte aligned in the stream).
+  // The wave's packed run (a multiple of 8 values, 16-byte aligned in the
+  // stream), after the runs of the waves before it.
   {
-    u32x4_t* dst = reinterpret_cast<u32x4_t*>(values + (int64_t)bh * val_stride + base);
-    for (uint32_t c = threadIdx.x; c < run / 8; c += kCompressWaves * kWave)
-      __builtin_nontemporal_store(*reinterpret_cast<const u32x4_t*>(s_out + 16 * c), &dst[c]);
+    u32x4_t* dst = reinterpret_cast<u32x4_t*>(values + (int64_t)bh * val_stride + base + wave_off);
+    const uint32_t n16 = (uint32_t)s_share[1 + wave] / 8u;
+    for (uint32_t c = lane; c < n16; c += kWave)
+      __builtin_nontemporal_store(lds_ld<u32x4_t>(base_lds + 16u * c), &dst[c]);
   }
   // Bitmaps and offsets of this lane's tiles (tile index = token * T + t).
   if ((int)lane < nt * LPT) {
@@ -472,7 +470,7 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
 #pragma unroll
     for (int t = 0; t < TPL; ++t) {
       if constexpr (!PRESET) bitmaps[tile0 + t] = (uint64_t)keep[2 * t] | ((uint64_t)keep[2 * t + 1] << 32);
-      offsets[tile0 + t] = base + lane_off + tile_pos[t];
+      offsets[tile0 + t] = base + wave_off + lane_off + tile_pos[t];
     }
   }
 }
@@ -1034,20 +1032,6 @@ __global__ __launch_bounds__(256) void k_window_fill(WindowView w, int b, int d,
   }
 }
 
-// Dynamic LDS of k_compress: the chunk's packed run (tokens of at most `tok`
-// values each) and a 16-byte trash slot.
-inline size_t packed_run_lds(int T, int tok) {
-  return (size_t)compress_chunk_tokens(T) * (size_t)tok * 2u + 16u;
-}
-
-// Worst-case fp16 elements of one token keeping k of d channels (every
-// non-empty tile padded to 8).
-inline int token_max_values(int d, int k) {
-  const int T = d / kTile, nonempty = k < T ? k : T;
-  const int m = (k + 7 * nonempty) / 8 * 8;
-  return m < d ? m : d;
-}
-
 template <int T>
 static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, int64_t x_stride,
                              int tok0, uint32_t* ws, hipStream_t s, const PruneOpts& o = PruneOpts{}) {
@@ -1061,7 +1045,7 @@ static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, i
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(k_compress<T>, dim3((uint32_t)n_wg), dim3(compress_waves<T>() * kWave),
-                     packed_run_lds(T, token_max_values(kTile * T, c.n_keep)), s, x, n_new, c.n_keep,
+                     0, s, x, n_new, c.n_keep,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
                      flags, ticket, n_chunks, x_stride, o);
   return hipGetLastError();
@@ -1135,7 +1119,7 @@ static hipError_t pack_preset_T(const CacheView& c, const uint16_t* x, int n_new
   const int clear_blocks = (int)((words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024);
   hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, words);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL((k_compress<T, true>), dim3((uint32_t)n_wg), dim3(compress_waves<T>() * kWave), packed_run_lds(T, kTile * T),
+  hipLaunchKernelGGL((k_compress<T, true>), dim3((uint32_t)n_wg), dim3(compress_waves<T>() * kWave), 0,
                      s, x, n_new, 0,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
                      flags, ticket, n_chunks, x_stride, PruneOpts{});
