@@ -54,6 +54,11 @@ extern "C" {
 
 #define MUSTAFAR_TILE 64 /* channels per tile, one bit per wavefront lane */
 #define MUSTAFAR_PAD 8   /* packed non-zeros per tile rounded up to this  */
+/* stream_len of a stream whose bulk compression gave up (see
+ * mustafar_prune_compress); no real stream length reaches it */
+#define MUSTAFAR_STREAM_POISONED 0xffffffffu
+/* look-back polls before a chunk of mustafar_prune_compress gives up */
+#define MUSTAFAR_LOOKBACK_POLLS (1u << 20)
 
 enum mustafar_status {
     MUSTAFAR_OK = 0,
@@ -144,9 +149,32 @@ size_t mustafar_compress_workspace_bytes(int B, int H, int n_new);
  *       and per-stream ticket counters), so calls that share one workspace
  *       must not overlap
  * On success c->n_tokens += n_new. Errors: EINVAL (bad descriptor, n_new < 1,
- * misaligned x), ECAPACITY (n_tokens + n_new > cap_tokens), EWORKSPACE. */
+ * misaligned x), ECAPACITY (n_tokens + n_new > cap_tokens), EWORKSPACE.
+ *
+ * Completion status. Each chunk of 64 tokens finds its place in the stream by
+ * waiting for the running totals of the chunks before it (a single-pass
+ * scan). That wait is bounded (MUSTAFAR_LOOKBACK_POLLS reads; the chunks it
+ * waits for are always already running, so the bound is a guard, never
+ * reached in a healthy run). A chunk that reaches the bound writes nothing;
+ * its stream then has a hole and, once the call has finished on the device,
+ * its stream_len is MUSTAFAR_STREAM_POISONED. The first 32-bit word of ws is
+ * 0 after a call in which every stream was compressed and nonzero if any
+ * stream was poisoned; the caller reads it (a device-to-host copy after the
+ * stream has synchronised) before it reuses ws. A poisoned stream stays so:
+ * every later call skips it (compression and appends write nothing to it, the
+ * decode attention treats its compressed part as empty) until the cache is
+ * refilled from token 0. */
 int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void* ws,
                             size_t ws_bytes, void* stream);
+
+/* mustafar_prune_compress with the caller's bound on the look-back of a chunk,
+ * counted in reads of the other chunks' totals (for callers with a latency
+ * budget, and to exercise the give-up path: with max_polls = 0 no chunk but the
+ * first of a stream may read, so every stream of more than one chunk -- 64
+ * tokens, 128 at d = 64 -- is poisoned). Same arguments, status word and
+ * errors. */
+int mustafar_prune_compress_bounded(mustafar_ccache_t* c, const void* x, int n_new, uint32_t max_polls,
+                                    void* ws, size_t ws_bytes, void* stream);
 
 /* Prune, compress and append ONE token per stream (the token that leaves the
  * dense local window at a decode step, Sec. 3 and Appendix C.2). Needs no
@@ -177,8 +205,8 @@ int mustafar_append_kv(mustafar_ccache_t* Kc, mustafar_ccache_t* Vc, const void*
  *                                channel; w are non-negative fp32 channel
  *                                weights per token (see mustafar_query_lookahead).
  * head_keep (all modes but 2:4): NULL, or a HOST array [H] of kept counts per
- * head, each in [0, c->n_keep] (finer-grained sparsity, Sec. 4.5; the cache's
- * capacity is the one of n_keep). H <= 256 with head_keep.
+ * head, each in [0, c->n_keep] (finer-grained sparsity, named as future work
+ * in Conclusion and Limitations; the cache's capacity is the one of n_keep). H <= 256 with head_keep.
  * Per-channel caches only (mustafar_prune_compress_ex; n_new and c->n_tokens
  * multiples of 32; head_keep must be NULL):
  *   MUSTAFAR_PRUNE_CHANNEL       per-channel magnitude pruning in groups of 32
@@ -346,15 +374,17 @@ int mustafar_window_step(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_c
  * before the window's prefill; window slot s of (b, h) holds the weights of the
  * token in that slot. Each call adds |q[b][h*G+g][c]| (fp16 q [B][Hq][d],
  * 16-byte aligned; G = Hq/H), for g = 0, 1, ..., G-1 one after the other in
- * fp32, to kacc[b][h][s][c] for every batch entry b, kv-head h and slot s
- * holding one of the newest min(len[b], 32) window tokens. Called once per
- * decode step with that step's queries, after the step's
- * mustafar_window_step_weighted, it leaves a token that leaves the window 32
- * steps after it arrived with the weights mustafar_query_lookahead (L = 32)
- * computes from the same queries, bit for bit. Errors: EINVAL, EUNSUPPORTED
- * (G > 8). */
+ * fp32, to kacc[b][h][s][c] for every ACTIVE batch entry b (active: int32
+ * device [B], 4-byte aligned, nonzero = active; NULL: every entry), kv-head h
+ * and slot s holding one of the newest min(len[b], 32) window tokens; an
+ * inactive entry's weights do not change. Called once per decode step with
+ * that step's queries and the step's active mask, after the step's
+ * mustafar_window_step_weighted, it leaves a token that leaves the window with
+ * the weights of the queries of its own entry's 32 active steps from its
+ * arrival on: those mustafar_query_lookahead (L = 32) computes from that
+ * entry's query sequence, bit for bit. Errors: EINVAL, EUNSUPPORTED (G > 8). */
 int mustafar_window_key_weights(const void* q, int B, int Hq, const mustafar_window_t* w,
-                                float* kacc, void* stream);
+                                const void* active, float* kacc, void* stream);
 
 /* mustafar_window_step whose leaving key (the oldest token of a full window)
  * is pruned output-aware: channel score fl32(|k_c| x kacc[b][h][slot][c]), the
@@ -379,21 +409,23 @@ int mustafar_window_decode_attn(const void* q, int B, int Hq, const mustafar_cca
                                 void* stream);
 
 /* Decode attention as mustafar_window_decode_attn, then the output-aware
- * scores of per-channel value pruning (Sec. 2): for every batch entry b,
- * kv-head h and window slot holding one of the entry's tokens that arrived
- * fewer than 32 steps ago (the newest 32 of its len[b]),
+ * scores of per-channel value pruning (Sec. 2): for every ACTIVE batch entry b
+ * (active: int32 device [B], 4-byte aligned, nonzero = active; NULL: every
+ * entry), kv-head h and window slot holding one of the entry's tokens that
+ * arrived fewer than 32 of its steps ago (the newest 32 of its len[b]),
  *   acc[b][h][slot] += sum over the G query heads of h of the attention
  *                      probability of that token (Algorithm 1's softmax over
  *                      the compressed and window tokens),
- * so that once a token is 32 steps old, its slot holds the sum over the
- * current and the 31 following decode steps. acc: device fp32 [B][H][W],
- * 4-byte aligned, zeroed by the caller before the first step (the grouped
- * window step clears the slots it frees). The workspace is the one of
- * mustafar_window_decode_attn. Errors as mustafar_window_decode_attn. */
+ * so that once a token has seen 32 active steps of its entry, its slot holds
+ * the sum over the step it arrived in and the 31 following ones; an inactive
+ * entry's scores do not change (its output is still computed). acc: device
+ * fp32 [B][H][W], 4-byte aligned, zeroed by the caller before the first step
+ * (the grouped window step clears the slots it frees). The workspace is the
+ * one of mustafar_window_decode_attn. Errors as mustafar_window_decode_attn. */
 int mustafar_window_decode_attn_scores(const void* q, int B, int Hq, const mustafar_ccache_t* Kc,
                                        const mustafar_ccache_t* Vc, const mustafar_window_t* w,
-                                       float* acc, float scale, void* out, int n_splits, void* ws,
-                                       size_t ws_bytes, void* stream);
+                                       const void* active, float* acc, float scale, void* out,
+                                       int n_splits, void* ws, size_t ws_bytes, void* stream);
 
 /* One decode step of the GROUPED window lifecycle (per-channel value pruning in
  * groups of 32 tokens, Sec. 2): Kc is a per-token cache, Vc a per-channel

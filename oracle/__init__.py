@@ -16,8 +16,9 @@ loops over streams:
 * ``sparse_decode_attention`` -- decompress, then ``decode_attention``.
 * ``prune_token_24``, ``prune_token_scored``, ``compress_variant`` -- the
   pruner variants in the same format: 2:4 per token (Appendix B), output-aware
-  key pruning (Sec. 2), per-head kept counts (Sec. 4.5's finer-grained
-  sparsity); ``query_lookahead`` -- the channel weights of output-aware pruning.
+  key pruning (Sec. 2), per-head kept counts (finer-grained sparsity, which
+  the Conclusion and Limitations section names as future work);
+  ``query_lookahead`` -- the channel weights of output-aware pruning.
 * ``prune_channel_group``, ``compress_grouped`` -- per-channel value pruning in
   groups of 32 tokens, by magnitude or output-aware (Sec. 2's value-cache
   study), in the same format; ``attention_probs`` -- the softmax weights of

@@ -38,14 +38,17 @@ class WindowOracle:
 
     With ``output_aware_keys`` the keys that leave the window are pruned by the
     output-aware score of Sec. 2 instead of by magnitude: every call of
-    ``accumulate_key_weights`` (one per decode step, with that step's queries)
-    adds |q| of each query head of a kv-head, one head after the other in
-    float32, to the channel weights of each of the entry's newest 32 window
-    tokens, and a key leaves with channels ranked by fl32(|k_c| * w_c). A token
-    that leaves 32 steps after it arrived thus carries the sum over the query
-    of its own step and the 31 after it, as ``query_lookahead`` adds them. The
-    tokens a prefill compresses at once have no decode queries and are pruned
-    by magnitude.
+    ``accumulate_key_weights`` (one per decode step, with that step's queries
+    and activity mask) adds, for every entry active in the step, |q| of each
+    query head of a kv-head, one head after the other in float32, to the
+    channel weights of each of the entry's newest 32 window tokens, and a key
+    leaves with channels ranked by fl32(|k_c| * w_c). An entry that sits a step
+    out has no query of its own in it and gathers nothing. A token that leaves
+    the window thus carries the sum over the queries of its own entry in the
+    step it arrived and the entry's 31 active steps after it, as
+    ``query_lookahead`` adds them over that entry's query sequence. The tokens
+    a prefill compresses at once have no decode queries and are pruned by
+    magnitude.
     """
 
     def __init__(self, B: int, H: int, d: int, W: int, sk: float, sv: float,
@@ -70,12 +73,14 @@ class WindowOracle:
                 self.hist_v[b].append(np.array(xv[b, :, j]))
             self.n_prefill[b] = self.n_comp(b)
 
-    def accumulate_key_weights(self, q) -> None:
+    def accumulate_key_weights(self, q, active=None) -> None:
         """One decode step's queries q [B][Hq][d] (fp16) into the key weights of the
-        newest KEY_WEIGHT_STEPS window tokens of every entry."""
+        newest KEY_WEIGHT_STEPS window tokens of every entry active in the step."""
         qa = np.abs(np.asarray(q).view(np.float16).astype(np.float32))
         G = qa.shape[1] // self.H
         for b in range(self.B):
+            if active is not None and not active[b]:
+                continue
             n, L = self.n_comp(b), self.window_len(b)
             for p in range(max(0, L - KEY_WEIGHT_STEPS), L):
                 w = self.key_w[b].setdefault(n + p, np.zeros((self.H, self.d), dtype=np.float32))
@@ -262,8 +267,9 @@ class GroupedWindowOracle:
 
     def score_increments(self, q, b: int, scale: float = 0.0) -> np.ndarray:
         """float64 [H][len]: for every window token of entry b younger than 32
-        steps (the newest 32), the attention probability it receives from q
-        [Hq][d], summed over the query heads of each kv-head; 0 for older ones."""
+        of its steps (the newest 32), the attention probability it receives from
+        q [Hq][d], summed over the query heads of each kv-head; 0 for older ones.
+        Only a step in which entry b is active adds these to its tokens' scores."""
         q = np.asarray(q).view(np.uint16)[None]
         enc_k, _ = self.compressed(b)
         wk, _ = self.window(b)

@@ -21,6 +21,8 @@ TILE = 64
 PAD = 8
 
 OK, EINVAL, ECAPACITY, EWORKSPACE, ELAUNCH, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+STREAM_POISONED = 0xFFFFFFFF   # stream_len of a stream whose bulk compression gave up
+LOOKBACK_POLLS = 1 << 20
 
 _lib = None
 
@@ -77,6 +79,9 @@ _SIGS = {
     "mustafar_prune_compress": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
                                                ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t,
                                                ctypes.c_void_p]),
+    "mustafar_prune_compress_bounded": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                                       ctypes.c_int, ctypes.c_uint32, ctypes.c_void_p,
+                                                       ctypes.c_size_t, ctypes.c_void_p]),
     "mustafar_append_kv": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.POINTER(ccache_t),
                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "mustafar_append": (ctypes.c_int, [ctypes.POINTER(ccache_t), ctypes.c_void_p,
@@ -110,7 +115,7 @@ _SIGS = {
                                                      ctypes.c_void_p]),
     "mustafar_window_key_weights": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
                                                    ctypes.POINTER(window_t), ctypes.c_void_p,
-                                                   ctypes.c_void_p]),
+                                                   ctypes.c_void_p, ctypes.c_void_p]),
     "mustafar_window_decode_attn": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
                                                    ctypes.POINTER(ccache_t),
                                                    ctypes.POINTER(ccache_t),
@@ -121,6 +126,7 @@ _SIGS = {
                                                           ctypes.POINTER(ccache_t),
                                                           ctypes.POINTER(ccache_t),
                                                           ctypes.POINTER(window_t), ctypes.c_void_p,
+                                                          ctypes.c_void_p,
                                                           ctypes.c_float, ctypes.c_void_p, ctypes.c_int,
                                                           ctypes.c_void_p, ctypes.c_size_t,
                                                           ctypes.c_void_p]),
@@ -277,6 +283,25 @@ def mustafar_prune_compress(cache: CompressedCache, x, ws=None, stream=None) -> 
     _check("mustafar_prune_compress", lib().mustafar_prune_compress(
         ctypes.byref(cache.desc), _dptr(x), n_new, _dptr(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
+
+
+def mustafar_prune_compress_bounded(cache: CompressedCache, x, max_polls: int, ws=None,
+                                    stream=None) -> None:
+    """mustafar_prune_compress with the caller's bound on a chunk's look-back polls."""
+    import torch
+    n_new = int(x.shape[2])
+    need = mustafar_compress_workspace_bytes(cache.desc.B, cache.desc.H, n_new)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=x.device)
+    _check("mustafar_prune_compress_bounded", lib().mustafar_prune_compress_bounded(
+        ctypes.byref(cache.desc), _dptr(x), n_new, int(max_polls), _dptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def compress_status(ws) -> int:
+    """The status word a bulk compression left at the start of its workspace: 0 if
+    every stream was compressed, nonzero if a stream was poisoned (synchronises)."""
+    return int(ws[:4].view(dtype=__import__("torch").int32).item())
 
 
 def mustafar_append_kv(Kc: CompressedCache, Vc: CompressedCache, k_new, v_new, stream=None) -> None:
@@ -444,12 +469,13 @@ def mustafar_window_step_weighted(win: DenseWindow, Kc: CompressedCache, Vc: Com
         _dptr(v_new), _dptr(active), _dptr(kacc), _stream(stream)))
 
 
-def mustafar_window_key_weights(q, win: DenseWindow, kacc, stream=None) -> None:
+def mustafar_window_key_weights(q, win: DenseWindow, kacc, active=None, stream=None) -> None:
     """kacc[b][h][slot] += |q| of the query heads of kv-head h (one after the other, in
-    fp32) for the newest 32 window tokens of every entry; q [B][Hq][d] fp16."""
+    fp32) for the newest 32 window tokens of every active entry (active: int32 device
+    [B] or None for all); q [B][Hq][d] fp16."""
     B, Hq, _ = (int(s) for s in q.shape)
     _check("mustafar_window_key_weights", lib().mustafar_window_key_weights(
-        _dptr(q), B, Hq, ctypes.byref(win.desc), _dptr(kacc), _stream(stream)))
+        _dptr(q), B, Hq, ctypes.byref(win.desc), _dptr(active), _dptr(kacc), _stream(stream)))
 
 
 def mustafar_window_decode_attn(q, Kc: CompressedCache, Vc: CompressedCache, win: DenseWindow,
@@ -470,10 +496,10 @@ def mustafar_window_decode_attn(q, Kc: CompressedCache, Vc: CompressedCache, win
 
 def mustafar_window_decode_attn_scores(q, Kc: CompressedCache, Vc: CompressedCache,
                                        win: DenseWindow, acc, scale: float = 0.0, out=None,
-                                       n_splits: int = 0, ws=None, stream=None):
+                                       n_splits: int = 0, ws=None, active=None, stream=None):
     """mustafar_window_decode_attn, then acc [B][H][W] (fp32, device) += the attention
     probability, summed over each kv-head's query heads, of every window token
-    younger than 32 steps."""
+    younger than 32 steps, for the active entries (active: int32 device [B] or None)."""
     import torch
     B, Hq, d = (int(s) for s in q.shape)
     if out is None:
@@ -481,7 +507,7 @@ def mustafar_window_decode_attn_scores(q, Kc: CompressedCache, Vc: CompressedCac
     ws = _attn_ws(B, Hq, Kc.desc.H, d, Kc.n_tokens, n_splits, ws, q.device)
     _check("mustafar_window_decode_attn_scores", lib().mustafar_window_decode_attn_scores(
         _dptr(q), B, Hq, ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), ctypes.byref(win.desc),
-        _dptr(acc), float(scale), _dptr(out), int(n_splits), _dptr(ws),
+        _dptr(active), _dptr(acc), float(scale), _dptr(out), int(n_splits), _dptr(ws),
         ws.numel() * ws.element_size(), _stream(stream)))
     return out
 

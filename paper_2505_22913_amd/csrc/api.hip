@@ -23,6 +23,8 @@ constexpr int kDenseGroupedTargetGroups = 4096;
 constexpr int kGroupedMinSegTokens = 128;
 constexpr int kSegAlign = 64;              // segments are whole 64-token blocks
 constexpr int kKeyWeightSteps = 32;        // output-aware keys: the current and 31 next queries
+static_assert(MUSTAFAR_LOOKBACK_POLLS == mf::kLookbackPolls, "look-back bound");
+static_assert(MUSTAFAR_STREAM_POISONED == mf::kStreamPoisoned, "poisoned stream marker");
 
 bool aligned(const void* p, uintptr_t a) { return p && ((uintptr_t)p % a) == 0; }
 bool head_dim_ok(int d) { return d == 64 || d == 128 || d == 256; }
@@ -43,6 +45,8 @@ int check_cache(const mustafar_ccache_t* c) {
                            ? mustafar_grouped_stream_capacity(c->d, c->group_keep, c->cap_tokens)
                            : mustafar_stream_capacity(c->d, c->n_keep, c->cap_tokens);
   if (c->val_stride % kPad != 0 || c->val_stride < need) return MUSTAFAR_EINVAL;
+  // Offsets and stream lengths are u32, and the largest u32 marks a poisoned stream.
+  if (need >= (int64_t)mf::kStreamPoisoned) return MUSTAFAR_EUNSUPPORTED;
   return MUSTAFAR_OK;
 }
 
@@ -68,6 +72,7 @@ mf::SparseSide side_of(const mustafar_ccache_t* c) {
   s.bitmaps = c->bitmaps;
   s.offsets = c->offsets;
   s.values = c->values;
+  s.stream_len = c->stream_len;
   s.val_stride = c->val_stride;
   s.cap_tokens = c->cap_tokens;
   s.n_keep = c->n_keep;
@@ -260,12 +265,13 @@ int mustafar_ccache_init_grouped(mustafar_ccache_t* c, void* bitmaps, void* offs
 size_t mustafar_compress_workspace_bytes(int B, int H, int n_new) {
   if (B < 1 || H < 1 || n_new < 1) return 0;
   const int64_t n_chunks = (n_new + mf::kMinCompressChunk - 1) / mf::kMinCompressChunk;
-  // per stream: a look-back flag per chunk and a ticket counter
-  return (size_t)((int64_t)B * H * (n_chunks * (int64_t)sizeof(uint64_t) + (int64_t)sizeof(uint32_t)) + 16);
+  // the status word (16 bytes), then per stream a look-back flag per chunk, a
+  // ticket counter and a give-up mark
+  return (size_t)(16 + (int64_t)B * H * (n_chunks * (int64_t)sizeof(uint64_t) + 2 * (int64_t)sizeof(uint32_t)));
 }
 
-int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void* ws,
-                            size_t ws_bytes, void* stream) {
+static int prune_compress_polls(mustafar_ccache_t* c, const void* x, int n_new, uint32_t max_polls,
+                                void* ws, size_t ws_bytes, void* stream) {
   int st = check_cache(c);
   if (st != MUSTAFAR_OK) return st;
   if (n_new < 1 || !aligned(x, 16)) return MUSTAFAR_EINVAL;
@@ -275,12 +281,22 @@ int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void
   if (!aligned(ws, 8) || ws_bytes < need) return MUSTAFAR_EWORKSPACE;
   const hipError_t e =
       grouped(c) ? mf::launch_compress_channel(view_of(c), (const uint16_t*)x, n_new, c->n_tokens,
-                                               (uint32_t*)ws, (hipStream_t)stream, nullptr)
+                                               (uint32_t*)ws, (hipStream_t)stream, nullptr, 0, max_polls)
                  : mf::launch_compress(view_of(c), (const uint16_t*)x, n_new, c->n_tokens,
-                                       (uint32_t*)ws, (hipStream_t)stream);
+                                       (uint32_t*)ws, (hipStream_t)stream, 0, max_polls);
   st = status_of(e);
   if (st == MUSTAFAR_OK) c->n_tokens += n_new;
   return st;
+}
+
+int mustafar_prune_compress(mustafar_ccache_t* c, const void* x, int n_new, void* ws,
+                            size_t ws_bytes, void* stream) {
+  return prune_compress_polls(c, x, n_new, MUSTAFAR_LOOKBACK_POLLS, ws, ws_bytes, stream);
+}
+
+int mustafar_prune_compress_bounded(mustafar_ccache_t* c, const void* x, int n_new, uint32_t max_polls,
+                                    void* ws, size_t ws_bytes, void* stream) {
+  return prune_compress_polls(c, x, n_new, max_polls, ws, ws_bytes, stream);
 }
 
 int mustafar_append(mustafar_ccache_t* c, const void* x_new, void* stream) {
@@ -475,7 +491,7 @@ int mustafar_dense_decode_attn(const void* q, int B, int Hq, int Hkv, const void
   int st = decode_common(q, B, Hq, Hkv, d, 0, n_tokens, 0, n_splits, scale, out, ws, ws_bytes, &sh,
                          &ws_ml, &ws_o);
   if (st != MUSTAFAR_OK) return st;
-  mf::SparseSide none = {nullptr, nullptr, nullptr, 0, 1, 0};
+  mf::SparseSide none = {nullptr, nullptr, nullptr, nullptr, 0, 1, 0};
   return status_of(mf::launch_attention(sh, (const uint16_t*)q, none, none, (const uint16_t*)k,
                                         (const uint16_t*)v, ws_ml, ws_o, (uint16_t*)out,
                                         (hipStream_t)stream));
@@ -566,15 +582,17 @@ int mustafar_window_step_weighted(mustafar_window_t* w, mustafar_ccache_t* Kc, m
   return window_step_common(w, Kc, Vc, k_new, v_new, active, kacc, stream);
 }
 
-int mustafar_window_key_weights(const void* q, int B, int Hq, const mustafar_window_t* w, float* kacc,
-                                void* stream) {
+int mustafar_window_key_weights(const void* q, int B, int Hq, const mustafar_window_t* w,
+                                const void* active, float* kacc, void* stream) {
   int st = check_window(w);
   if (st != MUSTAFAR_OK) return st;
   if (B != w->B || Hq < 1 || Hq % w->H != 0) return MUSTAFAR_EINVAL;
   if (Hq / w->H > 8) return MUSTAFAR_EUNSUPPORTED;
   if (!aligned(q, 16) || !aligned(kacc, 16)) return MUSTAFAR_EINVAL;
+  if (active && !aligned(active, 4)) return MUSTAFAR_EINVAL;
   return status_of(mf::launch_window_key_weights(window_view_of(w), (const uint16_t*)q, Hq / w->H,
-                                                 w->d / kTile, kacc, (hipStream_t)stream));
+                                                 w->d / kTile, (const int32_t*)active, kacc,
+                                                 (hipStream_t)stream));
 }
 
 static int window_step_common(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,
@@ -627,13 +645,14 @@ int mustafar_window_decode_attn(const void* q, int B, int Hq, const mustafar_cca
 
 int mustafar_window_decode_attn_scores(const void* q, int B, int Hq, const mustafar_ccache_t* Kc,
                                        const mustafar_ccache_t* Vc, const mustafar_window_t* w,
-                                       float* acc, float scale, void* out, int n_splits, void* ws,
-                                       size_t ws_bytes, void* stream) {
+                                       const void* active, float* acc, float scale, void* out,
+                                       int n_splits, void* ws, size_t ws_bytes, void* stream) {
   int st = check_window(w);
   if (st != MUSTAFAR_OK) return st;
   if ((st = check_cache(Kc)) != MUSTAFAR_OK || (st = check_cache(Vc)) != MUSTAFAR_OK) return st;
   if (!window_matches(w, Kc) || !window_matches(w, Vc) || w->B != B) return MUSTAFAR_EINVAL;
   if (Kc->n_tokens != Vc->n_tokens || !aligned(acc, 4)) return MUSTAFAR_EINVAL;
+  if (active && !aligned(active, 4)) return MUSTAFAR_EINVAL;
   mf::AttnShape sh;
   float *ws_ml, *ws_o;
   st = decode_common(q, B, Hq, Kc->H, Kc->d, Kc->n_tokens, w->W, 1, n_splits, scale, out, ws,
@@ -654,7 +673,7 @@ int mustafar_window_decode_attn_scores(const void* q, int B, int Hq, const musta
                                       ws_ml, ws_o, (uint16_t*)out, s));
   if (st != MUSTAFAR_OK) return st;
   return status_of(mf::launch_window_scores(window_view_of(w), (const uint16_t*)q, sh.G, sh.T,
-                                            sh.scale_log2, lse2, acc, s));
+                                            sh.scale_log2, lse2, (const int32_t*)active, acc, s));
 }
 
 int mustafar_window_step_grouped(mustafar_window_t* w, mustafar_ccache_t* Kc, mustafar_ccache_t* Vc,

@@ -121,6 +121,13 @@ struct SparseLds {
 
 constexpr int kHalfSlots = 33;
 constexpr float kSlack = 8.f;  // log2 headroom of the lazy softmax base
+// p is stored as fp16 for p.V; it is computed as exp2(score - base + kPBias),
+// base = m_run, so that the largest p (2^(kSlack + kPBias) = 2^15) still fits
+// fp16 and the small ones keep 2^kPBias more range before they flush to zero
+// (fp16's smallest subnormal is 2^-24). Numerator and denominator sum the same
+// rounded p; the partial's maximum is written as m_run - kPBias, so that (m, l)
+// stay a consistent pair for the merge.
+constexpr float kPBias = 7.f;
 constexpr uint32_t kPvRow = 32;  // dwords per half-tile row (T x NBH)
 
 // Bytes per tile of the q table: 49 dwords, so the two tiles of d = 128 sit 17
@@ -268,7 +275,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
           for (int k = 0; k < PU::UPL; ++k) oh[h][k] *= alpha;
         m_run = mnew;
       }
-      const _Float16 ph = valid ? (_Float16)__builtin_amdgcn_exp2f(sc - m_run) : (_Float16)0.f;
+      const _Float16 ph = valid ? (_Float16)__builtin_amdgcn_exp2f(sc - m_run + kPBias) : (_Float16)0.f;
       l_lane += t == 0 ? (float)ph : 0.f;
       if (t == 0) lds_store<_Float16>(base + L.ps + (j % PU::NBH) * 4 + (j / PU::NBH) * 2, ph);
     }
@@ -333,6 +340,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   }
 
   l_run = wave_sum_u(l_lane);
+  m_run -= kPBias;  // l and o are sums of exp2(score - (m_run - kPBias))
 
   // Back to the partial layout (lane = channel of each tile): channel `lane`
   // of tile tt is channel lane % 32 of half lane / 32, unit (lane % 32) T + tt.
@@ -452,7 +460,7 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void k_merge(const float2* __r
   for (int tt = 0; tt < T; ++tt) part[wave][lane + kTile * tt] = acc[tt];
   __syncthreads();
   if (wave == 0) {
-    const float inv = 1.f / L;
+    const float inv = L > 0.f ? 1.f / L : 0.f;  // no token at all (every stream skipped): 0
     const int64_t prow = (int64_t)blockIdx.y * BHq + r;
     if (!FINAL && lane == 0) part_ml[prow] = make_float2(M, L);
     if (FINAL && lse2 != nullptr && lane == 0) lse2[r] = M + __builtin_log2f(L);
@@ -577,18 +585,21 @@ hipError_t launch_attention(const AttnShape& sh, const uint16_t* q, const Sparse
 // probability of every window token younger than 32 steps, summed over the G
 // query heads of its kv-head and added to its slot's score. One wave per
 // (batch entry, kv-head), lane = window position; q staged in LDS (every lane
-// reads the same address, a broadcast).
+// reads the same address, a broadcast). An entry that is not active in this
+// step gathers nothing.
 // ------------------------------------------------------------------------------------------
 constexpr int kScoreSteps = 32;  // steps a token's score accumulates (the current and 31 more)
 
 template <int T, int G>
 __global__ __launch_bounds__(kWave) void k_window_scores(WindowView w, const uint16_t* __restrict__ q,
                                                          float scale_log2, const float* __restrict__ lse2,
+                                                         const int32_t* __restrict__ active,
                                                          float* __restrict__ acc) {
   constexpr int d = kTile * T;
   __shared__ __attribute__((aligned(16))) uint16_t qs[G * d];
   const int bh = blockIdx.x;
   const int b = bh / w.H;
+  if (active != nullptr && active[b] == 0) return;  // uniform over the workgroup
   const uint32_t lane = lane_id();
   for (int i = (int)lane; i < G * d; i += kWave) qs[i] = q[(int64_t)bh * G * d + i];
   __syncthreads();
@@ -624,24 +635,24 @@ __global__ __launch_bounds__(kWave) void k_window_scores(WindowView w, const uin
 
 template <int T>
 static hipError_t window_scores_T(const WindowView& w, const uint16_t* q, int G, float scale_log2,
-                                  const float* lse2, float* acc, hipStream_t s) {
+                                  const float* lse2, const int32_t* active, float* acc, hipStream_t s) {
   const dim3 grid((uint32_t)(w.B * w.H));
   switch (G) {
-    case 1: hipLaunchKernelGGL((k_window_scores<T, 1>), grid, dim3(kWave), 0, s, w, q, scale_log2, lse2, acc); break;
-    case 2: hipLaunchKernelGGL((k_window_scores<T, 2>), grid, dim3(kWave), 0, s, w, q, scale_log2, lse2, acc); break;
-    case 4: hipLaunchKernelGGL((k_window_scores<T, 4>), grid, dim3(kWave), 0, s, w, q, scale_log2, lse2, acc); break;
-    case 8: hipLaunchKernelGGL((k_window_scores<T, 8>), grid, dim3(kWave), 0, s, w, q, scale_log2, lse2, acc); break;
+    case 1: hipLaunchKernelGGL((k_window_scores<T, 1>), grid, dim3(kWave), 0, s, w, q, scale_log2, lse2, active, acc); break;
+    case 2: hipLaunchKernelGGL((k_window_scores<T, 2>), grid, dim3(kWave), 0, s, w, q, scale_log2, lse2, active, acc); break;
+    case 4: hipLaunchKernelGGL((k_window_scores<T, 4>), grid, dim3(kWave), 0, s, w, q, scale_log2, lse2, active, acc); break;
+    case 8: hipLaunchKernelGGL((k_window_scores<T, 8>), grid, dim3(kWave), 0, s, w, q, scale_log2, lse2, active, acc); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_window_scores(const WindowView& w, const uint16_t* q, int G, int T, float scale_log2,
-                                const float* lse2, float* acc, hipStream_t s) {
+                                const float* lse2, const int32_t* active, float* acc, hipStream_t s) {
   switch (T) {
-    case 1: return window_scores_T<1>(w, q, G, scale_log2, lse2, acc, s);
-    case 2: return window_scores_T<2>(w, q, G, scale_log2, lse2, acc, s);
-    case 4: return window_scores_T<4>(w, q, G, scale_log2, lse2, acc, s);
+    case 1: return window_scores_T<1>(w, q, G, scale_log2, lse2, active, acc, s);
+    case 2: return window_scores_T<2>(w, q, G, scale_log2, lse2, active, acc, s);
+    case 4: return window_scores_T<4>(w, q, G, scale_log2, lse2, active, acc, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -27,6 +27,12 @@ namespace mf {
 typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// The probabilities enter the p.V product as fp16, computed against the exact
+// running maximum with this exponent bias: the largest is 2^15 (inside fp16),
+// and the small ones keep 15 more binades before they flush to zero. The
+// partial's maximum is written as m - kMfmaPBias, consistent with l and o.
+constexpr float kMfmaPBias = 15.f;
+
 // Slots per tile in Kd and VdT: channel c of half h is slot 4 + 36h + (c % 32);
 // slot 3 + 36h is the scratch slot the walks address with channel -1, and the
 // 4-channel groups the MFMA operands read stay 8-byte aligned.
@@ -170,17 +176,19 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
     bmax = fmaxf(bmax, __shfl_xor(bmax, 32, kWave));
     const float mnew = fmaxf(m_run, bmax);
     const float alpha = __builtin_amdgcn_exp2f(m_run - mnew);
+    // p = exp2(score - mnew + kMfmaPBias) in fp16 (at most 2^15); the sum is
+    // taken over the same rounded p that the p.V product multiplies.
     float psum = 0.f;
     half4_t pa[NG];
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-      float p[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        p[e] = r16 < (uint32_t)G ? __builtin_amdgcn_exp2f(sc[g][e] - mnew) : 0.f;
-        psum += p[e];
+        const _Float16 ph =
+            r16 < (uint32_t)G ? (_Float16)__builtin_amdgcn_exp2f(sc[g][e] - mnew + kMfmaPBias) : (_Float16)0.f;
+        pa[g][e] = ph;
+        psum += (float)ph;
       }
-      pa[g] = (half4_t){(_Float16)p[0], (_Float16)p[1], (_Float16)p[2], (_Float16)p[3]};
     }
     psum += __shfl_xor(psum, 16, kWave);
     psum += __shfl_xor(psum, 32, kWave);
@@ -267,6 +275,7 @@ __global__ __launch_bounds__(64, (mfma_waves<T, G, STAGE>())) void k_sparse_attn
 #pragma unroll
   for (int c = 0; c < Geo::NC; ++c) o[c] = (f32x4){0.f, 0.f, 0.f, 0.f};
   sparse_body_mfma<T, G, STAGE>(a, seg, bh, smem, m_run, l_run, o);
+  m_run -= kMfmaPBias;  // -inf stays -inf for an empty segment
 
   const uint32_t lane = lane_id();
   const uint32_t r16 = lane % 16, q4 = lane / 16;

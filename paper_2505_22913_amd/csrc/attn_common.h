@@ -46,8 +46,10 @@ struct AttnArgs {
   float* lse2;  // optional: the final merge writes m + log2(l) per query head
 };
 
-// Compressed tokens of stream bh (its batch entry's count when ragged).
+// Compressed tokens of stream bh (its batch entry's count when ragged); none
+// when a bulk compression gave up on the stream (its offsets have holes).
 __device__ __forceinline__ int stream_tokens(const AttnArgs& a, int bh) {
+  if (a.K.stream_len[bh] == kStreamPoisoned || a.V.stream_len[bh] == kStreamPoisoned) return 0;
   return a.n_comp ? min(a.n_comp[bh / a.Hkv], a.n_s) : a.n_s;
 }
 

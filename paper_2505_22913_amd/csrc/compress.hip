@@ -122,13 +122,21 @@ __device__ __forceinline__ void load_token(const uint16_t* __restrict__ src, uin
 // Look-back flag of one chunk: status in bits 63:62, a 32-bit count below.
 constexpr uint64_t kFlagAgg = 1ull << 62;     // the chunk's own total is known
 constexpr uint64_t kFlagPrefix = 2ull << 62;  // the stream offset after the chunk is known
-constexpr uint32_t kSpinLimit = 1u << 20;     // polls before a chunk gives up (never reached)
-constexpr uint32_t kBadBase = 0xffffffffu;
+constexpr uint32_t kBadBase = 0xffffffffu;    // look_back gave up
 
 __global__ void k_clear(uint32_t* __restrict__ p, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x)
     p[i] = 0u;
+}
+
+// After a bulk compression (stream-ordered, so every chunk has finished): a
+// stream one of whose chunks gave up has holes, so its stream_len becomes
+// kStreamPoisoned, which every later call treats as "skip this stream".
+__global__ void k_compress_finalize(const uint32_t* __restrict__ gave_up, uint32_t* __restrict__ stream_len,
+                                    int BH) {
+  const int bh = blockIdx.x * blockDim.x + threadIdx.x;
+  if (bh < BH && gave_up[bh] != 0u) stream_len[bh] = kStreamPoisoned;
 }
 
 // The flag words are the only data workgroups exchange (the count travels in
@@ -142,7 +150,8 @@ __global__ void k_clear(uint32_t* __restrict__ p, int64_t n) {
 // the first known prefix, moving 64 chunks further back while none is found.
 // Chunks with lower tickets (of the same stream) are already running and
 // publish their totals without waiting, so every poll is eventually answered;
-// the poll count is bounded anyway.
+// the number of flag reads is bounded anyway (max_polls; with 0 every chunk
+// but a stream's first gives up, which is how the give-up path is tested).
 // The chunk's total (chunk 0: its prefix, first_base + total) is published as
 // soon as it is known, before the chunk packs, so that the chunks after it
 // rarely wait for it.
@@ -158,10 +167,11 @@ __device__ void publish_total(uint64_t* __restrict__ fl, int chunk, uint32_t tot
 }
 
 __device__ uint32_t look_back(uint64_t* __restrict__ fl, int chunk, uint32_t total,
-                              uint32_t first_base, uint32_t lane) {
+                              uint32_t first_base, uint32_t lane, uint32_t max_polls) {
   if (chunk == 0) return first_base;
   uint32_t acc = 0, polls = 0;
   for (int top = chunk - 1;;) {
+    if (polls++ >= max_polls) return kBadBase;
     const int p = top - (int)lane;
     // Positions before chunk 0 read as a known prefix of 0.
     const uint64_t f = p >= 0 ? __hip_atomic_load(fl + p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
@@ -172,7 +182,6 @@ __device__ uint32_t look_back(uint64_t* __restrict__ fl, int chunk, uint32_t tot
     const uint32_t first = pref ? (uint32_t)__builtin_ctzll(pref) : 64u;  // nearest prefix
     const uint64_t upto = first >= 63u ? ~0ull : ((2ull << first) - 1ull);
     if (none & upto) {  // a chunk between here and that prefix has not published yet
-      if (++polls > kSpinLimit) return kBadBase;
       __builtin_amdgcn_s_sleep(1);
       continue;
     }
@@ -258,7 +267,9 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
                                                     int cap_tokens, int tok0, int64_t val_stride,
                                                     uint64_t* __restrict__ flags,
                                                     uint32_t* __restrict__ ticket_ctr, int n_chunks,
-                                                    int64_t x_stride, PruneOpts o) {
+                                                    int64_t x_stride, PruneOpts o, uint32_t max_polls,
+                                                    uint32_t* __restrict__ gave_up,
+                                                    uint32_t* __restrict__ status) {
   constexpr int d = kTile * T;
   constexpr int kCompressWaves = compress_waves<T>();
   constexpr int LPT = T >= 2 ? 2 : 1;      // lanes per token (selection and packing)
@@ -276,6 +287,10 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
   // Workgroups take the streams in turn and, within a stream, ordered tickets
   // from the stream's counter (one counter per stream keeps the atomics spread).
   const int bh = (int)(blockIdx.x % (gridDim.x / (uint32_t)n_chunks));
+  // A stream poisoned by an earlier call takes no more tokens: every workgroup
+  // of it leaves before drawing a ticket (the last chunk, which rewrites
+  // stream_len, draws the last ticket, after every other workgroup's read).
+  if (tok0 > 0 && __builtin_amdgcn_readfirstlane((int)stream_len[bh]) == (int)kStreamPoisoned) return;
   if (threadIdx.x == 0) s_share[0] = atomicAdd(ticket_ctr + bh, 1u);
   __syncthreads();
   const int chunk = __builtin_amdgcn_readfirstlane((int)s_share[0]);
@@ -448,9 +463,15 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
   }
 
   if (wave == 0) {
-    const uint32_t b = look_back(flags + (int64_t)bh * n_chunks, chunk, run, first, lane);
+    const uint32_t b = look_back(flags + (int64_t)bh * n_chunks, chunk, run, first, lane, max_polls);
     if (lane == 0) s_share[kCompressWaves + 1] = b;
-    if (lane == 0 && chunk == n_chunks - 1) stream_len[bh] = b == kBadBase ? kBadBase : b + run;
+    if (lane == 0 && b == kBadBase) {
+      // Mark the stream and the call; k_compress_finalize poisons the stream
+      // once every chunk has finished.
+      __hip_atomic_store(gave_up + bh, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (lane == 0 && chunk == n_chunks - 1 && b != kBadBase) stream_len[bh] = b + run;
   }
   __syncthreads();  // the chunk's base
   const uint32_t base = __builtin_amdgcn_readfirstlane((int)s_share[kCompressWaves + 1]);
@@ -716,6 +737,7 @@ template <int T>
 __device__ __forceinline__ void append_one(const CacheView& c, int bh, int tok,
                                            const uint16_t* __restrict__ src, uint32_t lane) {
   const uint32_t base = tok > 0 ? c.stream_len[bh] : 0u;
+  if (base == kStreamPoisoned) return;  // the stream lost tokens: it takes no more
   uint16_t xv[T];
   load_token<T>(src, lane, xv);
   uint32_t mag[T];
@@ -739,6 +761,7 @@ __device__ __forceinline__ void append_one_variant(const CacheView& c, const Pru
                                                    const uint16_t* __restrict__ src,
                                                    const float* __restrict__ w, uint32_t lane) {
   const uint32_t base = tok > 0 ? c.stream_len[bh] : 0u;
+  if (base == kStreamPoisoned) return;
   uint16_t xv[T];
   load_token<T>(src, lane, xv);
   uint64_t bm[T];
@@ -788,6 +811,7 @@ __device__ __forceinline__ void append_one_weighted(const CacheView& c, int bh, 
                                                     const uint16_t* __restrict__ src,
                                                     const float* __restrict__ w, uint32_t lane) {
   const uint32_t base = tok > 0 ? c.stream_len[bh] : 0u;
+  if (base == kStreamPoisoned) return;
   uint16_t xv[T];
   load_token<T>(src, lane, xv);
   uint64_t bm[T];
@@ -852,18 +876,21 @@ __global__ __launch_bounds__(256) void k_window_step(CacheView kc, CacheView vc,
 // 256-thread block per (entry, kv-head); a thread owns four channels of some of
 // the newest kKeyWeightSteps slots, loads all of them before it adds and
 // stores (no load waits on a store), and adds the |q| of the G query heads one
-// by one, head order.
+// by one, head order. An entry that is not active in this step has no query
+// of its own here and gathers nothing.
 constexpr int kKeyWeightSteps = 32;
 
 template <int T>
 __global__ __launch_bounds__(256) void k_window_key_weights(WindowView w, const uint16_t* __restrict__ q,
-                                                            int G, float* __restrict__ kacc) {
+                                                            int G, const int32_t* __restrict__ active,
+                                                            float* __restrict__ kacc) {
   constexpr int d = kTile * T;
   constexpr int C4 = d / 4;                  // four-channel columns per slot
   constexpr int ROWS = 256 / C4;             // slots per pass of the block
   constexpr int PASSES = kKeyWeightSteps / ROWS;
   const int bh = blockIdx.x;
   const int b = bh / w.H;
+  if (active != nullptr && active[b] == 0) return;
   const int len = w.len[b], head = w.head[b];
   if (len <= 0 || len > w.W || head < 0 || head >= w.W) return;
   const int c4 = (int)threadIdx.x % C4, r0 = (int)threadIdx.x / C4;
@@ -940,9 +967,10 @@ __global__ __launch_bounds__(256) void k_window_step_grouped(CacheView kc, Cache
   const int slot = (head + len) % w.W;
   const int tok = w.n_comp[b];
   if (len >= w.W && tok >= 0 && tok + kGroup <= kc.cap_tokens && tok + kGroup <= vc.cap_tokens) {
-    // Keys, one token at a time (the selection of mustafar_append).
+    // Keys, one token at a time (the selection of mustafar_append); a poisoned
+    // stream takes no more tokens.
     uint32_t base = tok > 0 ? kc.stream_len[bh] : 0u;
-    for (int u = 0; u < kGroup; ++u) {
+    for (int u = 0; u < kGroup && base != kStreamPoisoned; ++u) {
       uint16_t xv[T];
       load_token<T>(kr + (int64_t)((head + u) % w.W) * d, lane, xv);
       uint32_t mag[T];
@@ -957,7 +985,7 @@ __global__ __launch_bounds__(256) void k_window_step_grouped(CacheView kc, Cache
       if (lane < (uint32_t)T) kc.bitmaps[tile0 + lane] = mine;
       base += pack_token<T>(xv, bm, base, kc.values + (int64_t)bh * kc.val_stride, kc.offsets + tile0, lane);
     }
-    if (lane == 0) kc.stream_len[bh] = base;
+    if (lane == 0 && base != kStreamPoisoned) kc.stream_len[bh] = base;
     // Values: per-channel keep words over the group, then each token packed
     // with its tile bitmaps.
     uint32_t word[T];
@@ -972,7 +1000,7 @@ __global__ __launch_bounds__(256) void k_window_step_grouped(CacheView kc, Cache
       word[t] = channel_keep_word<SCORED ? 31 : 15>(key, vc.group_keep);
     }
     base = tok > 0 ? vc.stream_len[bh] : 0u;
-    for (int u = 0; u < kGroup; ++u) {
+    for (int u = 0; u < kGroup && base != kStreamPoisoned; ++u) {
       uint16_t xv[T];
       load_token<T>(vr + (int64_t)((head + u) % w.W) * d, lane, xv);
       uint64_t bm[T];
@@ -985,7 +1013,7 @@ __global__ __launch_bounds__(256) void k_window_step_grouped(CacheView kc, Cache
       if (lane < (uint32_t)T) vc.bitmaps[tile0 + lane] = mine;
       base += pack_token<T>(xv, bm, base, vc.values + (int64_t)bh * vc.val_stride, vc.offsets + tile0, lane);
     }
-    if (lane == 0) vc.stream_len[bh] = base;
+    if (lane == 0 && base != kStreamPoisoned) vc.stream_len[bh] = base;
   }
   // The graduated tokens were consumed above, so their slots can be reused.
 #pragma unroll
@@ -1032,23 +1060,34 @@ __global__ __launch_bounds__(256) void k_window_fill(WindowView w, int b, int d,
   }
 }
 
-template <int T>
-static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, int64_t x_stride,
-                             int tok0, uint32_t* ws, hipStream_t s, const PruneOpts& o = PruneOpts{}) {
+// Clears the workspace, runs k_compress (PRESET: with the bitmaps already in the
+// cache) and poisons the streams one of whose chunks gave up.
+template <int T, bool PRESET>
+static hipError_t compress_launch(const CacheView& c, const uint16_t* x, int n_new, int64_t x_stride,
+                                  int tok0, uint32_t* ws, hipStream_t s, const PruneOpts& o,
+                                  uint32_t max_polls) {
   const int n_chunks = (n_new + compress_chunk_tokens(T) - 1) / compress_chunk_tokens(T);
   const int64_t n_wg = (int64_t)c.BH * n_chunks;
-  uint64_t* flags = reinterpret_cast<uint64_t*>(ws);
-  uint32_t* ticket = reinterpret_cast<uint32_t*>(flags + n_wg);  // [BH]
-  const int64_t words = 2 * n_wg + c.BH;
-  const int clear_blocks = (int)((words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024);
-  hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, words);
+  const CompressWs w = compress_ws(ws, c.BH, n_chunks);
+  const int clear_blocks = (int)((w.words + 255) / 256 < 1024 ? (w.words + 255) / 256 : 1024);
+  hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, w.words);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_compress<T>, dim3((uint32_t)n_wg), dim3(compress_waves<T>() * kWave),
-                     0, s, x, n_new, c.n_keep,
+  hipLaunchKernelGGL((k_compress<T, PRESET>), dim3((uint32_t)n_wg), dim3(compress_waves<T>() * kWave),
+                     0, s, x, n_new, PRESET ? 0 : c.n_keep,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
-                     flags, ticket, n_chunks, x_stride, o);
+                     w.flags, w.ticket, n_chunks, x_stride, o, max_polls, w.bad, w.status);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_compress_finalize, dim3((c.BH + 255) / 256), dim3(256), 0, s, w.bad, c.stream_len,
+                     c.BH);
   return hipGetLastError();
+}
+
+template <int T>
+static hipError_t compress_T(const CacheView& c, const uint16_t* x, int n_new, int64_t x_stride,
+                             int tok0, uint32_t* ws, hipStream_t s, const PruneOpts& o = PruneOpts{},
+                             uint32_t max_polls = kLookbackPolls) {
+  return compress_launch<T, false>(c, x, n_new, x_stride, tok0, ws, s, o, max_polls);
 }
 
 template <int T>
@@ -1075,12 +1114,12 @@ static hipError_t window_step_T(const CacheView& kc, const CacheView& vc, const 
 }
 
 hipError_t launch_compress(const CacheView& c, const uint16_t* x, int n_new, int tok0, uint32_t* ws,
-                           hipStream_t s, int64_t x_stride) {
+                           hipStream_t s, int64_t x_stride, uint32_t max_polls) {
   if (x_stride <= 0) x_stride = n_new;
   switch (c.T) {
-    case 1: return compress_T<1>(c, x, n_new, x_stride, tok0, ws, s);
-    case 2: return compress_T<2>(c, x, n_new, x_stride, tok0, ws, s);
-    case 4: return compress_T<4>(c, x, n_new, x_stride, tok0, ws, s);
+    case 1: return compress_T<1>(c, x, n_new, x_stride, tok0, ws, s, PruneOpts{}, max_polls);
+    case 2: return compress_T<2>(c, x, n_new, x_stride, tok0, ws, s, PruneOpts{}, max_polls);
+    case 4: return compress_T<4>(c, x, n_new, x_stride, tok0, ws, s, PruneOpts{}, max_polls);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1109,26 +1148,14 @@ hipError_t launch_append_kv(const CacheView& kc, const CacheView& vc, const uint
 // Offsets and packing of tokens whose bitmaps are already in the cache.
 template <int T>
 static hipError_t pack_preset_T(const CacheView& c, const uint16_t* x, int n_new, int64_t x_stride,
-                                int tok0, uint32_t* ws, hipStream_t s) {
-  hipError_t e;
-  const int n_chunks = (n_new + compress_chunk_tokens(T) - 1) / compress_chunk_tokens(T);
-  const int64_t n_wg = (int64_t)c.BH * n_chunks;
-  uint64_t* flags = reinterpret_cast<uint64_t*>(ws);
-  uint32_t* ticket = reinterpret_cast<uint32_t*>(flags + n_wg);  // [BH]
-  const int64_t words = 2 * n_wg + c.BH;
-  const int clear_blocks = (int)((words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024);
-  hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, words);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL((k_compress<T, true>), dim3((uint32_t)n_wg), dim3(compress_waves<T>() * kWave), 0,
-                     s, x, n_new, 0,
-                     c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
-                     flags, ticket, n_chunks, x_stride, PruneOpts{});
-  return hipGetLastError();
+                                int tok0, uint32_t* ws, hipStream_t s, uint32_t max_polls = kLookbackPolls) {
+  return compress_launch<T, true>(c, x, n_new, x_stride, tok0, ws, s, PruneOpts{}, max_polls);
 }
 
 template <int T>
 static hipError_t compress_channel_T(const CacheView& c, const uint16_t* x, int n_new, int tok0,
-                                     uint32_t* ws, hipStream_t s, const float* w, int64_t x_stride) {
+                                     uint32_t* ws, hipStream_t s, const float* w, int64_t x_stride,
+                                     uint32_t max_polls) {
   const int64_t waves = (int64_t)c.BH * (n_new / kGroup);
   const dim3 grid((uint32_t)((waves + 3) / 4));
   if (w != nullptr)
@@ -1137,16 +1164,17 @@ static hipError_t compress_channel_T(const CacheView& c, const uint16_t* x, int 
     hipLaunchKernelGGL((k_select_channel<T, false>), grid, dim3(256), 0, s, c, x, n_new, x_stride, tok0, w);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return pack_preset_T<T>(c, x, n_new, x_stride, tok0, ws, s);
+  return pack_preset_T<T>(c, x, n_new, x_stride, tok0, ws, s, max_polls);
 }
 
 hipError_t launch_compress_channel(const CacheView& c, const uint16_t* x, int n_new, int tok0,
-                                   uint32_t* ws, hipStream_t s, const float* w, int64_t x_stride) {
+                                   uint32_t* ws, hipStream_t s, const float* w, int64_t x_stride,
+                                   uint32_t max_polls) {
   if (x_stride <= 0) x_stride = n_new;
   switch (c.T) {
-    case 1: return compress_channel_T<1>(c, x, n_new, tok0, ws, s, w, x_stride);
-    case 2: return compress_channel_T<2>(c, x, n_new, tok0, ws, s, w, x_stride);
-    case 4: return compress_channel_T<4>(c, x, n_new, tok0, ws, s, w, x_stride);
+    case 1: return compress_channel_T<1>(c, x, n_new, tok0, ws, s, w, x_stride, max_polls);
+    case 2: return compress_channel_T<2>(c, x, n_new, tok0, ws, s, w, x_stride, max_polls);
+    case 4: return compress_channel_T<4>(c, x, n_new, tok0, ws, s, w, x_stride, max_polls);
     default: return hipErrorInvalidValue;
   }
 }
@@ -1259,13 +1287,13 @@ hipError_t launch_window_step(const CacheView& kc, const CacheView& vc, const Wi
   }
 }
 
-hipError_t launch_window_key_weights(const WindowView& w, const uint16_t* q, int G, int T, float* kacc,
-                                     hipStream_t s) {
+hipError_t launch_window_key_weights(const WindowView& w, const uint16_t* q, int G, int T,
+                                     const int32_t* active, float* kacc, hipStream_t s) {
   const dim3 grid((uint32_t)(w.B * w.H));
   switch (T) {
-    case 1: hipLaunchKernelGGL(k_window_key_weights<1>, grid, dim3(256), 0, s, w, q, G, kacc); break;
-    case 2: hipLaunchKernelGGL(k_window_key_weights<2>, grid, dim3(256), 0, s, w, q, G, kacc); break;
-    case 4: hipLaunchKernelGGL(k_window_key_weights<4>, grid, dim3(256), 0, s, w, q, G, kacc); break;
+    case 1: hipLaunchKernelGGL(k_window_key_weights<1>, grid, dim3(256), 0, s, w, q, G, active, kacc); break;
+    case 2: hipLaunchKernelGGL(k_window_key_weights<2>, grid, dim3(256), 0, s, w, q, G, active, kacc); break;
+    case 4: hipLaunchKernelGGL(k_window_key_weights<4>, grid, dim3(256), 0, s, w, q, G, active, kacc); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

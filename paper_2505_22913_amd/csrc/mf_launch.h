@@ -25,12 +25,38 @@ struct CacheView {
   int group_keep;    // per-channel caches: tokens kept per channel and group of 32; else -1
 };
 
+// A stream whose bulk compression gave up waiting in the look-back (see
+// k_compress) has this stream_len; every later call skips it.
+constexpr uint32_t kStreamPoisoned = 0xffffffffu;
+// Look-back polls before a chunk gives up (never reached in practice: the
+// chunks a chunk waits for are already running).
+constexpr uint32_t kLookbackPolls = 1u << 20;
+
+// Workspace of the bulk compression: a u32 status word at byte 0 (nonzero once a
+// stream gave up; 16 bytes reserved), then u64 look-back flags [BH][n_chunks],
+// u32 ticket counters [BH] and u32 give-up marks [BH]. Cleared by each call.
+struct CompressWs {
+  uint32_t* status;
+  uint64_t* flags;
+  uint32_t* ticket;
+  uint32_t* bad;
+  int64_t words;  // 32-bit words to clear from ws
+};
+inline CompressWs compress_ws(uint32_t* ws, int64_t BH, int64_t n_chunks) {
+  CompressWs w;
+  w.status = ws;
+  w.flags = reinterpret_cast<uint64_t*>(ws + 4);
+  w.ticket = reinterpret_cast<uint32_t*>(w.flags + BH * n_chunks);
+  w.bad = w.ticket + BH;
+  w.words = 4 + 2 * BH * n_chunks + 2 * BH;
+  return w;
+}
+
 // Compress n_new tokens per stream (x: [BH][x_stride][64T] fp16, x_stride = n_new
-// when 0) after tok0 tokens.
-// ws: u64 look-back flags [BH][n_chunks] followed by a u32 ticket counter; it is
-// cleared by the call itself.
+// when 0) after tok0 tokens, with the workspace above; a chunk's look-back gives
+// up after max_polls polls.
 hipError_t launch_compress(const CacheView& c, const uint16_t* x, int n_new, int tok0, uint32_t* ws,
-                           hipStream_t s, int64_t x_stride = 0);
+                           hipStream_t s, int64_t x_stride = 0, uint32_t max_polls = kLookbackPolls);
 // Compress one token per stream (x: [BH][64T]) as token tok0.
 hipError_t launch_append(const CacheView& c, const uint16_t* x, int tok0, hipStream_t s);
 // launch_append of the keys and the values of one step in one launch (same shapes).
@@ -60,7 +86,8 @@ hipError_t launch_append_variant(const CacheView& c, const uint16_t* x, int tok0
 // preset mode. w: NULL (magnitude) or fp32 token weights [BH][n_new].
 constexpr int kGroup = 32;
 hipError_t launch_compress_channel(const CacheView& c, const uint16_t* x, int n_new, int tok0,
-                                   uint32_t* ws, hipStream_t s, const float* w, int64_t x_stride = 0);
+                                   uint32_t* ws, hipStream_t s, const float* w, int64_t x_stride = 0,
+                                   uint32_t max_polls = kLookbackPolls);
 // Output-aware weights: w[b][h][T][c] = sum over t = T .. min(T+L, Nq)-1, then over
 // the G query heads of h, of |q[b][h*G+g][t][c]| (fp32, in that order).
 hipError_t launch_query_lookahead(const uint16_t* q, int B, int Hq, int Hkv, int n_q, int T, int L,
@@ -84,9 +111,10 @@ hipError_t launch_window_fill(const WindowView& w, int b, int d, const uint16_t*
 hipError_t launch_window_step(const CacheView& kc, const CacheView& vc, const WindowView& w,
                               const uint16_t* k_new, const uint16_t* v_new, const int32_t* active,
                               hipStream_t s, float* kacc = nullptr);
-// kacc[bh][slot] += |q| of the G query heads of bh, for the newest 32 window tokens.
-hipError_t launch_window_key_weights(const WindowView& w, const uint16_t* q, int G, int T, float* kacc,
-                                     hipStream_t s);
+// kacc[bh][slot] += |q| of the G query heads of bh, for the newest 32 window tokens
+// of every active entry (active: int32 [B] or null for all).
+hipError_t launch_window_key_weights(const WindowView& w, const uint16_t* q, int G, int T,
+                                     const int32_t* active, float* kacc, hipStream_t s);
 // Grouped lifecycle step (see mustafar_window_step_grouped): kc per token, vc
 // per channel; acc: fp32 [B][H][W] scores or NULL (magnitude).
 hipError_t launch_window_step_grouped(const CacheView& kc, const CacheView& vc, const WindowView& w,
@@ -94,14 +122,17 @@ hipError_t launch_window_step_grouped(const CacheView& kc, const CacheView& vc, 
                                       const int32_t* active, float* acc, hipStream_t s);
 // Scores of the window tokens younger than 32 steps: acc[b][h][slot] += sum over
 // the G query heads of h of exp2(scale_log2 * q.k - lse2[b][hq]) (lse2: the
-// log2-domain log-sum-exp the merge wrote).
+// log2-domain log-sum-exp the merge wrote), for the active entries (active:
+// int32 [B] or null for all).
 hipError_t launch_window_scores(const WindowView& w, const uint16_t* q, int G, int T,
-                                float scale_log2, const float* lse2, float* acc, hipStream_t s);
+                                float scale_log2, const float* lse2, const int32_t* active, float* acc,
+                                hipStream_t s);
 
 struct SparseSide {
   const uint64_t* bitmaps;
   const uint32_t* offsets;
   const uint16_t* values;
+  const uint32_t* stream_len;  // a poisoned stream is read as empty
   int64_t val_stride;
   int cap_tokens;
   int n_keep;

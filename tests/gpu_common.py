@@ -13,8 +13,20 @@ ATTN_TOL = 2e-3
 
 
 def announce(msg: str) -> None:
-    sys.__stderr__.write(f"[gpu-case] {msg}\n")
+    """Names the case (and, after it, what it measured) on stderr and, when
+    MUSTAFAR_CASE_LOG names a file, appended there: pytest's capture holds back
+    a passing test's stderr, and a process that a GPU failure ends loses it."""
+    line = f"[gpu-case] {msg}\n"
+    sys.__stderr__.write(line)
     sys.__stderr__.flush()
+    path = os.environ.get("MUSTAFAR_CASE_LOG")
+    if path:
+        fd = os.open(path, os.O_WRONLY | os.O_APPEND | os.O_CREAT, 0o644)
+        try:
+            os.write(fd, line.encode())
+            os.fsync(fd)
+        finally:
+            os.close(fd)
 
 
 def have_lib() -> bool:

@@ -118,9 +118,15 @@ def test_ccache_init_validates(lib):
 def test_compress_and_append_reject_before_launch(lib):
     c, _ = _fake_cache(B=2, H=4, cap=100)
     ws_need = lib.mustafar_compress_workspace_bytes(2, 4, 50)
-    # per stream: one 8-byte scan flag per 64-token chunk and a 4-byte ticket counter
-    assert ws_need == 2 * 4 * (1 * 8 + 4) + 16
-    assert lib.mustafar_compress_workspace_bytes(1, 1, 65) == 2 * 8 + 4 + 16
+    # a 16-byte status word, then per stream one 8-byte scan flag per 64-token chunk,
+    # a 4-byte ticket counter and a 4-byte give-up mark
+    assert ws_need == 16 + 2 * 4 * (1 * 8 + 4 + 4)
+    assert lib.mustafar_compress_workspace_bytes(1, 1, 65) == 16 + 2 * 8 + 4 + 4
+    # the bounded form checks the same arguments
+    assert lib.mustafar_prune_compress_bounded(ctypes.byref(c), x := 0x500000, 50, 0, 0x600000,
+                                               ws_need - 1, None) == mf.EWORKSPACE
+    assert lib.mustafar_prune_compress_bounded(ctypes.byref(c), x, 0, 0, 0x600000, ws_need,
+                                               None) == mf.EINVAL
     x = 0x500000
     assert lib.mustafar_prune_compress(ctypes.byref(c), x, 0, 0x600000, ws_need, None) == mf.EINVAL
     assert lib.mustafar_prune_compress(ctypes.byref(c), x + 2, 50, 0x600000, ws_need,
@@ -320,9 +326,10 @@ def test_window_calls_reject_before_launch(lib):
     w16, _ = _fake_window(W=16)
     assert wstep(w=w16) == mf.EINVAL                 # a key must see 32 steps in the window
     kw_ = lambda **kw: lib.mustafar_window_key_weights(  # noqa: E731
-        kw.get("q", 0x700000), kw.get("B", 2), kw.get("Hq", 8), ctypes.byref(w), kw.get("kacc", kacc),
-        None)
+        kw.get("q", 0x700000), kw.get("B", 2), kw.get("Hq", 8), ctypes.byref(w), kw.get("act", None),
+        kw.get("kacc", kacc), None)
     assert kw_(B=3) == mf.EINVAL
+    assert kw_(act=0x900002) == mf.EINVAL            # misaligned activity mask
     assert kw_(Hq=6) == mf.EINVAL                    # not a multiple of H
     assert kw_(Hq=64) == mf.EUNSUPPORTED             # 16 query heads per kv-head
     assert kw_(q=0x700002) == mf.EINVAL
@@ -431,7 +438,8 @@ def test_grouped_calls_reject_before_launch(lib):
     K.n_tokens = V.n_tokens = 32
     anb = lib.mustafar_attn_workspace_bytes(2, 8, 4, 128, 32, 0)
     att = lambda **kw: lib.mustafar_window_decode_attn_scores(  # noqa: E731
-        0x700000, 2, 8, ctypes.byref(K), ctypes.byref(V), ctypes.byref(w), kw.get("acc", acc), 0.0,
-        0x800000, 0, 0xb00000, kw.get("ws_bytes", anb), None)
+        0x700000, 2, 8, ctypes.byref(K), ctypes.byref(V), ctypes.byref(w), kw.get("act", None),
+        kw.get("acc", acc), 0.0, 0x800000, 0, 0xb00000, kw.get("ws_bytes", anb), None)
     assert att(ws_bytes=anb - 4) == mf.EWORKSPACE
+    assert att(act=0x900001) == mf.EINVAL            # misaligned activity mask
     assert att(acc=acc + 1) == mf.EINVAL

@@ -166,8 +166,12 @@ def test_window_lifecycle_output_aware_keys(W, G, d):
         if s % 10 == 9 or s == steps - 1:
             _check_state(o, win, Kc, Vc, B, H, W)
             _check_attention(o, win, Kc, Vc, q, B, G, f"output-aware keys W={W} G={G} step {s + 1}")
-        mf.mustafar_window_key_weights(q, win, kacc)
-        o.accumulate_key_weights(q.cpu().numpy())
+        before = kacc.clone() if not act.all() else None
+        mf.mustafar_window_key_weights(q, win, kacc, active=torch.from_numpy(act).cuda())
+        o.accumulate_key_weights(q.cpu().numpy(), act)
+        if before is not None:   # an entry that sits the step out gathers nothing
+            idle = torch.from_numpy(act == 0).cuda()
+            assert torch.equal(kacc[idle], before[idle]), s
         if s % 10 == 9 or s == steps - 1:
             torch.cuda.synchronize()
             a = kacc.cpu().numpy()

@@ -5,7 +5,8 @@
 * output-aware key pruning (Sec. 2): numpy's float32 products and stable sort,
   unit weights reduce it to magnitude pruning, power-of-two scalings and
   channel permutations act as they must;
-* per-head kept counts (finer-grained sparsity, Sec. 4.5): every head keeps its
+* per-head kept counts (finer-grained sparsity, future work in Conclusion and
+  Limitations): every head keeps its
   own count, and equals the magnitude compressor run on that head alone;
 * the query lookahead weights: closed forms for constant queries.
 """

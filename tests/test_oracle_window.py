@@ -115,8 +115,12 @@ def _output_aware_run(W, S, G, inactive=()):
         if act[0]:
             keys.append(k[0])
         q = rng.standard_normal((B, H * G, d)).astype(np.float16)
-        o.accumulate_key_weights(q)
-        qs.append(q[0])
+        before = {j: o.key_weights(0, j).copy() for j in range(o.arrived(0))}
+        o.accumulate_key_weights(q, act)
+        if act[0]:
+            qs.append(q[0])
+        else:   # a step the entry sits out leaves every weight as it was
+            assert all(np.array_equal(o.key_weights(0, j), w) for j, w in before.items())
     return o, np.stack(keys, axis=1)[None], np.stack(qs, axis=1)[None]
 
 
@@ -165,7 +169,7 @@ def test_output_aware_key_pins_reject_planted_mistakes(monkeypatch):
     assert not weights_match()
     monkeypatch.undo()
 
-    def reversed_heads(self, q):
+    def reversed_heads(self, q, active=None):
         qa = np.abs(np.asarray(q).view(np.float16).astype(np.float32))
         G = qa.shape[1] // self.H
         for b in range(self.B):
@@ -180,27 +184,28 @@ def test_output_aware_key_pins_reject_planted_mistakes(monkeypatch):
     assert not weights_match()
 
 
-def test_output_aware_keys_of_a_paused_entry_gather_every_query():
-    """While an entry receives no tokens its newest window tokens keep adding the
-    queries of every step: a token's weights are the sum over the steps in which it
-    was among the newest 32 window tokens."""
-    W, S, G = 32, 60, 1
-    pause = set(range(10, 15))
+@pytest.mark.parametrize("G", [1, 2])
+def test_output_aware_keys_of_a_paused_entry_gather_only_its_own_queries(G):
+    """An entry that sits steps out gathers no query in them: a key that leaves
+    carries exactly the lookahead weights (L = 32, bit for bit) of the entry's own
+    query sequence -- the queries of the steps it was active in -- from the step
+    the key arrived in; the prompt token the 31 first ones. Its caches equal the
+    output-aware compression with those weights."""
+    W, S, H, d = 32, 90, 2, 64
+    pause = set(range(10, 15)) | {40, 41, 60}
     o, K, Q = _output_aware_run(W, S, G, inactive=pause)
-    # token j arrived in step a_j; it stays among the newest 32 until 32 newer
-    # tokens have arrived
-    arrive = [-1]
-    for s in range(S):
-        if s not in pause:
-            arrive.append(s)
-    qa = np.abs(Q[0].astype(np.float32))        # [Hq][S][d]
-    for j in range(o.n_comp(0)):
-        first = max(arrive[j], 0)
-        last = arrive[j + 32] if j + 32 < len(arrive) else S    # the step the 32nd newer token came
-        w = np.zeros((2, 64), dtype=np.float32)
-        for s in range(first, last):
-            w = w + qa[:, s]
-        assert np.array_equal(o.key_weights(0, j), w), j
+    n = o.n_comp(0)
+    assert n == S - len(pause) + 1 - W
+    look = oracle.query_lookahead(Q, H, 32)           # over the entry's own queries
+    want_w = np.stack([oracle.query_lookahead(Q, H, 31)[0, :, 0]] +
+                      [look[0, :, j - 1] for j in range(1, n)], axis=1)
+    for j in range(n):
+        assert np.array_equal(o.key_weights(0, j), want_w[:, j]), j
+    want = oracle.compress_variant(K[:, :, :n], "output_aware", k=oracle.keep_count(d, 0.5),
+                                   weights=want_w[None])
+    got, _ = o.compressed(0)
+    for key in ("bitmaps", "offsets", "stream_len"):
+        assert np.array_equal(got[key], want[key]), key
 
 
 # ---- the grouped lifecycle (per-channel value pruning in groups of 32) -------------------
