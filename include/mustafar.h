@@ -66,7 +66,8 @@ enum mustafar_status {
     MUSTAFAR_ECAPACITY = -2,   /* cache has no room for the tokens              */
     MUSTAFAR_EWORKSPACE = -3,  /* workspace missing or smaller than required    */
     MUSTAFAR_ELAUNCH = -4,     /* the HIP runtime rejected a launch             */
-    MUSTAFAR_EUNSUPPORTED = -5 /* valid but unsupported shape (d, group size)   */
+    MUSTAFAR_EUNSUPPORTED = -5, /* valid but unsupported shape (d, group size)  */
+    MUSTAFAR_ESCRATCH = -6      /* needs more than the static scratch buffer    */
 };
 
 /* Descriptor of one compressed cache. Pointers are device memory owned by the
@@ -299,6 +300,26 @@ int mustafar_sparse_decode_attn(const void* q, int B, int Hq, const mustafar_cca
                                 const mustafar_ccache_t* Vc, const void* k_tail,
                                 const void* v_tail, int n_tail, float scale, void* out,
                                 int n_splits, void* ws, size_t ws_bytes, void* stream);
+
+/* FOR CALLERS THAT CANNOT ALLOCATE (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): mustafar_sparse_decode_attn without a
+ * workspace argument. Its split-K partials go to a static device buffer of
+ * MUSTAFAR_STATIC_SCRATCH_BYTES that the library holds on every GPU it runs
+ * on until the process ends; the call allocates nothing itself (no hipMalloc,
+ * hipFree or allocating library routine). The first call on a device looks up
+ * that device's buffer (the current device, which `stream` must belong to).
+ * Every call on a GPU shares the one buffer, so calls that overlap on one GPU
+ * race: issue them on one stream, or order them. The buffer needs no clearing
+ * (every call writes each partial it reads). Same arguments and result as
+ * mustafar_sparse_decode_attn (the same kernels), bit for bit for the same
+ * n_splits. Errors as mustafar_sparse_decode_attn, plus ESCRATCH when the
+ * partials (mustafar_attn_workspace_bytes for the call's sizes and split
+ * count) exceed the buffer; an invalid call launches nothing. */
+#define MUSTAFAR_STATIC_SCRATCH_BYTES (32u << 20)
+int mustafar_sparse_decode_attn_static(const void* q, int B, int Hq, const mustafar_ccache_t* Kc,
+                                       const mustafar_ccache_t* Vc, const void* k_tail,
+                                       const void* v_tail, int n_tail, float scale, void* out,
+                                       int n_splits, void* stream);
 
 /* The same attention over dense fp16 caches k, v [B][Hkv][n_tokens][d]: the
  * in-house dense baseline the sparse path is measured against (the paper

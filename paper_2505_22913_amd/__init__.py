@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(_HERE, "libmustafar.so")
 TILE = 64
 PAD = 8
 
-OK, EINVAL, ECAPACITY, EWORKSPACE, ELAUNCH, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+OK, EINVAL, ECAPACITY, EWORKSPACE, ELAUNCH, EUNSUPPORTED, ESCRATCH = 0, -1, -2, -3, -4, -5, -6
+STATIC_SCRATCH_BYTES = 32 << 20   # the static buffer of mustafar_sparse_decode_attn_static
 STREAM_POISONED = 0xFFFFFFFF   # stream_len of a stream whose bulk compression gave up
 LOOKBACK_POLLS = 1 << 20
 
@@ -94,6 +95,12 @@ _SIGS = {
                                                    ctypes.c_void_p, ctypes.c_int, ctypes.c_float,
                                                    ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                                    ctypes.c_size_t, ctypes.c_void_p]),
+    "mustafar_sparse_decode_attn_static": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                                          ctypes.POINTER(ccache_t),
+                                                          ctypes.POINTER(ccache_t), ctypes.c_void_p,
+                                                          ctypes.c_void_p, ctypes.c_int, ctypes.c_float,
+                                                          ctypes.c_void_p, ctypes.c_int,
+                                                          ctypes.c_void_p]),
     "mustafar_dense_decode_attn": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
                                                   ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
                                                   ctypes.c_int, ctypes.c_int, ctypes.c_float,
@@ -389,6 +396,22 @@ def mustafar_sparse_decode_attn(q, Kc: CompressedCache, Vc: CompressedCache, k_t
         _dptr(q), B, Hq, ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), _dptr(k_tail),
         _dptr(v_tail), n_tail, float(scale), _dptr(out), int(n_splits), _dptr(ws),
         ws.numel() * ws.element_size(), _stream(stream)))
+    return out
+
+
+def mustafar_sparse_decode_attn_static(q, Kc: CompressedCache, Vc: CompressedCache, k_tail=None,
+                                       v_tail=None, scale: float = 0.0, out=None, n_splits: int = 0,
+                                       stream=None):
+    """mustafar_sparse_decode_attn with its partials in the library's static device
+    buffer (no workspace; for callers that cannot allocate). out may be preallocated."""
+    import torch
+    B, Hq, d = (int(s) for s in q.shape)
+    n_tail = 0 if k_tail is None else int(k_tail.shape[2])
+    if out is None:
+        out = torch.empty((B, Hq, d), dtype=torch.float16, device=q.device)
+    _check("mustafar_sparse_decode_attn_static", lib().mustafar_sparse_decode_attn_static(
+        _dptr(q), B, Hq, ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), _dptr(k_tail), _dptr(v_tail),
+        n_tail, float(scale), _dptr(out), int(n_splits), _stream(stream)))
     return out
 
 

@@ -4,8 +4,18 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "mf_launch.h"
 #include "mustafar.h"
+
+// Static device scratch of mustafar_sparse_decode_attn_static: the split-K
+// partials of a decode call live here instead of in a caller workspace. Each
+// GPU the library runs on holds its own copy until the process ends. In host
+// code `scratch` is only a stand-in for the symbol: its device address comes
+// from hipGetSymbolAddress (once per device, below) and only that address is
+// ever passed to a kernel.
+static __device__ __align__(256) unsigned char scratch[MUSTAFAR_STATIC_SCRATCH_BYTES];
 
 namespace {
 
@@ -30,6 +40,26 @@ bool aligned(const void* p, uintptr_t a) { return p && ((uintptr_t)p % a) == 0; 
 bool head_dim_ok(int d) { return d == 64 || d == 128 || d == 256; }
 
 int status_of(hipError_t e) { return e == hipSuccess ? MUSTAFAR_OK : MUSTAFAR_ELAUNCH; }
+
+// Device address of `scratch` on the current device, looked up at the first call
+// on that device and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_of_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return MUSTAFAR_ELAUNCH;
+  if (dev < 0 || dev >= kMaxDevices) return MUSTAFAR_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return MUSTAFAR_ELAUNCH;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MUSTAFAR_OK;
+}
 
 int check_cache(const mustafar_ccache_t* c) {
   if (!c) return MUSTAFAR_EINVAL;
@@ -482,6 +512,33 @@ int mustafar_sparse_decode_attn(const void* q, int B, int Hq, const mustafar_cca
                                         ws_o, (uint16_t*)out, (hipStream_t)stream));
 }
 
+int mustafar_sparse_decode_attn_static(const void* q, int B, int Hq, const mustafar_ccache_t* Kc,
+                                       const mustafar_ccache_t* Vc, const void* k_tail,
+                                       const void* v_tail, int n_tail, float scale, void* out,
+                                       int n_splits, void* stream) {
+  // Every argument is checked on the host first (no GPU call before that).
+  int st = check_cache(Kc);
+  if (st != MUSTAFAR_OK) return st;
+  if ((st = check_cache(Vc)) != MUSTAFAR_OK) return st;
+  if (Kc->B != B || Vc->B != B || Kc->H != Vc->H || Kc->d != Vc->d || Kc->n_tokens != Vc->n_tokens)
+    return MUSTAFAR_EINVAL;
+  if (n_tail < 0) return MUSTAFAR_EINVAL;
+  if (n_tail > 0 && (!aligned(k_tail, 16) || !aligned(v_tail, 16))) return MUSTAFAR_EINVAL;
+  if (B < 1 || Hq < 1 || Hq % Kc->H != 0) return MUSTAFAR_EINVAL;
+  const int G = Hq / Kc->H;
+  if (G != 1 && G != 2 && G != 4 && G != 8) return MUSTAFAR_EUNSUPPORTED;
+  const int n_main = Kc->n_tokens;
+  if (n_splits <= 0)
+    n_splits = mustafar_attn_default_splits(B, Hq, Kc->H, n_main > 0 ? n_main : 1, MUSTAFAR_ATTN_SPARSE);
+  if (n_splits > (1 << 20)) return MUSTAFAR_EINVAL;
+  const size_t need = mustafar_attn_workspace_bytes(B, Hq, Kc->H, Kc->d, n_main, n_splits);
+  if (need > (size_t)MUSTAFAR_STATIC_SCRATCH_BYTES) return MUSTAFAR_ESCRATCH;
+  void* ws = nullptr;
+  if ((st = scratch_of_current_device(&ws)) != MUSTAFAR_OK) return st;
+  return mustafar_sparse_decode_attn(q, B, Hq, Kc, Vc, k_tail, v_tail, n_tail, scale, out, n_splits, ws,
+                                     (size_t)MUSTAFAR_STATIC_SCRATCH_BYTES, stream);
+}
+
 int mustafar_dense_decode_attn(const void* q, int B, int Hq, int Hkv, const void* k,
                                const void* v, int n_tokens, int d, float scale, void* out,
                                int n_splits, void* ws, size_t ws_bytes, void* stream) {
@@ -715,6 +772,9 @@ const char* mustafar_strerror(int status) {
     case MUSTAFAR_EWORKSPACE: return "workspace missing, misaligned or too small";
     case MUSTAFAR_ELAUNCH: return "the HIP runtime rejected a kernel launch";
     case MUSTAFAR_EUNSUPPORTED: return "unsupported shape (head dim or query group size)";
+    case MUSTAFAR_ESCRATCH:
+      return "the call needs more than the library's static scratch buffer "
+             "(MUSTAFAR_STATIC_SCRATCH_BYTES per GPU): use the workspace form";
     default: return "unknown status";
   }
 }

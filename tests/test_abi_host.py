@@ -443,3 +443,26 @@ def test_grouped_calls_reject_before_launch(lib):
     assert att(ws_bytes=anb - 4) == mf.EWORKSPACE
     assert att(act=0x900001) == mf.EINVAL            # misaligned activity mask
     assert att(acc=acc + 1) == mf.EINVAL
+
+
+def test_static_scratch_decode_rejects_before_touching_the_gpu(lib):
+    """mustafar_sparse_decode_attn_static checks every argument, and that the call's
+    partials fit the static buffer, before its first HIP call."""
+    K, _ = _fake_cache(B=2, H=4, cap=100)
+    V, _ = _fake_cache(B=2, H=4, cap=100, s=0.7)
+    K.n_tokens = V.n_tokens = 100
+    call = lambda **kw: lib.mustafar_sparse_decode_attn_static(  # noqa: E731
+        0x700000, kw.get("B", 2), kw.get("Hq", 16), ctypes.byref(K), ctypes.byref(kw.get("V", V)),
+        kw.get("kt", 0x900000), 0x980000, kw.get("nt", 32), 0.0, 0x800000, kw.get("splits", 0), None)
+    assert call(B=3) == mf.EINVAL
+    assert call(Hq=12) == mf.EUNSUPPORTED                    # three query heads per kv-head
+    assert call(Hq=6) == mf.EINVAL                           # not a multiple of the kv-heads
+    assert call(kt=0x900002) == mf.EINVAL                    # misaligned window
+    assert call(nt=-1) == mf.EINVAL
+    V.n_tokens = 99
+    assert call() == mf.EINVAL                               # K and V differ in length
+    V.n_tokens = 100
+    need = lib.mustafar_attn_workspace_bytes(2, 16, 4, 128, 100, 1 << 16)
+    assert need > mf.STATIC_SCRATCH_BYTES
+    assert call(splits=1 << 16) == mf.ESCRATCH
+    assert "static scratch" in mf.strerror(mf.ESCRATCH)
