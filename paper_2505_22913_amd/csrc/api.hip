@@ -126,15 +126,19 @@ bool window_matches(const mustafar_window_t* w, const mustafar_ccache_t* c) {
   return c->B == w->B && c->H == w->H && c->d == w->d;
 }
 
-int round_up(int x, int a) { return (x + a - 1) / a * a; }
+// Token counts of a decode call are at most kMaxTokens, so the segment
+// arithmetic below stays inside int (it is carried out in 64 bits).
+constexpr int kMaxTokens = 1 << 30;
+
+int round_up(int64_t x, int64_t a) { return (int)((x + a - 1) / a * a); }
 
 // Segment size (tokens, multiple of 64) for n tokens split n_splits ways.
 int seg_tokens(int n, int n_splits) {
   if (n <= 0) return kSegAlign;
-  return round_up((n + n_splits - 1) / n_splits, kSegAlign);
+  return round_up(((int64_t)n + n_splits - 1) / n_splits, kSegAlign);
 }
 
-int n_segments(int n, int seg) { return n <= 0 ? 0 : (n + seg - 1) / seg; }
+int n_segments(int n, int seg) { return n <= 0 ? 0 : (int)(((int64_t)n + seg - 1) / seg); }
 
 float scale_log2_of(float scale, int d) {
   const double s = scale > 0.f ? (double)scale : 1.0 / sqrt((double)d);
@@ -294,7 +298,8 @@ int mustafar_ccache_init_grouped(mustafar_ccache_t* c, void* bitmaps, void* offs
 
 size_t mustafar_compress_workspace_bytes(int B, int H, int n_new) {
   if (B < 1 || H < 1 || n_new < 1) return 0;
-  const int64_t n_chunks = (n_new + mf::kMinCompressChunk - 1) / mf::kMinCompressChunk;
+  if ((int64_t)B * H > kMaxGrid) return 0;  // no compression call accepts more streams
+  const int64_t n_chunks = ((int64_t)n_new + mf::kMinCompressChunk - 1) / mf::kMinCompressChunk;
   // the status word (16 bytes), then per stream a look-back flag per chunk, a
   // ticket counter and a give-up mark
   return (size_t)(16 + (int64_t)B * H * (n_chunks * (int64_t)sizeof(uint64_t) + 2 * (int64_t)sizeof(uint32_t)));
@@ -424,7 +429,7 @@ int mustafar_attn_default_splits(int B, int Hq, int Hkv, int n_tokens, int kind)
   const int min_seg = grouped_q ? kGroupedMinSegTokens : kWalkMinSegTokens;
   const int64_t streams = (int64_t)B * Hkv;
   int64_t want = (target + streams - 1) / streams;
-  const int64_t most = (n_tokens + min_seg - 1) / min_seg;
+  const int64_t most = ((int64_t)n_tokens + min_seg - 1) / min_seg;
   if (want > most) want = most;
   if (want < 1) want = 1;
   return (int)want;
@@ -432,6 +437,8 @@ int mustafar_attn_default_splits(int B, int Hq, int Hkv, int n_tokens, int kind)
 
 size_t mustafar_attn_workspace_bytes(int B, int Hq, int Hkv, int d, int n_tokens, int n_splits) {
   if (B < 1 || Hq < 1 || Hkv < 1 || d < 1 || n_tokens < 0) return 0;
+  // no decode call accepts more streams, query heads per kv-head, head size or splits
+  if ((int64_t)B * Hkv > kMaxGrid || Hq > (int64_t)8 * Hkv || d > 256 || n_splits > (1 << 20)) return 0;
   if (n_splits <= 0) {
     const int sp = mustafar_attn_default_splits(B, Hq, Hkv, n_tokens, MUSTAFAR_ATTN_SPARSE);
     const int dn = mustafar_attn_default_splits(B, Hq, Hkv, n_tokens, MUSTAFAR_ATTN_DENSE);
@@ -454,6 +461,7 @@ static int decode_common(const void* q, int B, int Hq, int Hkv, int d, int n_s, 
   if ((int64_t)B * Hkv > kMaxGrid) return MUSTAFAR_EINVAL;
   if (!head_dim_ok(d)) return MUSTAFAR_EINVAL;
   if (n_s < 0 || n_dense < 0 || (int64_t)n_s + n_dense < 1) return MUSTAFAR_EINVAL;
+  if (n_s > kMaxTokens || n_dense > kMaxTokens) return MUSTAFAR_EINVAL;
   if (!aligned(q, 16) || !aligned(out, 16)) return MUSTAFAR_EINVAL;
   const int G = Hq / Hkv;
   if (G != 1 && G != 2 && G != 4 && G != 8) return MUSTAFAR_EUNSUPPORTED;
