@@ -268,9 +268,11 @@ enum mustafar_attn_kind {
 /* Split-K segment count a decode call of the given kind picks when it is
  * passed n_splits <= 0, for B*Hkv streams of n_tokens tokens (the compressed
  * tokens for the sparse calls). It depends on the kernel that runs: with one
- * query head per kv-head, many segments down to one 64-token block; with
- * grouped queries, about 2048 (sparse) or 4096 (dense) workgroups of at least
- * 128 tokens. Returns 1 for invalid arguments or kind. */
+ * query head per kv-head, many segments down to one 64-token block; with 2 or
+ * 4 query heads per kv-head (the same bit walks), about 4096 workgroups of at
+ * least 256 tokens; with 8 (the matrix-core kernel), about 2048 of at least
+ * 128; the dense kernel with grouped queries about 4096 of at least 128.
+ * Returns 1 for invalid arguments or kind. */
 int mustafar_attn_default_splits(int B, int Hq, int Hkv, int n_tokens, int kind);
 
 /* Device workspace for the decode-attention calls: fp32 partial results

@@ -28,6 +28,9 @@ constexpr int kMaxGrid = 65535;            // grid.y limit for the stream index
 // the grouped-query kernels want fewer, longer segments.
 constexpr int kWalkTargetGroups = 32768;
 constexpr int kWalkMinSegTokens = 64;
+constexpr int kWalkGroupedTargetGroups = 4096;  // the walks with 2 or 4 query heads per kv-head,
+constexpr int kWalkGroupedMinSegTokens = 256;   // segments of at least 256 tokens
+constexpr int kMfmaMinGroup = 8;                // the matrix-core kernel from 8 on (attn_common.h)
 constexpr int kMfmaTargetGroups = 2048;
 constexpr int kDenseGroupedTargetGroups = 4096;
 constexpr int kGroupedMinSegTokens = 128;
@@ -425,8 +428,11 @@ int mustafar_attn_default_splits(int B, int Hq, int Hkv, int n_tokens, int kind)
   const bool grouped_q = Hq / Hkv >= 2;
   const int64_t target = !grouped_q ? kWalkTargetGroups
                          : kind == MUSTAFAR_ATTN_DENSE ? kDenseGroupedTargetGroups
-                                                       : kMfmaTargetGroups;
-  const int min_seg = grouped_q ? kGroupedMinSegTokens : kWalkMinSegTokens;
+                         : Hq / Hkv >= kMfmaMinGroup   ? kMfmaTargetGroups
+                                                       : kWalkGroupedTargetGroups;
+  const int min_seg = !grouped_q ? kWalkMinSegTokens
+                      : (kind == MUSTAFAR_ATTN_SPARSE && Hq / Hkv < kMfmaMinGroup) ? kWalkGroupedMinSegTokens
+                                                                                 : kGroupedMinSegTokens;
   const int64_t streams = (int64_t)B * Hkv;
   int64_t want = (target + streams - 1) / streams;
   const int64_t most = ((int64_t)n_tokens + min_seg - 1) / min_seg;

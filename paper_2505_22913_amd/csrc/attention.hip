@@ -140,12 +140,12 @@ __host__ __device__ constexpr uint32_t qtab_stride(int G) {
 
 __host__ __device__ constexpr uint32_t half_tile_bytes(int) { return kHalfSlots * kPvRow * 4u; }
 
-__host__ __device__ inline SparseLds sparse_lds_layout(int T, int kmaxK, int kmaxV) {
+__host__ __device__ inline SparseLds sparse_lds_layout(int T, int kmaxK, int kmaxV, int G = 1) {
   const int NB = kWave / T;
   SparseLds L;
   uint32_t o = 0;
-  L.qtab = o;  o += (T * qtab_stride(1) + 15u) & ~15u;           // [t][slot] fp16
-  L.ps = o;    o += ((NB / 2) * 4 + 15) & ~15;                   // [j % NBH] half2
+  L.qtab = o;  o += (T * qtab_stride(G) + 15u) & ~15u;           // [t][slot][g] fp16
+  L.ps = o;    o += (G * (NB / 2) * 4 + 15) & ~15;               // [g][j % NBH] half2
   L.vst = o;   o += (run_region_elems(NB * kmaxV) * 2 + 15) & ~15u;
   const uint32_t kst_bytes = (run_region_elems(NB * kmaxK) * 2 + 15) & ~15u;
   L.kst = o;
@@ -367,6 +367,323 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   }
 }
 
+// ------------------------------------------------------------------------------------------
+// Grouped queries on the walks (G = 2, 4, 8 query heads per kv-head). The q
+// table holds the G heads of a channel next to each other (2G bytes per slot),
+// so the key walk gathers them with one load per packed key and adds
+// v x q_g for every head in fp32 (mixed-precision FMA); the scores, the lazy
+// softmax base and the p table are per head. The values are expanded into the
+// channel-major half tile exactly as for one head, and p.V takes one v_dot2 per
+// head and pair of tokens. Same staging and LDS layout as the one-head body,
+// with G-wide q and p tables: no dense key tile, so about half the LDS of the
+// matrix-core kernel per wave.
+// ------------------------------------------------------------------------------------------
+template <int GW>
+struct QSlot;  // the q values of GW heads at one channel
+template <>
+struct QSlot<2> { typedef uint32_t type; };
+template <>
+struct QSlot<4> { typedef u32x2 type; };
+
+template <int GW>
+__device__ __forceinline__ float qslot_head(const typename QSlot<GW>::type& v, int g) {
+  uint32_t w;
+  if constexpr (GW == 2) w = v;
+  else w = v[g >> 1];
+  const half2_t h = as_h2(w);
+  return (float)((g & 1) ? h.y : h.x);
+}
+
+template <int GW>
+struct KeyGroupG {
+  u32x4 w;
+  typename QSlot<GW>::type q[8];
+};
+
+template <int GW, bool PEEL, bool HI>
+__device__ __forceinline__ void keyg_issue(uint32_t& x, uint32_t va, uint32_t qaddr, uint32_t m,
+                                           KeyGroupG<GW>& k) {
+  k.w = group_load<HI>(va);
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const uint32_t c = next_bit<PEEL>(x, u, m);
+    k.q[u] = lds_load<typename QSlot<GW>::type>(qaddr + (2u * GW) * c);
+  }
+}
+
+template <int GW>
+__device__ __forceinline__ void keyg_consume(const KeyGroupG<GW>& k, float (&acc)[GW]) {
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const float v = (float)group_value(k.w, u);
+#pragma unroll
+    for (int g = 0; g < GW; ++g) acc[g] = fmaf(v, qslot_head<GW>(k.q[u], g), acc[g]);
+  }
+}
+
+template <int GW, bool HI>
+__device__ __forceinline__ void keyg_half(int n, uint32_t x, uint32_t a, uint32_t qaddr, uint32_t m,
+                                          float (&acc)[GW]) {
+  if (n == 0) return;
+  KeyGroupG<GW> k0, k1;
+  keyg_issue<GW, HI, HI>(x, a, qaddr, m, k0);
+  int g = 1;
+  for (; g + 1 < n; g += 2) {
+    keyg_issue<GW, false, HI>(x, a + 16u * g, qaddr, 0u, k1);
+    keyg_consume<GW>(k0, acc);
+    keyg_issue<GW, false, HI>(x, a + 16u * (g + 1), qaddr, 0u, k0);
+    keyg_consume<GW>(k1, acc);
+  }
+  if (g < n) {
+    keyg_issue<GW, false, HI>(x, a + 16u * g, qaddr, 0u, k1);
+    keyg_consume<GW>(k0, acc);
+    keyg_consume<GW>(k1, acc);
+  } else {
+    keyg_consume<GW>(k0, acc);
+  }
+}
+
+// Scores of one tile for GW heads (q table of those heads at q_w0 / q_w1;
+// q31 / q63: their q at channels 31 and 63 of the tile, as fp32).
+template <int GW>
+__device__ __forceinline__ void keyg_walk(int nlo, int nhi, uint64_t bm, uint32_t va, uint32_t q_w0,
+                                          uint32_t q_w1, const float (&q31)[GW], const float (&q63)[GW],
+                                          float (&acc)[GW]) {
+  const uint32_t lo = (uint32_t)bm, hi = (uint32_t)(bm >> 32);
+  const uint32_t s = (uint32_t)__popc(lo), c = s + (uint32_t)__popc(hi), m = s & 3u;
+  const float v31 = (float)lds_load<_Float16>(va + 2u * s - 2u);
+  const float v63 = (float)lds_load<_Float16>(va + 2u * c - 2u);
+  keyg_half<GW, false>(nlo, lo & kLow31, va, q_w0, 0u, acc);
+  keyg_half<GW, true>(nhi, hi & kLow31, va + 2u * (s - m), q_w1, m, acc);
+#pragma unroll
+  for (int g = 0; g < GW; ++g) {
+    acc[g] = fmaf((int)lo < 0 ? q31[g] : 0.f, v31, acc[g]);
+    acc[g] = fmaf((int)hi < 0 ? q63[g] : 0.f, v63, acc[g]);
+  }
+}
+
+// Compressed segment, G query heads per kv-head (G >= 2).
+template <int T, int G, int STAGE>
+__device__ __forceinline__ void sparse_body_g(const AttnArgs& a, int seg, int bh, unsigned char* smem,
+                                              float (&m_run)[G], float (&l_run)[G], float (&o)[G][T]) {
+  constexpr int d = kTile * T;
+  constexpr int NB = kWave / T;
+  constexpr int GW = G < 4 ? G : 4;       // heads per key walk (G = 8 walks twice)
+  constexpr uint32_t QS = 2u * GW;        // bytes per q-table slot
+  using PU = PvUnits<T>;
+  const SparseLds L = sparse_lds_layout(T, a.kmaxK, a.kmaxV, G);
+  const uint32_t base = lds_addr(smem);
+  const uint32_t lane = lane_id();
+  const uint32_t j = lane / T, t = lane % T;
+  constexpr uint32_t QTS = qtab_stride(GW);     // bytes per tile of one head group's table
+  constexpr uint32_t QGS = T * QTS;             // bytes per head group
+
+  // q tables [head group][t][slot][GW heads]: slots 0 and 33 and channels 31
+  // and 63 hold zeros (the walks add channels 31 and 63 from their ranks).
+  {
+    const uint16_t* qsrc = a.q + (int64_t)bh * G * d;
+    for (int i = lane; i < G * T * kSlots; i += kWave) {
+      const int gi = i % G, rest = i / G;
+      const int slot = rest % kSlots, tt = rest / kSlots;
+      const int c = slot < 33 ? slot - 1 : slot - 2;
+      const bool zero = slot == 0 || slot == 33 || c == 31 || c == 63;
+      uint16_t* qt = reinterpret_cast<uint16_t*>(smem + L.qtab + (gi / GW) * QGS + tt * QTS + slot * QS);
+      qt[gi % GW] = zero ? (uint16_t)0 : qsrc[(int64_t)gi * d + kTile * tt + c];
+    }
+    if (lane == 0) lds_store<u32x4>(lds_addr(smem) + L.kst - 16u, (u32x4){0u, 0u, 0u, 0u});
+  }
+
+  const int j0 = seg * a.sparse_seg_tokens;
+  const int j1 = min(j0 + a.sparse_seg_tokens, stream_tokens(a, bh));
+  if (j0 >= j1) return;
+  const int64_t kt0 = (int64_t)bh * a.K.cap_tokens * T;
+  const int64_t vt0 = (int64_t)bh * a.V.cap_tokens * T;
+  const uint16_t* kv = a.K.values + (int64_t)bh * a.K.val_stride;
+  const uint16_t* vv = a.V.values + (int64_t)bh * a.V.val_stride;
+
+  int nb = min(NB, j1 - j0);
+  TileMeta cur = load_meta<T>(a, kt0, vt0, j0, nb, lane);
+  Runs rcur = runs_of<T>(cur, nb);
+  u32x4 stg[STAGE];
+  stage_issue<STAGE>(stg, kv, vv, rcur, lane);
+  int nb_next = min(NB, j1 - (j0 + NB));
+  TileMeta nxt = {0ull, 0ull, 0u, 0u};
+  if (nb_next > 0) nxt = load_meta<T>(a, kt0, vt0, j0 + NB, nb_next, lane);
+  stage_commit<STAGE>(stg, base + L.kst, base + L.vst, rcur, lane);
+
+  const uint32_t q_w0 = base + L.qtab + t * QTS + QS;   // slot 1: channel 0 of the tile
+  const uint32_t q_w1 = q_w0 + 33u * QS;
+  float q31[G], q63[G];
+  {
+    const uint16_t* qrow = a.q + (int64_t)bh * G * d + kTile * t;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      q31[g] = half_bits_to_float(qrow[(int64_t)g * d + 31]);
+      q63[g] = half_bits_to_float(qrow[(int64_t)g * d + 63]);
+    }
+  }
+  constexpr uint32_t NBH = PU::NBH;
+  constexpr uint32_t kRowB = kPvRow * 4u;
+  const uint32_t d_w = base + L.dense + kRowB + (t * NBH + j % NBH) * 4u + (j / NBH) * 2u;
+  const uint32_t pv_dw0 = T == 1 ? (lane / 32u) * (NBH / 2) : 0u;
+  uint32_t pv_row[PU::UPL], pv_rot[PU::UPL];
+#pragma unroll
+  for (int k = 0; k < PU::UPL; ++k) {
+    const uint32_t u = T == 1 ? lane % 32u : lane + 64u * k;
+    const uint32_t tu = u % T, c = u / T;
+    pv_row[k] = base + L.dense + ((1u + c) * kPvRow + tu * NBH + pv_dw0) * 4u;
+    pv_rot[k] = c;
+  }
+  constexpr uint32_t PSG = NBH * 4u;   // bytes of one head's p table
+  float oh[G][2][PU::UPL];
+  float l_lane[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    l_lane[g] = 0.f;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int k = 0; k < PU::UPL; ++k) oh[g][hh][k] = 0.f;
+  }
+
+  for (int b0 = j0; b0 < j1; b0 += NB) {
+    const bool has_next = nb_next > 0;
+    Runs rnext = {0u, 0u, 0u, 0u};
+    TileMeta nxt2 = {0ull, 0ull, 0u, 0u};
+    const int nb_next2 = min(NB, j1 - (b0 + 2 * NB));
+    if (has_next) rnext = runs_of<T>(nxt, nb_next);
+    stage_issue<STAGE>(stg, kv, vv, rnext, lane);
+    if (nb_next2 > 0) nxt2 = load_meta<T>(a, kt0, vt0, b0 + 2 * NB, nb_next2, lane);
+
+    // Scores of every head.
+    const WalkCounts wc = walk_counts(cur.kb, cur.vb);
+    float acc[G];
+    {
+      const uint32_t va = base + L.kst + ((int)j < nb ? 2u * (cur.ko - rcur.kstart) : 0u);
+#pragma unroll
+      for (int g0 = 0; g0 < G; g0 += GW) {
+        float ag[GW], a31[GW], a63[GW];
+#pragma unroll
+        for (int g = 0; g < GW; ++g) {
+          ag[g] = 0.f;
+          a31[g] = q31[g0 + g];
+          a63[g] = q63[g0 + g];
+        }
+        keyg_walk<GW>(wc.klo, wc.khi, cur.kb, va, q_w0 + (uint32_t)(g0 / GW) * QGS,
+                      q_w1 + (uint32_t)(g0 / GW) * QGS, a31, a63, ag);
+#pragma unroll
+        for (int g = 0; g < GW; ++g) acc[g0 + g] = ag[g];
+      }
+    }
+    // Online softmax per head with the lazy base of the one-head body; p as fp16
+    // with the exponent bias, the two token halves of the block in one dword.
+    {
+      const bool valid = (int)j < nb;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float sc = valid ? tile_sum<T>(acc[g]) * a.scale_log2 : -INFINITY;
+        if (ballot(sc > m_run[g] + kSlack)) {
+          const float mnew = fmaxf(m_run[g], wave_max_u(sc));
+          const float alpha = __builtin_amdgcn_exp2f(m_run[g] - mnew);
+          l_lane[g] *= alpha;
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+            for (int k = 0; k < PU::UPL; ++k) oh[g][hh][k] *= alpha;
+          m_run[g] = mnew;
+        }
+        const _Float16 ph = valid ? (_Float16)__builtin_amdgcn_exp2f(sc - m_run[g] + kPBias) : (_Float16)0.f;
+        l_lane[g] += t == 0 ? (float)ph : 0.f;
+        if (t == 0) lds_store<_Float16>(base + L.ps + g * PSG + (j % NBH) * 4 + (j / NBH) * 2, ph);
+      }
+    }
+
+    // Values, one half of every tile at a time, as in the one-head body.
+    const uint32_t va = base + L.vst + ((int)j < nb ? 2u * (cur.vo - rcur.vstart) : 0u);
+    const uint32_t vlo = (uint32_t)cur.vb, vhi = (uint32_t)(cur.vb >> 32);
+    const uint32_t vs = (uint32_t)__popc(vlo), vm = vs & 3u;
+    const _Float16 v31 = lds_load<_Float16>(va + 2u * vs - 2u);
+    const _Float16 v63 = lds_load<_Float16>(va + 2u * (vs + (uint32_t)__popc(vhi)) - 2u);
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      {
+        constexpr int n16 = (int)(half_tile_bytes(T) / 16);
+        const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int i = 0; i < (n16 + kWave - 1) / kWave; ++i)
+          if (i * kWave + (int)lane < n16) lds_store<u32x4>(base + L.dense + 16u * (i * kWave + lane), z);
+      }
+      if (hh == 0) {
+        value_half<false, kRowB>(wc.vlo, vlo & kLow31, va, d_w, 0u);
+        lds_store<_Float16>(d_w + kRowB * 31u, (int)vlo < 0 ? v31 : (_Float16)0.f);
+      } else {
+        value_half<true, kRowB>(wc.vhi, vhi & kLow31, va + 2u * (vs - vm), d_w, vm);
+        lds_store<_Float16>(d_w + kRowB * 31u, (int)vhi < 0 ? v63 : (_Float16)0.f);
+      }
+      // p.V for every head: one chunk (eight tokens) of values per unit, then the
+      // same chunk of each head's p.
+#pragma unroll 1
+      for (int q0 = 0; q0 < PU::NQL; ++q0) {
+        u32x4 v4[PU::UPL];
+        uint32_t ch[PU::UPL];
+#pragma unroll
+        for (int k = 0; k < PU::UPL; ++k) {
+          ch[k] = ((uint32_t)q0 + pv_rot[k]) % (uint32_t)PU::NQL;
+          v4[k] = lds_load<u32x4>(pv_row[k] + 16u * ch[k]);
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+          for (int k = 0; k < PU::UPL; ++k) {
+            const u32x4 p4 = lds_load<u32x4>(base + L.ps + g * PSG + (pv_dw0 + 4u * ch[k]) * 4u);
+            float r = oh[g][hh][k];
+            r = __builtin_amdgcn_fdot2(as_h2(v4[k].x), as_h2(p4.x), r, false);
+            r = __builtin_amdgcn_fdot2(as_h2(v4[k].y), as_h2(p4.y), r, false);
+            r = __builtin_amdgcn_fdot2(as_h2(v4[k].z), as_h2(p4.z), r, false);
+            r = __builtin_amdgcn_fdot2(as_h2(v4[k].w), as_h2(p4.w), r, false);
+            oh[g][hh][k] = r;
+          }
+      }
+    }
+
+    if (has_next) {
+      stage_commit<STAGE>(stg, base + L.kst, base + L.vst, rnext, lane);
+      cur = nxt;
+      rcur = rnext;
+      nxt = nxt2;
+    }
+    nb = nb_next;
+    nb_next = nb_next2;
+  }
+
+  const bool upper = lane >= 32u;
+  const int c = (int)(lane % 32u);
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    l_run[g] = wave_sum_u(l_lane[g]);
+    m_run[g] -= kPBias;
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) {
+      if constexpr (T == 1) {
+        const float a0 = __shfl(oh[g][0][0], c, kWave) + __shfl(oh[g][0][0], c + 32, kWave);
+        const float a1 = __shfl(oh[g][1][0], c, kWave) + __shfl(oh[g][1][0], c + 32, kWave);
+        o[g][tt] = upper ? a1 : a0;
+      } else if constexpr (T == 2) {
+        const int src = c * 2 + tt;
+        const float a0 = __shfl(oh[g][0][0], src, kWave);
+        const float a1 = __shfl(oh[g][1][0], src, kWave);
+        o[g][tt] = upper ? a1 : a0;
+      } else {
+        const int u = c * T + tt, src = u % 64;
+        const bool k1 = u >= 64;
+        const float a00 = __shfl(oh[g][0][0], src, kWave), a01 = __shfl(oh[g][0][1], src, kWave);
+        const float a10 = __shfl(oh[g][1][0], src, kWave), a11 = __shfl(oh[g][1][1], src, kWave);
+        o[g][tt] = upper ? (k1 ? a11 : a10) : (k1 ? a01 : a00);
+      }
+    }
+  }
+}
+
 // Sparse call: grid (n_sparse_segs + n_dense_segs, BHkv); compressed segments first.
 template <int T, int G, int STAGE>
 __global__ __launch_bounds__(64) void k_sparse_attn(AttnArgs a) {
@@ -374,11 +691,9 @@ __global__ __launch_bounds__(64) void k_sparse_attn(AttnArgs a) {
   const int seg = blockIdx.x, bh = blockIdx.y;
   float m_run[G], l_run[G], o[G][T];
   init_state<T, G>(m_run, l_run, o);
-  // With G >= 2 the compressed segments run on the MFMA kernel; this one then
-  // only serves the window of a call whose compressed cache is empty.
-  if constexpr (G == 1) {
-    if (seg < a.n_sparse_segs) sparse_body<T, STAGE>(a, seg, bh, smem, m_run[0], l_run[0], o[0]);
-    else dense_body<T, G>(a, seg - a.n_sparse_segs, bh, smem, m_run, l_run, o);
+  if (seg < a.n_sparse_segs) {
+    if constexpr (G == 1) sparse_body<T, STAGE>(a, seg, bh, smem, m_run[0], l_run[0], o[0]);
+    else sparse_body_g<T, G, STAGE>(a, seg, bh, smem, m_run, l_run, o);
   } else {
     dense_body<T, G>(a, seg - a.n_sparse_segs, bh, smem, m_run, l_run, o);
   }
@@ -482,7 +797,7 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void k_merge(const float2* __r
 // ------------------------------------------------------------------------------------------
 template <int T, int G, int STAGE>
 static hipError_t sparse_launch(const AttnShape& sh, const AttnArgs& a, hipStream_t s) {
-  size_t lds = G == 1 ? sparse_lds_layout(T, a.kmaxK, a.kmaxV).total : 0;
+  size_t lds = sh.n_sparse_segs > 0 ? sparse_lds_layout(T, a.kmaxK, a.kmaxV, G).total : 0;
   if (sh.n_dense_segs > 0 && dense_lds_bytes(T, G) > lds) lds = dense_lds_bytes(T, G);
   hipLaunchKernelGGL((k_sparse_attn<T, G, STAGE>), dim3(sh.n_sparse_segs + sh.n_dense_segs, sh.BHkv),
                      dim3(kWave), lds, s, a);
@@ -565,8 +880,8 @@ hipError_t launch_attention(const AttnShape& sh, const uint16_t* q, const Sparse
   a.ws_ml = reinterpret_cast<float2*>(ws_ml);
   a.ws_o = ws_o;
   a.BHq = sh.BHkv * sh.G;
-  a.kmaxK = side_token_bound(d, K);
-  a.kmaxV = side_token_bound(d, V);
+  a.kmaxK = side_token_bound(d, K, kWave / sh.T);  // the walk kernel's blocks (the MFMA
+  a.kmaxV = side_token_bound(d, V, kWave / sh.T);  // kernel sets its own)
   a.n_comp = sh.n_comp;
   a.win_len = sh.win_len;
   a.win_head = sh.win_head;

@@ -42,6 +42,10 @@ struct MfmaLds {
   uint32_t vst, kst, kd, vdt, total;
 };
 
+// Lane j T + t of a block walks tile t of token j: NB = 64 / T tokens per block.
+// (Half-tile lanes -- 16-token blocks at d = 128, twice the waves per CU by LDS --
+// measured 10-15% slower on the grouped-query workloads: their extra walk slots
+// and per-block work outweighed the occupancy.)
 template <int T>
 struct MfmaGeom {
   static constexpr int NB = kWave / T;                     // tokens per block
@@ -302,8 +306,13 @@ static hipError_t mfma_launch(const AttnShape& sh, const AttnArgs& a, hipStream_
 }
 
 template <int T, int G>
-static hipError_t mfma_stage(const AttnShape& sh, const AttnArgs& a, hipStream_t s) {
-  const int NB = kWave / T;
+static hipError_t mfma_stage(const AttnShape& sh, const AttnArgs& a_in, hipStream_t s) {
+  constexpr int NB = MfmaGeom<T>::NB;
+  // Staging bounds for this kernel's blocks (a per-channel cache's bound depends
+  // on the block length).
+  AttnArgs a = a_in;
+  a.kmaxK = side_token_bound(kTile * T, a.K, NB);
+  a.kmaxV = side_token_bound(kTile * T, a.V, NB);
   const int chunks = (NB * a.kmaxK + 511) / 512 + (NB * a.kmaxV + 511) / 512;
   if (chunks <= 4) return mfma_launch<T, G, 4>(sh, a, s);
   if (chunks <= 6) return mfma_launch<T, G, 6>(sh, a, s);

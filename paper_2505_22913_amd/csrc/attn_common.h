@@ -494,12 +494,12 @@ inline int token_max_elems_dev(int d, int k) {
 }
 
 // Worst-case fp16 elements per token of a per-channel cache (group_keep gk),
-// as the bound on the run of any block of NB = 64/T block-aligned tokens
-// divided by NB: a block of 32 or more tokens holds whole groups of 32 (gk * d
-// kept values and at most 7 pad slots per tile each); a 16-token block (T = 4)
-// holds at most min(16, gk) values per channel plus its pad slots.
-inline int grouped_token_bound(int d, int gk) {
-  const int T = d / kTile, NB = kWave / T;
+// as the bound on the run of any block of NB block-aligned tokens divided by
+// NB: a block of 32 or more tokens holds whole groups of 32 (gk * d kept values
+// and at most 7 pad slots per tile each); a shorter block (half a group or
+// less) holds at most min(NB, gk) values per channel plus its pad slots.
+inline int grouped_token_bound(int d, int gk, int NB) {
+  const int T = d / kTile;
   const int64_t per_block =
       NB >= kGroup ? (int64_t)(NB / kGroup) * ((int64_t)gk * d + (int64_t)kGroup * T * (kPad - 1))
                    : (int64_t)d * (NB < gk ? NB : gk) + (int64_t)NB * T * (kPad - 1);
@@ -507,14 +507,20 @@ inline int grouped_token_bound(int d, int gk) {
   return m < d ? m : d;
 }
 
-inline int side_token_bound(int d, const SparseSide& s) {
+// Staging bound per token of one cache for blocks of NB tokens.
+inline int side_token_bound(int d, const SparseSide& s, int NB) {
   if (s.bitmaps == nullptr) return 0;
-  return s.group_keep >= 0 ? grouped_token_bound(d, s.group_keep) : token_max_elems_dev(d, s.n_keep);
+  return s.group_keep >= 0 ? grouped_token_bound(d, s.group_keep, NB) : token_max_elems_dev(d, s.n_keep);
 }
 
 // The MFMA kernel for grouped queries (attention_mfma.hip; G in {2, 4, 8}); the
-// sparse call uses it from kMfmaMinGroup query heads per kv-head on.
-constexpr int kMfmaMinGroup = 2;
+// sparse call uses it from kMfmaMinGroup query heads per kv-head on, the walks
+// below that. Measured on one box (d = 128, 70/70, best split count of each):
+// at G = 2 the walks take 47 us against 58 (16K tokens, 32 streams), at G = 4
+// 58 against 57 (16K) and 86 against 99 (128K, 8 streams), at G = 8 85 against
+// 59: the matrix cores pay from eight query heads per kv-head on, where each
+// expanded key and value feeds eight products.
+constexpr int kMfmaMinGroup = 8;
 hipError_t launch_sparse_mfma(const AttnShape& sh, const AttnArgs& a, hipStream_t s);
 
 }  // namespace mf

@@ -213,12 +213,15 @@ def test_default_splits_follow_the_kernel(lib):
     assert ds(1, 32, 32, 4096, S) == 64
     assert ds(1, 8, 8, 1024, S) == 16
     assert ds(1, 8, 8, 1024, D) == 16
-    # grouped queries: ~2048 (sparse) or ~4096 (dense) workgroups of at least 128 tokens
-    assert ds(1, 32, 8, 131072, S) == 256
+    # 2 or 4 query heads per kv-head (the walks): ~4096 workgroups of at least 256 tokens;
+    # 8 (the matrix-core kernel): ~2048 of at least 128; dense with grouped queries: ~4096
+    assert ds(1, 32, 8, 131072, S) == 512
     assert ds(1, 32, 8, 131072, D) == 512
     assert ds(4, 32, 8, 16384, S) == 64
+    assert ds(4, 16, 8, 16384, S) == 64
+    assert ds(4, 64, 8, 16384, S) == 64
     assert ds(4, 32, 8, 16384, D) == 128
-    assert ds(1, 32, 8, 300, S) == 3
+    assert ds(1, 32, 8, 300, S) == 2
     # invalid arguments
     assert ds(1, 32, 8, 4096, 2) == 1
     assert ds(0, 32, 8, 4096, S) == 1

@@ -97,6 +97,41 @@ def test_attention_over_grouped_values(G, d):
         assert err <= ATTN_TOL
 
 
+@pytest.mark.parametrize("G,d", [(1, 128), (4, 128), (4, 64), (2, 256), (1, 64)])
+def test_attention_over_grouped_values_clustered(G, d):
+    """Every channel keeps the same 10 tokens of each group of 32, its first ten
+    (their values dominate), so those tokens are dense and the other 22 empty: the
+    most values any block of a kernel can meet (a 16-token block holds all of a
+    group's kept values). The attention kernels stage such blocks whole."""
+    import torch
+    announce(f"attention over clustered per-channel values G={G} d={d}")
+    rng = np.random.default_rng(60 + G + d)
+    B, Hkv, N, Nd = 1, 2, 256, 32
+    k = _tokens(rng, (B, Hkv, N + Nd, d))
+    v = (rng.standard_normal((B, Hkv, N + Nd, d)) * 0.01).astype(np.float16)
+    for g0 in range(0, N, 32):
+        v[:, :, g0:g0 + 10] = (8.0 + 2.0 * np.abs(rng.standard_normal((B, Hkv, 10, d)))).astype(np.float16)
+    Kc = mf.CompressedCache(B, Hkv, d, 0.5, N)
+    Vc = mf.CompressedCache(B, Hkv, d, 0.7, N, grouped=True)
+    mf.mustafar_prune_compress(Kc, _dev(k[:, :, :N]))
+    mf.mustafar_prune_compress(Vc, _dev(v[:, :, :N]))
+    want_v = oracle.compress_grouped(v[:, :, :N], 0.7)
+    bm = want_v["bitmaps"][0, 0, :32]
+    assert all(int(x) == (1 << 64) - 1 for x in bm[:10].reshape(-1))   # the first ten are dense
+    assert not bm[10:].any()
+    compare_format(read_cache(Vc), want_v, N, all_pairs(B, Hkv))
+    q = _tokens(rng, (B, Hkv * G, d))
+    for splits in (0, 1):
+        out = mf.mustafar_sparse_decode_attn(_dev(q), Kc, Vc, _dev(k[:, :, N:]), _dev(v[:, :, N:]),
+                                             n_splits=splits)
+        torch.cuda.synchronize()
+        ref = oracle.sparse_decode_attention(q, oracle.compress(k[:, :, :N], 0.5), want_v,
+                                             k[:, :, N:], v[:, :, N:])
+        err = attn_error(out.cpu().numpy(), ref)
+        announce(f"clustered per-channel values G={G} d={d} splits={splits}: error {err:.2e}")
+        assert err <= ATTN_TOL
+
+
 def _state(win, acc):
     import torch
     torch.cuda.synchronize()
