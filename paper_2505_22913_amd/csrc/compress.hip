@@ -210,17 +210,51 @@ __device__ uint32_t look_back(uint64_t* __restrict__ fl, int chunk, uint32_t tot
 // reach k) or all move to `above`. At the end the threshold ties (`cand`) are
 // taken lowest channel first up to k. This is the same selection as the radix
 // search on the magnitude, with a per-plane cost instead of a per-key one.
+// (m & a) | (~m & b) in one instruction (the compiler splits the masked
+// halves apart when it sees them).
+__device__ __forceinline__ uint32_t bit_select(uint32_t m, uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "s"(m), "v"(a), "v"(b));
+  return r;
+}
+
+// a * b + c on 24-bit signed operands, one instruction (|a|, |b| < 2^23).
+__device__ __forceinline__ int mad_i24(int a, int b, int c) {
+  int r;
+  asm("v_mad_i32_i24 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// (a << s) + b, one instruction (kept as written: a running sum of bits
+// would otherwise be rebuilt from a second counter at every step).
+__device__ __forceinline__ int lshl_add(int a, int s, int b) {
+  int r;
+  asm("v_lshl_add_u32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "i"(s), "v"(b));
+  return r;
+}
+
+// The transpose is four rounds of block swaps (8, 4, 2, 1 bits): in the round
+// of s, rows i and i+s (i without bit s) exchange the s-bit blocks that sit
+// off the diagonal. The byte round is one byte permute per row; the others
+// are a shift and a bit select per row.
 __device__ __forceinline__ void transpose16x2(uint32_t* x) {
-  constexpr uint32_t kMask[4] = {0x00ff00ffu, 0x0f0f0f0fu, 0x33333333u, 0x55555555u};
 #pragma unroll
-  for (int l = 0; l < 4; ++l) {
-    const int s = 8 >> l;
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t a = x[i], b = x[i + 8];
+    x[i] = __builtin_amdgcn_perm(b, a, 0x06020400u);      // a.byte0, b.byte0, a.byte2, b.byte2
+    x[i + 8] = __builtin_amdgcn_perm(b, a, 0x07030501u);  // a.byte1, b.byte1, a.byte3, b.byte3
+  }
+  constexpr uint32_t kMask[3] = {0x0f0f0f0fu, 0x33333333u, 0x55555555u};
+#pragma unroll
+  for (int l = 0; l < 3; ++l) {
+    const int s = 4 >> l;
+    const uint32_t m = kMask[l];  // the low block of each pair; ~m == m << s
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       if (i & s) continue;
-      const uint32_t t = ((x[i] >> s) ^ x[i + s]) & kMask[l];
-      x[i + s] ^= t;
-      x[i] ^= t << s;
+      const uint32_t a = x[i], b = x[i + s];
+      x[i] = bit_select(m, a, b << s);
+      x[i + s] = bit_select(m, a >> s, b);
     }
   }
 }
@@ -234,6 +268,18 @@ __device__ __forceinline__ uint32_t interleave_halves(uint32_t x) {
     const uint32_t t = ((x >> s) ^ x) & kMask[l];
     x ^= t ^ (t << s);
   }
+  return x;
+}
+
+// Inclusive prefix sum over the 64 lanes: shifts within rows of 16 lanes,
+// then the last lane of row 0 (of rows 0-1) is added to row 1 and 3 (2-3).
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);  // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false); // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false); // row_bcast:31
   return x;
 }
 
@@ -338,22 +384,37 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
   } else {
     const int jt = min((int)lane / LPT, max(nt, 1) - 1);
     const unsigned char* row = s_rows + jt * ROW + ((int)lane % LPT) * CPL * 2;
+    // Register 16 g + i holds the keys of channels 32 g + i (low half) and
+    // 32 g + 16 + i (high half), so that bit r of plane word b of group g is
+    // bit b of channel 32 g + r: the planes come out in channel order. The
+    // sign bits land in plane 15, which the search never reads.
     uint32_t pl[NR];
 #pragma unroll
     for (int i = 0; i < NR / 4; ++i) {
       const u32x4_t w = *reinterpret_cast<const u32x4_t*>(row + 16 * i);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) pl[4 * i + e] = w[e] & 0x7fff7fffu;
+      for (int e = 0; e < 4; ++e) pl[4 * i + e] = w[e];  // channels 8i+2e, 8i+2e+1
     }
 #pragma unroll
-    for (int g = 0; g < NW; ++g) transpose16x2(pl + 16 * g);   // pl[16g + b] = plane b of group g
+    for (int g = 0; g < NW; ++g) {
+      uint32_t r[16];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t a = pl[16 * g + j], b = pl[16 * g + 8 + j];
+        r[2 * j] = __builtin_amdgcn_perm(b, a, 0x05040100u);      // low halves of a and b
+        r[2 * j + 1] = __builtin_amdgcn_perm(b, a, 0x07060302u);  // high halves
+      }
+      transpose16x2(r);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) pl[16 * g + i] = r[i];  // pl[16g + b] = plane b of group g
+    }
     uint32_t cand[NW], above[NW];
 #pragma unroll
     for (int g = 0; g < NW; ++g) {
       cand[g] = 0xffffffffu;
       above[g] = 0u;
     }
-    int n_above = 0;
+    int need = k;  // keys still to keep beyond `above`
 #pragma unroll
     for (int b = 14; b >= 0; --b) {
       uint32_t ones[NW];
@@ -363,34 +424,48 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
         ones[g] = cand[g] & pl[16 * g + b];
         c1 += __popc(ones[g]);
       }
-      if constexpr (LPT == 2) c1 += __builtin_amdgcn_mov_dpp(c1, 0xB1, 0xF, 0xF, false);
-      const bool take = n_above + c1 >= k;
+      if constexpr (LPT == 2) c1 += __builtin_amdgcn_update_dpp(0, c1, 0xB1, 0xF, 0xF, true);
+      // The candidates with a one here reach the rest of k: they stay the
+      // candidates. Otherwise (fall = -1) they are all kept and those with a
+      // zero stay candidates.
+      const int fall = (c1 - need) >> 31;
 #pragma unroll
       for (int g = 0; g < NW; ++g) {
-        above[g] = take ? above[g] : (above[g] | ones[g]);
-        cand[g] = take ? ones[g] : (cand[g] & ~pl[16 * g + b]);
+        above[g] |= ones[g] & (uint32_t)fall;
+        cand[g] = ones[g] ^ (cand[g] & (uint32_t)fall);
       }
-      n_above += take ? 0 : c1;
+      need = mad_i24(c1, fall, need);  // need - c1 when they fell
     }
     // Ties at the threshold: the lowest channels first, up to k (across the two
-    // lanes of a d = 256 token, the lower half of the channels first).
-    int need = k - n_above, n_cand = 0;
+    // lanes of a token, the lower half of the channels first): `drop` of this
+    // lane's candidates, the highest channels, are not kept.
+    int n_cand = 0;
 #pragma unroll
-    for (int g = 0; g < NW; ++g) {
-      above[g] = interleave_halves(above[g]);
-      cand[g] = interleave_halves(cand[g]);
-      n_cand += __popc(cand[g]);
-    }
+    for (int g = 0; g < NW; ++g) n_cand += __popc(cand[g]);
     if constexpr (LPT == 2) {
       const int lower = __builtin_amdgcn_mov_dpp(n_cand, 0xB1, 0xF, 0xF, false);
       if (lane & 1u) need -= lower;
     }
-    if (ballot(need < n_cand)) {
+    int drop = n_cand - min(max(need, 0), n_cand);
+    if (ballot(drop > 2)) {
 #pragma unroll
       for (int g = 0; g < NW; ++g) {
         const int c = __popc(cand[g]);
         cand[g] = lowest_bits(cand[g], need);
         need -= c;
+      }
+    } else {
+      // Usually at most one tie: clear the highest candidate drop times.
+      while (ballot(drop > 0)) {
+        bool done = drop <= 0;
+#pragma unroll
+        for (int g = NW - 1; g >= 0; --g) {
+          const bool here = !done && cand[g] != 0u;
+          const uint32_t top = cand[g] != 0u ? 0x80000000u >> __clz(cand[g]) : 0u;
+          cand[g] = here ? cand[g] & ~top : cand[g];
+          done = done || here;
+        }
+        --drop;
       }
     }
 #pragma unroll
@@ -409,12 +484,7 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
     lane_len += pad8((uint32_t)(__popc(keep[2 * t]) + __popc(keep[2 * t + 1])));
   }
   if ((int)lane >= nt * LPT) lane_len = 0;   // lanes past the chunk hold no token
-  uint32_t incl = lane_len;
-#pragma unroll
-  for (int o = 1; o < kWave; o <<= 1) {
-    const uint32_t v = (uint32_t)__shfl_up((int)incl, o, kWave);
-    if ((int)lane >= o) incl += v;
-  }
+  const uint32_t incl = wave_incl_scan(lane_len);
   const uint32_t wave_run = (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
   if (lane == 0) s_share[1 + wave] = wave_run;
   __syncthreads();
@@ -450,14 +520,17 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
     for (int t = 0; t < TPL; ++t) {
       const uint32_t lo = live ? keep[2 * t] : 0u, hi = live ? keep[2 * t + 1] : 0u;
       const uint32_t cnt = (uint32_t)(__popc(lo) + __popc(hi));
-      uint32_t pos = base_lds + 2u * (lane_off + tile_pos[t]);
+      const uint32_t pos = base_lds + 2u * (lane_off + tile_pos[t]);
       if (cnt & 7u) lds_st<u32x4_t>(pos + 16u * (cnt / 8u), (u32x4_t){0u, 0u, 0u, 0u});
+      // Value c goes to trash + bit * delta: the next packed slot when kept
+      // (delta, in bytes from the trash slot, then moves one slot on).
+      int delta = (int)pos - (int)trash;  // |delta| < 64 KiB
 #pragma unroll
       for (int c = 0; c < kTile; ++c) {
-        const uint32_t bit = ((c < 32 ? lo : hi) >> (c & 31)) & 1u;
+        const int bit = (int)(((c < 32 ? lo : hi) >> (c & 31)) & 1u);
         const uint32_t pair = v[(kTile / 2) * t + c / 2];
-        lds_st<uint16_t>(bit ? pos : trash, (uint16_t)(c & 1 ? pair >> 16 : pair));
-        pos += bit << 1;
+        lds_st<uint16_t>((uint32_t)mad_i24(bit, delta, (int)trash), (uint16_t)(c & 1 ? pair >> 16 : pair));
+        delta = lshl_add(bit, 1, delta);
       }
     }
   }
