@@ -150,6 +150,30 @@ def read_ceiling_gbs(n_bytes: int = 8 << 30) -> float:
     return n_bytes / t / 1e9
 
 
+def rw_ceiling_gbs(write_16ths: int, n_bytes: int = 8 << 30) -> float:
+    """HBM read + write rate of this GPU at a given write share: the library's
+    streaming kernel reads an n_bytes buffer and writes write_16ths/16 of it;
+    the rate counts both directions."""
+    import torch
+
+    import paper_2505_22913_amd as mf
+    x = torch.empty(n_bytes, dtype=torch.uint8, device="cuda")
+    x.fill_(1)
+    y = torch.empty(n_bytes * write_16ths // 16 + 16, dtype=torch.uint8, device="cuda")
+    sink = mf.mustafar_stream_mix(x, y, write_16ths)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(5):
+        mf.mustafar_stream_mix(x, y, write_16ths, sink)
+    b.record()
+    torch.cuda.synchronize()
+    t = a.elapsed_time(b) / 1e3 / 5
+    del x, y
+    torch.cuda.empty_cache()
+    return n_bytes * (1 + write_16ths / 16) / t / 1e9
+
+
 def call_stats(marks) -> dict:
     """Per-call HIP-event times (us) of recorded (start, end) pairs: mean, median, min, max."""
     import numpy as np
@@ -688,6 +712,8 @@ def main():
         torch.cuda.empty_cache()
 
     ceiling = read_ceiling_gbs()
+    pc_w16 = max(1, min(16, round(16 * comp_kv / dense_kv)))  # the compression's write share
+    rw_ceiling = rw_ceiling_gbs(pc_w16)
 
     result = {
         "metric": METRIC,
@@ -732,6 +758,11 @@ def main():
                            "gb_s": (dense_kv + comp_kv) / t_pc / 1e9,
                            "frac": (dense_kv + comp_kv) / t_pc / 1e9 / HBM_PEAK_GBS,
                            "traffic": pc_traffic,
+                           "rw_ceiling": {"gb_s": rw_ceiling, "write_16ths": pc_w16,
+                                          "frac_of_ceiling": (dense_kv + comp_kv) / t_pc / 1e9 / rw_ceiling,
+                                          "how": "mustafar_stream_mix over an 8 GiB buffer: every 16-byte "
+                                                 "word read, write_16ths of each 16 written (the "
+                                                 "compression's write share); rate of both directions"},
                            "how": "K and V of every kv-head: tokens_per_s = batch x context / time; "
                                   "token_vectors_per_s counts each (kv-head, K or V) vector"},
         "append_us_per_step": (total_s / steps - attn_s) * 1e6,

@@ -483,6 +483,18 @@ const char* mustafar_strerror(int status);
 size_t mustafar_stream_read_sink_bytes(void);
 int mustafar_stream_read(const void* src, size_t bytes, void* sink, void* stream);
 
+/* MEASUREMENT HELPER (not a step of the method). Streams `bytes` of device
+ * memory at `src` through 16-byte loads, writes one 32-bit checksum per
+ * workgroup to `sink` (as mustafar_stream_read does) and writes
+ * write_16ths/16 of the words to `dst` (device, at least
+ * bytes * write_16ths / 16 bytes): of every 16 consecutive 16-byte words, the
+ * first write_16ths are stored, packed. The rate is the HBM ceiling of a pass
+ * that reads a dense cache and writes its compressed form in that ratio.
+ * `src` and `dst` must be 16-byte aligned, `sink` 4-byte aligned, `bytes` a
+ * multiple of 256 and 0 <= write_16ths <= 16. Errors: EINVAL. */
+int mustafar_stream_mix(const void* src, size_t bytes, void* dst, int write_16ths, void* sink,
+                        void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -153,6 +153,8 @@ _SIGS = {
     "mustafar_stream_read_sink_bytes": (ctypes.c_size_t, []),
     "mustafar_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                                             ctypes.c_void_p]),
+    "mustafar_stream_mix": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
+                                           ctypes.c_void_p, ctypes.c_void_p]),
 }
 
 
@@ -543,6 +545,20 @@ def mustafar_window_step_grouped(win: DenseWindow, Kc: CompressedCache, Vc: Comp
     _check("mustafar_window_step_grouped", lib().mustafar_window_step_grouped(
         ctypes.byref(win.desc), ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), _dptr(k_new),
         _dptr(v_new), _dptr(active), _dptr(acc), _stream(stream)))
+
+
+def mustafar_stream_mix(src, dst, write_16ths: int, sink=None, stream=None):
+    """Measurement helper: stream device tensor `src`, write write_16ths/16 of it to `dst`."""
+    import torch
+    need = src.numel() * src.element_size() * write_16ths // 16
+    if dst.numel() * dst.element_size() < need:
+        raise ValueError(f"dst holds {dst.numel() * dst.element_size()} bytes, {need} needed")
+    if sink is None:
+        sink = torch.empty(lib().mustafar_stream_read_sink_bytes(), dtype=torch.uint8, device=src.device)
+    _check("mustafar_stream_mix", lib().mustafar_stream_mix(
+        _dptr(src), src.numel() * src.element_size(), _dptr(dst), int(write_16ths), _dptr(sink),
+        _stream(stream)))
+    return sink
 
 
 def mustafar_stream_read(buf, sink=None, stream=None):

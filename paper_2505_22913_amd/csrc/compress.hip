@@ -166,16 +166,22 @@ __device__ void publish_total(uint64_t* __restrict__ fl, int chunk, uint32_t tot
                        __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// The flags of the 64 chunks before `top` (lane i: chunk top - i); positions
+// before chunk 0 read as a known prefix of 0.
+__device__ __forceinline__ uint64_t poll_flags(const uint64_t* __restrict__ fl, int top, uint32_t lane) {
+  const int p = top - (int)lane;
+  return p >= 0 ? __hip_atomic_load(fl + p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : kFlagPrefix;
+}
+
+// f0: the first poll, poll_flags(fl, chunk - 1, lane), issued by the caller
+// ahead of time so that its latency overlaps other work.
 __device__ uint32_t look_back(uint64_t* __restrict__ fl, int chunk, uint32_t total,
-                              uint32_t first_base, uint32_t lane, uint32_t max_polls) {
+                              uint32_t first_base, uint32_t lane, uint32_t max_polls, uint64_t f0) {
   if (chunk == 0) return first_base;
   uint32_t acc = 0, polls = 0;
   for (int top = chunk - 1;;) {
     if (polls++ >= max_polls) return kBadBase;
-    const int p = top - (int)lane;
-    // Positions before chunk 0 read as a known prefix of 0.
-    const uint64_t f = p >= 0 ? __hip_atomic_load(fl + p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                              : kFlagPrefix;
+    const uint64_t f = polls == 1 ? f0 : poll_flags(fl, top, lane);
     const uint32_t st = (uint32_t)(f >> 62);
     const uint64_t pref = ballot(st == 2u);
     const uint64_t none = ballot(st == 0u);
@@ -294,6 +300,14 @@ __device__ __forceinline__ uint32_t lowest_bits(uint32_t w, int n) {
   return w & (p >= 31u ? 0xffffffffu : ((2u << p) - 1u));
 }
 
+// Workgroup barrier that orders LDS only: the waves of a workgroup exchange
+// nothing else, and a full barrier would also wait for loads in flight.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // compress_waves() waves per workgroup; a chunk is that many runs of 64 tokens
 // (32 from d = 128 on) of one stream, one run per wave. The waves select and
 // pack their runs side by side and share the chunk's ticket, scan total and
@@ -337,28 +351,43 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
   // of it leaves before drawing a ticket (the last chunk, which rewrites
   // stream_len, draws the last ticket, after every other workgroup's read).
   if (tok0 > 0 && __builtin_amdgcn_readfirstlane((int)stream_len[bh]) == (int)kStreamPoisoned) return;
-  if (threadIdx.x == 0) s_share[0] = atomicAdd(ticket_ctr + bh, 1u);
-  __syncthreads();
-  const int chunk = __builtin_amdgcn_readfirstlane((int)s_share[0]);
-  const int k = o.per_head ? o.head_keep[bh % o.H] : k_all;  // kept channels of this stream
-  const int jc = chunk * (kCompressWaves * TPW);                // the chunk's first token
-  const int j0 = jc + wave * TPW;                               // this wave's first token
-  const int nt = min(TPW, n_new - j0);      // <= 0: the chunk ends before this wave's half
-  const uint32_t base_lds = (uint32_t)(uintptr_t)s_rows;
-
-  // Stage the wave's dense rows: 16-byte coalesced non-temporal loads (every
-  // load issued; lanes past the rows re-read the chunk's first piece and store
-  // nothing).
-  {
-    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(x + ((int64_t)bh * x_stride + (nt > 0 ? j0 : jc)) * d);
-    const int n16 = max(nt, 0) * P16;
-    constexpr int kIt = TPW * P16 / kWave;
-    u32x4_t r[kIt];
+  constexpr int kChunk = kCompressWaves * TPW;
+  constexpr int kIt = TPW * P16 / kWave;  // 16-byte loads per lane for the wave's rows
+  // Stage loads of the wave's dense rows of chunk `ch`: 16-byte coalesced
+  // non-temporal loads (every load issued; lanes past the rows re-read the
+  // chunk's first piece and store nothing).
+  auto stage_load = [&](int ch, u32x4_t (&r)[kIt]) {
+    const int sj0 = ch * kChunk + wave * TPW;
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(
+        x + ((int64_t)bh * x_stride + (sj0 < n_new ? sj0 : ch * kChunk)) * d);
+    const int n16 = max(min(TPW, n_new - sj0), 0) * P16;
 #pragma unroll
     for (int i = 0; i < kIt; ++i) {
       const int c = i * kWave + (int)lane;
       r[i] = __builtin_nontemporal_load(&src[c < n16 ? c : 0]);
     }
+  };
+  // The chunk comes with the ticket; the rows of the chunk that workgroups
+  // launched in order would draw are loaded meanwhile (and loaded again in
+  // the rare case that the ticket differs). The ticket is drawn with an
+  // increment: the wave-aggregating rewrite of an add waits for its result
+  // at once.
+  const int guess = (int)(blockIdx.x / (gridDim.x / (uint32_t)n_chunks));
+  uint32_t tk = 0u;
+  if (threadIdx.x == 0) tk = atomicInc(ticket_ctr + bh, 0xffffffffu);
+  u32x4_t r[kIt];
+  stage_load(guess, r);
+  if (threadIdx.x == 0) s_share[0] = tk;
+  lds_barrier();
+  const int chunk = __builtin_amdgcn_readfirstlane((int)s_share[0]);
+  if (chunk != guess) stage_load(chunk, r);
+  const int k = o.per_head ? o.head_keep[bh % o.H] : k_all;  // kept channels of this stream
+  const int jc = chunk * kChunk;                // the chunk's first token
+  const int j0 = jc + wave * TPW;               // this wave's first token
+  const int nt = min(TPW, n_new - j0);          // <= 0: the chunk ends before this wave's half
+  const uint32_t base_lds = (uint32_t)(uintptr_t)s_rows;
+  {
+    const int n16 = max(nt, 0) * P16;
 #pragma unroll
     for (int i = 0; i < kIt; ++i) {
       const int c = i * kWave + (int)lane;
@@ -366,8 +395,20 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
     }
   }
 
-  // Keep-mask of this lane's token (lanes past the chunk select on a copy of
-  // the last row and store nothing): NW words of 32 channels, channel order.
+  // This lane's half row (lanes past the chunk take a copy of the last row
+  // and store nothing), kept in registers for the packing.
+  uint32_t raw[NR];
+  {
+    const unsigned char* row = s_rows + min((int)lane / LPT, max(nt, 1) - 1) * ROW + ((int)lane % LPT) * CPL * 2;
+#pragma unroll
+    for (int i = 0; i < NR / 4; ++i) {
+      const u32x4_t w = *reinterpret_cast<const u32x4_t*>(row + 16 * i);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) raw[4 * i + e] = w[e];  // channels 8i+2e, 8i+2e+1
+    }
+  }
+
+  // Keep-mask of this lane's token: NW words of 32 channels, channel order.
   constexpr int NW = NR / 16;
   uint32_t keep[NW];
   if constexpr (PRESET) {
@@ -382,25 +423,17 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
       keep[2 * t + 1] = (uint32_t)(bm >> 32);
     }
   } else {
-    const int jt = min((int)lane / LPT, max(nt, 1) - 1);
-    const unsigned char* row = s_rows + jt * ROW + ((int)lane % LPT) * CPL * 2;
     // Register 16 g + i holds the keys of channels 32 g + i (low half) and
     // 32 g + 16 + i (high half), so that bit r of plane word b of group g is
     // bit b of channel 32 g + r: the planes come out in channel order. The
     // sign bits land in plane 15, which the search never reads.
     uint32_t pl[NR];
 #pragma unroll
-    for (int i = 0; i < NR / 4; ++i) {
-      const u32x4_t w = *reinterpret_cast<const u32x4_t*>(row + 16 * i);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) pl[4 * i + e] = w[e];  // channels 8i+2e, 8i+2e+1
-    }
-#pragma unroll
     for (int g = 0; g < NW; ++g) {
       uint32_t r[16];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const uint32_t a = pl[16 * g + j], b = pl[16 * g + 8 + j];
+        const uint32_t a = raw[16 * g + j], b = raw[16 * g + 8 + j];
         r[2 * j] = __builtin_amdgcn_perm(b, a, 0x05040100u);      // low halves of a and b
         r[2 * j + 1] = __builtin_amdgcn_perm(b, a, 0x07060302u);  // high halves
       }
@@ -487,7 +520,7 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
   const uint32_t incl = wave_incl_scan(lane_len);
   const uint32_t wave_run = (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
   if (lane == 0) s_share[1 + wave] = wave_run;
-  __syncthreads();
+  lds_barrier();
   uint32_t run = 0, wave_off = 0;           // the chunk's run: the waves' runs in order
 #pragma unroll
   for (int w = 0; w < kCompressWaves; ++w) {
@@ -497,25 +530,19 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
   const uint32_t lane_off = incl - lane_len;  // in the wave's run
   const uint32_t first = (chunk == 0 && tok0 > 0) ? stream_len[bh] : 0u;
   if (wave == 0) publish_total(flags + (int64_t)bh * n_chunks, chunk, run, first, lane);
+  // The first look-back poll, in flight while the run is packed.
+  const uint64_t f0 = (wave == 0 && chunk > 0) ? poll_flags(flags + (int64_t)bh * n_chunks, chunk - 1, lane) : 0ull;
 
-  // Packing, lane = its tiles: the lane reloads its row into registers, then
+  // Packing, lane = its tiles: from its row held in registers, the lane
   // writes the kept values of each tile in channel order, value r of a tile
   // at r, over the wave's own rows (a wave's LDS operations run in program
-  // order, so every row is read before the first write). The run is at most
+  // order, so every row was read before the first write). The run is at most
   // d values per token, so it ends before the last row's pad, the trash slot
   // of the dropped channels. The tile's last group of 8 is zeroed first, so
   // its pad slots hold +0.0.
   {
     const uint32_t trash = base_lds + (uint32_t)(TPW * ROW - 16);
     const bool live = (int)lane < nt * LPT;
-    const uint32_t row = base_lds + (uint32_t)(min((int)lane / LPT, max(nt, 1) - 1) * ROW + ((int)lane % LPT) * CPL * 2);
-    uint32_t v[NR];
-#pragma unroll
-    for (int i = 0; i < NR / 4; ++i) {
-      const u32x4_t w = lds_ld<u32x4_t>(row + 16u * (uint32_t)i);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[4 * i + e] = w[e];
-    }
 #pragma unroll
     for (int t = 0; t < TPL; ++t) {
       const uint32_t lo = live ? keep[2 * t] : 0u, hi = live ? keep[2 * t + 1] : 0u;
@@ -528,7 +555,7 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
 #pragma unroll
       for (int c = 0; c < kTile; ++c) {
         const int bit = (int)(((c < 32 ? lo : hi) >> (c & 31)) & 1u);
-        const uint32_t pair = v[(kTile / 2) * t + c / 2];
+        const uint32_t pair = raw[(kTile / 2) * t + c / 2];
         lds_st<uint16_t>((uint32_t)mad_i24(bit, delta, (int)trash), (uint16_t)(c & 1 ? pair >> 16 : pair));
         delta = lshl_add(bit, 1, delta);
       }
@@ -536,7 +563,7 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
   }
 
   if (wave == 0) {
-    const uint32_t b = look_back(flags + (int64_t)bh * n_chunks, chunk, run, first, lane, max_polls);
+    const uint32_t b = look_back(flags + (int64_t)bh * n_chunks, chunk, run, first, lane, max_polls, f0);
     if (lane == 0) s_share[kCompressWaves + 1] = b;
     if (lane == 0 && b == kBadBase) {
       // Mark the stream and the call; k_compress_finalize poisons the stream
@@ -546,7 +573,7 @@ __global__ __launch_bounds__(compress_waves<T>() * kWave) void k_compress(const 
     }
     if (lane == 0 && chunk == n_chunks - 1 && b != kBadBase) stream_len[bh] = b + run;
   }
-  __syncthreads();  // the chunk's base
+  lds_barrier();  // the chunk's base
   const uint32_t base = __builtin_amdgcn_readfirstlane((int)s_share[kCompressWaves + 1]);
   if (base == kBadBase) return;  // look-back gave up: nothing is written
 

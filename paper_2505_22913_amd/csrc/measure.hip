@@ -1,4 +1,6 @@
-// Streaming-read ceiling: every lane reads 16-byte words grid-stride with
+// Streaming ceilings the kernels are compared with.
+//
+// Read: every lane reads 16-byte words grid-stride with
 // non-temporal loads (eight in flight) and XORs them; one checksum per
 // workgroup keeps the loads alive. The rate of this kernel over a buffer much
 // larger than the caches is the HBM read rate the decode kernels are compared
@@ -38,7 +40,53 @@ __global__ __launch_bounds__(kReadThreads) void k_stream_read(const u32x4m* __re
   if (threadIdx.x == 0) sink[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
 }
 
+// Streaming read + write: every word is read (and XORed into the workgroup's
+// checksum, like the read ceiling); of every 16 consecutive 16-byte words the
+// first w16 are also written, packed, to dst (word i of group g at
+// g * w16 + i), so dst receives w16/16 of the bytes read, interleaved with the
+// reads the way a compressing pass writes its output.
+__global__ __launch_bounds__(kReadThreads) void k_stream_mix(const u32x4m* __restrict__ src, int64_t n16,
+                                                             u32x4m* __restrict__ dst, int w16,
+                                                             uint32_t* __restrict__ sink) {
+  uint32_t acc = 0;
+  const int64_t g = (int64_t)gridDim.x * kReadThreads;
+  int64_t i = (int64_t)blockIdx.x * kReadThreads + threadIdx.x;
+  for (; i + (kReadUnroll - 1) * g < n16; i += kReadUnroll * g) {
+    u32x4m v[kReadUnroll];
+#pragma unroll
+    for (int u = 0; u < kReadUnroll; ++u) v[u] = __builtin_nontemporal_load(&src[i + u * g]);
+#pragma unroll
+    for (int u = 0; u < kReadUnroll; ++u) {
+      const int64_t j = i + u * g;
+      acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+      if ((int)(j & 15) < w16) __builtin_nontemporal_store(v[u], &dst[(j >> 4) * w16 + (j & 15)]);
+    }
+  }
+  for (; i < n16; i += g) {
+    const u32x4m a = __builtin_nontemporal_load(&src[i]);
+    acc ^= a.x ^ a.y ^ a.z ^ a.w;
+    if ((int)(i & 15) < w16) __builtin_nontemporal_store(a, &dst[(i >> 4) * w16 + (i & 15)]);
+  }
+  __shared__ uint32_t red[kReadThreads / kWave];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) acc ^= (uint32_t)__shfl_xor((int)acc, o, kWave);
+  if (lane_id() == 0) red[threadIdx.x / kWave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
+}
+
 }  // namespace mf
+
+extern "C" int mustafar_stream_mix(const void* src, size_t bytes, void* dst, int write_16ths, void* sink,
+                                   void* stream) {
+  if (!src || !dst || !sink || ((uintptr_t)src % 16) != 0 || ((uintptr_t)dst % 16) != 0 ||
+      ((uintptr_t)sink % 4) != 0 || bytes % 256 != 0 || write_16ths < 0 || write_16ths > 16)
+    return MUSTAFAR_EINVAL;
+  hipLaunchKernelGGL(mf::k_stream_mix, dim3(mf::kReadBlocks), dim3(mf::kReadThreads), 0, (hipStream_t)stream,
+                     reinterpret_cast<const mf::u32x4m*>(src), (int64_t)(bytes / 16),
+                     reinterpret_cast<mf::u32x4m*>(dst), write_16ths, reinterpret_cast<uint32_t*>(sink));
+  return hipGetLastError() == hipSuccess ? MUSTAFAR_OK : MUSTAFAR_ELAUNCH;
+}
 
 extern "C" size_t mustafar_stream_read_sink_bytes(void) {
   return (size_t)mf::kReadBlocks * sizeof(uint32_t);

@@ -469,3 +469,15 @@ def test_static_scratch_decode_rejects_before_touching_the_gpu(lib):
     assert need > mf.STATIC_SCRATCH_BYTES
     assert call(splits=1 << 16) == mf.ESCRATCH
     assert "static scratch" in mf.strerror(mf.ESCRATCH)
+
+
+def test_stream_mix_helper_rejects_bad_arguments(lib):
+    S = 0x300000
+    assert lib.mustafar_stream_mix(0x100008, 256, 0x200000, 9, S, None) == mf.EINVAL   # src not 16-aligned
+    assert lib.mustafar_stream_mix(0x100000, 256, 0x200008, 9, S, None) == mf.EINVAL   # dst not 16-aligned
+    assert lib.mustafar_stream_mix(0x100000, 240, 0x200000, 9, S, None) == mf.EINVAL   # bytes % 256
+    assert lib.mustafar_stream_mix(0x100000, 256, 0x200000, 17, S, None) == mf.EINVAL
+    assert lib.mustafar_stream_mix(0x100000, 256, 0x200000, -1, S, None) == mf.EINVAL
+    assert lib.mustafar_stream_mix(None, 256, 0x200000, 9, S, None) == mf.EINVAL
+    assert lib.mustafar_stream_mix(0x100000, 256, 0x200000, 9, None, None) == mf.EINVAL
+    assert lib.mustafar_stream_mix(0x100000, 256, 0x200000, 9, S + 2, None) == mf.EINVAL

@@ -236,3 +236,24 @@ def test_stream_read_checksum():
     buf = torch.from_numpy(words.view(np.int32)).cuda()
     sink = mf.mustafar_stream_read(buf).cpu().numpy().view(np.uint32)
     assert int(np.bitwise_xor.reduce(sink)) == int(np.bitwise_xor.reduce(words))
+
+
+@pytest.mark.parametrize("w16", [0, 9, 16])
+def test_stream_mix_writes_the_selected_words(w16):
+    # The read+write ceiling helper reads every word (the checksum) and stores
+    # words 0..w16-1 of every group of 16 16-byte words, packed; nothing past
+    # them.
+    import torch
+    announce(f"stream mix w16={w16}")
+    rng = np.random.default_rng(4)
+    n16 = (1 << 16) + 48  # a multiple of 16 words, past one grid-stride pass
+    words = rng.integers(0, 2 ** 32, size=(n16, 4), dtype=np.uint64).astype(np.uint32)
+    src = torch.from_numpy(words.view(np.int32)).cuda()
+    out_words = n16 // 16 * w16
+    dst = torch.full((out_words + 16, 4), -1, dtype=torch.int32, device="cuda")
+    sink = mf.mustafar_stream_mix(src, dst, w16).cpu().numpy().view(np.uint32)
+    assert int(np.bitwise_xor.reduce(sink)) == int(np.bitwise_xor.reduce(words.ravel()))
+    got = dst.cpu().numpy().view(np.uint32)
+    want = words.reshape(-1, 16, 4)[:, :w16].reshape(-1, 4)
+    assert np.array_equal(got[:out_words], want)
+    assert (got[out_words:] == 0xffffffff).all()
