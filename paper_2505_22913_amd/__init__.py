@@ -153,6 +153,8 @@ _SIGS = {
     "mustafar_stream_read_sink_bytes": (ctypes.c_size_t, []),
     "mustafar_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                                             ctypes.c_void_p]),
+    "mustafar_kernel_timing_start": (ctypes.c_int, []),
+    "mustafar_kernel_timing_stop": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int)]),
     "mustafar_stream_mix": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
                                            ctypes.c_void_p, ctypes.c_void_p]),
 }
@@ -545,6 +547,18 @@ def mustafar_window_step_grouped(win: DenseWindow, Kc: CompressedCache, Vc: Comp
     _check("mustafar_window_step_grouped", lib().mustafar_window_step_grouped(
         ctypes.byref(win.desc), ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), _dptr(k_new),
         _dptr(v_new), _dptr(active), _dptr(acc), _stream(stream)))
+
+
+def mustafar_kernel_timing_start() -> None:
+    """Measurement helper: start timing the main kernel of every attention and bulk-compression call."""
+    _check("mustafar_kernel_timing_start", lib().mustafar_kernel_timing_start())
+
+
+def mustafar_kernel_timing_stop():
+    """Stop timing; returns (summed kernel ms, number of timed launches)."""
+    ms, n = ctypes.c_double(0.0), ctypes.c_int(0)
+    _check("mustafar_kernel_timing_stop", lib().mustafar_kernel_timing_stop(ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
 
 
 def mustafar_stream_mix(src, dst, write_16ths: int, sink=None, stream=None):

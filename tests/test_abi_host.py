@@ -481,3 +481,7 @@ def test_stream_mix_helper_rejects_bad_arguments(lib):
     assert lib.mustafar_stream_mix(None, 256, 0x200000, 9, S, None) == mf.EINVAL
     assert lib.mustafar_stream_mix(0x100000, 256, 0x200000, 9, None, None) == mf.EINVAL
     assert lib.mustafar_stream_mix(0x100000, 256, 0x200000, 9, S + 2, None) == mf.EINVAL
+
+
+def test_kernel_timing_stop_rejects_null(lib):
+    assert lib.mustafar_kernel_timing_stop(None, None) == mf.EINVAL
