@@ -60,6 +60,11 @@ def parse():
     ap.add_argument("--settle-s", type=float, default=0.5,
                     help="wall seconds of attention-only calls before the timed steps (reported)")
     ap.add_argument("--workload", default="mha-b16-32k")
+    ap.add_argument("--route", choices=("default", "walks", "matrix_cores"), default="default",
+                    help="kernel route of grouped-query sparse calls (mustafar_attn_set_route)")
+    ap.add_argument("--route-ab", action="store_true",
+                    help="only: the sparse attention of --workload under the walks and the matrix-core "
+                         "kernel, alternating, three rounds (same process, same box)")
     ap.add_argument("--splits", type=int, default=0, help="split-K segments (0: library default)")
     ap.add_argument("--seed", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -368,6 +373,62 @@ def workload_leg(name: str, seed: int, splits: int, flush, reps: int = 20) -> di
     return res
 
 
+ROUTES = {"default": 0, "walks": 1, "matrix_cores": 2}
+
+
+def route_ab(args) -> None:
+    """The grouped-query kernels side by side: warm sparse attention of --workload
+    with its compressed segments on the bit walks, then on the matrix-core
+    kernel (each with its own default split count), alternating, three rounds;
+    per route the median over rounds of each round's median call time and mean
+    decode-kernel time."""
+    import numpy as np
+    import torch
+
+    import paper_2505_22913_amd as mf
+    from paper_2505_22913_amd import synth
+    w = synth.WORKLOADS[args.workload]
+    dev = "cuda"
+    K, V = synth.make_kv_torch(w.B, w.Hkv, w.N + w.n_tail, w.d, seed=args.seed, device=dev)
+    gq = torch.Generator(device=dev)
+    gq.manual_seed(args.seed)
+    q = torch.randn((w.B, w.Hq, w.d), generator=gq, device=dev).half()
+    Kc = mf.CompressedCache(w.B, w.Hkv, w.d, w.sK, w.N, device=dev)
+    Vc = mf.CompressedCache(w.B, w.Hkv, w.d, w.sV, w.N, device=dev)
+    win = mf.DenseWindow(w.B, w.Hkv, w.d, w.n_tail, device=dev)
+    ws_c = torch.empty(mf.mustafar_compress_workspace_bytes(w.B, w.Hkv, w.N + w.n_tail),
+                       dtype=torch.uint8, device=dev)
+    mf.mustafar_window_prefill(win, Kc, Vc, K, V, [w.N + w.n_tail] * w.B, ws_c)
+    del K, V
+    out = torch.empty((w.B, w.Hq, w.d), dtype=torch.float16, device=dev)
+    torch.cuda.synchronize()
+    k_len = int(Kc.stream_len.to(torch.int64).sum().item())
+    v_len = int(Vc.stream_len.to(torch.int64).sum().item())
+    alg = attn_alg_bytes(w, k_len, v_len, w.N)
+    res = {name: {"call_us": [], "kernel_us": []} for name in ("walks", "matrix_cores")}
+    try:
+        for _ in range(3):
+            for name in res:
+                mf.mustafar_attn_set_route(ROUTES[name])
+                splits = mf.mustafar_attn_default_splits(w.B, w.Hq, w.Hkv, w.N)
+                ws_a = torch.empty(mf.mustafar_attn_workspace_bytes(w.B, w.Hq, w.Hkv, w.d, w.N, splits),
+                                   dtype=torch.uint8, device=dev)
+                st = timed_calls(lambda: mf.mustafar_window_decode_attn(q, Kc, Vc, win, out=out,
+                                                                        n_splits=splits, ws=ws_a), 20)
+                res[name]["splits"] = splits
+                res[name]["call_us"].append(st["median"])
+                res[name]["kernel_us"].append(st["kernel_us"])
+                del ws_a
+    finally:
+        mf.mustafar_attn_set_route(ROUTES["default"])
+    for name, r in res.items():
+        r["call_us_median"] = float(np.median(r["call_us"]))
+        r["kernel_us_median"] = float(np.median(r["kernel_us"]))
+        r["kernel_gb_s"] = alg / (r["kernel_us_median"] * 1e-6) / 1e9
+    print(json.dumps({"route_ab": res, "workload": w.name, "q_heads_per_kv_head": w.G, "alg_bytes": alg,
+                      "default": "matrix_cores" if w.G >= 8 else "walks"}), flush=True)
+
+
 def attn_only(args) -> None:
     """Warm sparse attention calls of --workload alone (for rocprofv3 kernel traces
     and counters of the attention kernels)."""
@@ -396,7 +457,7 @@ def attn_only(args) -> None:
     alg = attn_alg_bytes(w, k_len, v_len, w.N)
     st = timed_calls(lambda: mf.mustafar_window_decode_attn(q, Kc, Vc, win, out=out, n_splits=args.splits,
                                                             ws=ws_a), args.attn_reps)
-    print(json.dumps({"workload": w.name, "attention_us": st, "alg_bytes": alg,
+    print(json.dumps({"workload": w.name, "route": args.route, "attention_us": st, "alg_bytes": alg,
                       "gb_s": alg / (st["mean"] * 1e-6) / 1e9,
                       "frac": alg / (st["mean"] * 1e-6) / 1e9 / HBM_PEAK_GBS}), flush=True)
 
@@ -418,6 +479,10 @@ def main():
     from paper_2505_22913_amd import synth
 
     torch.cuda.set_device(0)
+    if args.route_ab:
+        route_ab(args)
+        return
+    mf.mustafar_attn_set_route(ROUTES[args.route])
     if args.attn_only:
         attn_only(args)
         return

@@ -272,8 +272,27 @@ enum mustafar_attn_kind {
  * 4 query heads per kv-head (the same bit walks), about 4096 workgroups of at
  * least 256 tokens; with 8 (the matrix-core kernel), about 2048 of at least
  * 128; the dense kernel with grouped queries about 4096 of at least 128.
- * Returns 1 for invalid arguments or kind. */
+ * With a route other than the default (mustafar_attn_set_route), the split
+ * count follows the kernel the route picks. Returns 1 for invalid arguments
+ * or kind. */
 int mustafar_attn_default_splits(int B, int Hq, int Hkv, int n_tokens, int kind);
+
+/* Kernel route of the sparse calls with grouped queries (2, 4 or 8 query heads
+ * per kv-head; one head always takes the bit walks). DEFAULT: the bit walks
+ * below 8 query heads per kv-head, the matrix-core kernel (zero-filled tiles
+ * contracted with v_mfma) from 8 on, the faster of the two on MI355X at each
+ * group size; WALKS and MATRIX_CORES force one kernel for every group size,
+ * for comparing them. Both give the same results up to rounding (each within
+ * the attention tolerance of the reference). The setting is process-wide and
+ * takes effect for calls issued after it; it is not synchronized with calls
+ * in flight on other threads. Errors: EINVAL (unknown route). */
+enum mustafar_route {
+    MUSTAFAR_ROUTE_DEFAULT = 0,
+    MUSTAFAR_ROUTE_WALKS = 1,
+    MUSTAFAR_ROUTE_MATRIX_CORES = 2
+};
+int mustafar_attn_set_route(int route);
+int mustafar_attn_route(void);
 
 /* Device workspace for the decode-attention calls: fp32 partial results
  * (running max, running sum, d accumulators) for n_splits token ranges plus

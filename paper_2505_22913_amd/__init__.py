@@ -153,6 +153,8 @@ _SIGS = {
     "mustafar_stream_read_sink_bytes": (ctypes.c_size_t, []),
     "mustafar_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                                             ctypes.c_void_p]),
+    "mustafar_attn_set_route": (ctypes.c_int, [ctypes.c_int]),
+    "mustafar_attn_route": (ctypes.c_int, []),
     "mustafar_kernel_timing_start": (ctypes.c_int, []),
     "mustafar_kernel_timing_stop": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int)]),
     "mustafar_stream_mix": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
@@ -547,6 +549,18 @@ def mustafar_window_step_grouped(win: DenseWindow, Kc: CompressedCache, Vc: Comp
     _check("mustafar_window_step_grouped", lib().mustafar_window_step_grouped(
         ctypes.byref(win.desc), ctypes.byref(Kc.desc), ctypes.byref(Vc.desc), _dptr(k_new),
         _dptr(v_new), _dptr(active), _dptr(acc), _stream(stream)))
+
+
+ROUTE_DEFAULT, ROUTE_WALKS, ROUTE_MATRIX_CORES = 0, 1, 2
+
+
+def mustafar_attn_set_route(route: int) -> None:
+    """Kernel route of grouped-query sparse calls (ROUTE_DEFAULT, ROUTE_WALKS, ROUTE_MATRIX_CORES)."""
+    _check("mustafar_attn_set_route", lib().mustafar_attn_set_route(int(route)))
+
+
+def mustafar_attn_route() -> int:
+    return lib().mustafar_attn_route()
 
 
 def mustafar_kernel_timing_start() -> None:

@@ -4,6 +4,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <mutex>
 
 #include "mf_launch.h"
@@ -38,6 +39,18 @@ constexpr int kSegAlign = 64;              // segments are whole 64-token blocks
 constexpr int kKeyWeightSteps = 32;        // output-aware keys: the current and 31 next queries
 static_assert(MUSTAFAR_LOOKBACK_POLLS == mf::kLookbackPolls, "look-back bound");
 static_assert(MUSTAFAR_STREAM_POISONED == mf::kStreamPoisoned, "poisoned stream marker");
+
+// Kernel route of grouped queries (mustafar_attn_set_route), process-wide.
+std::atomic<int> g_route{MUSTAFAR_ROUTE_DEFAULT};
+
+// Whether a sparse call with G query heads per kv-head runs its compressed
+// segments on the matrix-core kernel.
+bool mfma_route(int G, int route) {
+  if (G < 2) return false;
+  if (route == MUSTAFAR_ROUTE_WALKS) return false;
+  if (route == MUSTAFAR_ROUTE_MATRIX_CORES) return true;
+  return G >= kMfmaMinGroup;
+}
 
 bool aligned(const void* p, uintptr_t a) { return p && ((uintptr_t)p % a) == 0; }
 bool head_dim_ok(int d) { return d == 64 || d == 128 || d == 256; }
@@ -422,17 +435,27 @@ int mustafar_query_lookahead(const void* q, int B, int Hq, int Hkv, int n_q, int
                                               (float*)w, (hipStream_t)stream));
 }
 
+int mustafar_attn_set_route(int route) {
+  if (route != MUSTAFAR_ROUTE_DEFAULT && route != MUSTAFAR_ROUTE_WALKS && route != MUSTAFAR_ROUTE_MATRIX_CORES)
+    return MUSTAFAR_EINVAL;
+  g_route.store(route, std::memory_order_relaxed);
+  return MUSTAFAR_OK;
+}
+
+int mustafar_attn_route(void) { return g_route.load(std::memory_order_relaxed); }
+
 int mustafar_attn_default_splits(int B, int Hq, int Hkv, int n_tokens, int kind) {
   if (B < 1 || Hkv < 1 || Hq < Hkv || n_tokens < 1) return 1;
   if (kind != MUSTAFAR_ATTN_SPARSE && kind != MUSTAFAR_ATTN_DENSE) return 1;
   const bool grouped_q = Hq / Hkv >= 2;
+  const bool mfma = mfma_route(Hq / Hkv, g_route.load(std::memory_order_relaxed));
   const int64_t target = !grouped_q ? kWalkTargetGroups
                          : kind == MUSTAFAR_ATTN_DENSE ? kDenseGroupedTargetGroups
-                         : Hq / Hkv >= kMfmaMinGroup   ? kMfmaTargetGroups
+                         : mfma                        ? kMfmaTargetGroups
                                                        : kWalkGroupedTargetGroups;
   const int min_seg = !grouped_q ? kWalkMinSegTokens
-                      : (kind == MUSTAFAR_ATTN_SPARSE && Hq / Hkv < kMfmaMinGroup) ? kWalkGroupedMinSegTokens
-                                                                                 : kGroupedMinSegTokens;
+                      : (kind == MUSTAFAR_ATTN_SPARSE && !mfma) ? kWalkGroupedMinSegTokens
+                                                                : kGroupedMinSegTokens;
   const int64_t streams = (int64_t)B * Hkv;
   int64_t want = (target + streams - 1) / streams;
   const int64_t most = ((int64_t)n_tokens + min_seg - 1) / min_seg;
@@ -481,6 +504,7 @@ static int decode_common(const void* q, int B, int Hq, int Hkv, int d, int n_s, 
 
   sh->BHkv = B * Hkv;
   sh->G = G;
+  sh->mfma = dense_is_window && mfma_route(G, g_route.load(std::memory_order_relaxed));
   sh->T = d / kTile;
   sh->n_s = n_s;
   sh->n_dense = n_dense;

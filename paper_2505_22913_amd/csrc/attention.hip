@@ -821,9 +821,14 @@ static hipError_t attention_TG(const AttnShape& sh, const AttnArgs& a, uint16_t*
   hipError_t e;
   timing_mark(s, false);
   if (sh.n_sparse_segs > 0) {
-    // Grouped queries contract on the matrix cores (attention_mfma.hip).
-    if constexpr (G >= kMfmaMinGroup) e = launch_sparse_mfma(sh, a, s);
-    else e = sparse_stage<T, G>(sh, a, s);
+    // Grouped queries contract on the matrix cores (attention_mfma.hip) when
+    // the route says so (by default from kMfmaMinGroup heads per kv-head on).
+    if constexpr (G >= 2) {
+      if (sh.mfma) e = launch_sparse_mfma(sh, a, s);
+      else e = sparse_stage<T, G>(sh, a, s);
+    } else {
+      e = sparse_stage<T, G>(sh, a, s);
+    }
   } else if (sh.n_s == 0 && sh.n_dense_segs > 0 && a.K.bitmaps != nullptr) {
     // Sparse call with an empty compressed cache: only the window segment.
     e = sparse_launch<T, G, 4>(sh, a, s);

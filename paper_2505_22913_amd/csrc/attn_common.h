@@ -513,9 +513,9 @@ inline int side_token_bound(int d, const SparseSide& s, int NB) {
   return s.group_keep >= 0 ? grouped_token_bound(d, s.group_keep, NB) : token_max_elems_dev(d, s.n_keep);
 }
 
-// The MFMA kernel for grouped queries (attention_mfma.hip; G in {2, 4, 8}); the
-// sparse call uses it from kMfmaMinGroup query heads per kv-head on, the walks
-// below that. Measured on one box (d = 128, 70/70, best split count of each):
+// The MFMA kernel for grouped queries (attention_mfma.hip; G in {2, 4, 8}); by
+// default the sparse call uses it from kMfmaMinGroup query heads per kv-head
+// on, the walks below that (mustafar_attn_set_route overrides the choice). Measured on one box (d = 128, 70/70, best split count of each):
 // at G = 2 the walks take 47 us against 58 (16K tokens, 32 streams), at G = 4
 // 58 against 57 (16K) and 86 against 99 (128K, 8 streams), at G = 8 85 against
 // 59: the matrix cores pay from eight query heads per kv-head on, where each

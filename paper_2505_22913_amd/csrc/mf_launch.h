@@ -163,6 +163,8 @@ struct AttnShape {
   // If set, the final merge also writes each query head's log-sum-exp of the
   // scores in the log2 domain, m + log2(l), to lse2 [BHq].
   float* lse2 = nullptr;
+  // Compressed segments on the matrix-core kernel (G >= 2) instead of the walks.
+  bool mfma = false;
 };
 
 // Split-K merge in two levels when a single level would run on too few

@@ -70,6 +70,10 @@ WORKLOADS = {
     "mha-b16-32k": Workload("mha-b16-32k", B=16, Hq=32, Hkv=32, N=32768, d=128, sK=0.5, sV=0.7),
     "gqa-128k-decode": Workload("gqa-128k-decode", B=1, Hq=32, Hkv=8, N=131072, d=128,
                                 sK=0.7, sV=0.7, decode_steps=256),
+    # Group-size points around the Llama-3-8B shape (32 streams of 16K tokens,
+    # 70/70) with 2 and 8 query heads per kv-head, for comparing the kernels.
+    "gqa2-b4-16k": Workload("gqa2-b4-16k", B=4, Hq=16, Hkv=8, N=16384, d=128, sK=0.7, sV=0.7),
+    "gqa8-b4-16k": Workload("gqa8-b4-16k", B=4, Hq=64, Hkv=8, N=16384, d=128, sK=0.7, sV=0.7),
 }
 
 

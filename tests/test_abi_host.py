@@ -485,3 +485,23 @@ def test_stream_mix_helper_rejects_bad_arguments(lib):
 
 def test_kernel_timing_stop_rejects_null(lib):
     assert lib.mustafar_kernel_timing_stop(None, None) == mf.EINVAL
+
+
+def test_attn_route_setting(lib):
+    # The route is host state: unknown routes are rejected, the setting sticks
+    # and steers the default split count to the chosen kernel's.
+    assert lib.mustafar_attn_set_route(3) == mf.EINVAL
+    assert lib.mustafar_attn_set_route(-1) == mf.EINVAL
+    try:
+        assert lib.mustafar_attn_set_route(mf.ROUTE_WALKS) == 0
+        assert lib.mustafar_attn_route() == mf.ROUTE_WALKS
+        walks = lib.mustafar_attn_default_splits(1, 64, 8, 131072, 0)   # 8 streams, G = 8
+        assert lib.mustafar_attn_set_route(mf.ROUTE_MATRIX_CORES) == 0
+        cores = lib.mustafar_attn_default_splits(1, 64, 8, 131072, 0)
+        cores_g2 = lib.mustafar_attn_default_splits(1, 16, 8, 131072, 0)
+    finally:
+        assert lib.mustafar_attn_set_route(mf.ROUTE_DEFAULT) == 0
+    assert (walks, cores) == (512, 256)   # 4096 and 2048 workgroups over 8 streams
+    assert lib.mustafar_attn_default_splits(1, 64, 8, 131072, 0) == cores   # default: cores at G = 8
+    assert lib.mustafar_attn_default_splits(1, 16, 8, 131072, 0) == walks   # default: walks at G = 2
+    assert cores_g2 == cores

@@ -281,3 +281,24 @@ def test_kernel_timing_counts_main_kernels():
     mf.mustafar_kernel_timing_start()
     ms2, n2 = mf.mustafar_kernel_timing_stop()
     assert n2 == 0 and ms2 == 0.0
+
+
+@pytest.fixture
+def route():
+    """Sets a kernel route for one test and restores the default afterwards."""
+    def set_route(r):
+        mf.mustafar_attn_set_route(r)
+    yield set_route
+    mf.mustafar_attn_set_route(mf.ROUTE_DEFAULT)
+
+
+@pytest.mark.parametrize("kernel", ["walks", "matrix_cores"])
+@pytest.mark.parametrize("G", [2, 4, 8])
+@pytest.mark.parametrize("d", [64, 128, 256])
+def test_attention_both_grouped_kernels(route, kernel, G, d):
+    # Either kernel serves every group size (the default picks one per size):
+    # both meet the oracle, over several blocks, a ragged tail and a window.
+    route(mf.ROUTE_WALKS if kernel == "walks" else mf.ROUTE_MATRIX_CORES)
+    announce(f"route {kernel} G={G} d={d}")
+    _attn_case(B=2, Hkv=2, G=G, Ns=517, Nd=32, d=d, sK=0.5, sV=0.7, splits=0, seed=40 + G + d)
+    _attn_case(B=1, Hkv=2, G=G, Ns=1000, Nd=0, d=d, sK=0.7, sV=0.7, splits=3, seed=41 + G + d)
