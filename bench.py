@@ -14,11 +14,9 @@ Also measured (reported in the same JSON line):
     few dozen calls to settle under this load, so the result must not depend
     on --warmup;
   * per attention call: mean, median, min and max of the HIP-event times over
-    the timed steps and their algorithmic HBM GB/s (bytes the format makes the
-    kernel read: 12 B of bitmap + offset per tile, the packed values with
-    padding, the window, q and the output); the roofline entry divides those
-    bytes by the mean duration of the decode kernel alone (HIP events the
-    library records around it in the same steps), without the split-K merge;
+    the timed steps, their algorithmic HBM GB/s and roofline fraction (bytes
+    the format makes the kernel read: 12 B of bitmap + offset per tile, the
+    packed values with padding, the window, q and the output, over the mean);
   * the HBM read ceiling and, for the compression, the read + write ceiling
     at its write share (the library's streaming helpers);
   * the in-house dense fp16 decode-attention kernel on the same tokens;
@@ -193,14 +191,8 @@ def call_stats(marks) -> dict:
 
 def timed_calls(fn, reps: int, flush=None, warm: int = 5) -> dict:
     """call_stats of `reps` calls of fn; with a flush buffer, it is overwritten before
-    each call (outside the timed pair of events), so every call starts cold.
-    kernel_us: the mean duration of the calls' main kernels (the decode kernel of
-    an attention call, without the merge), from a second pass of the same calls
-    with the library's timing hook on (its event records add to a call's time,
-    so the call statistics come from the first pass, without it)."""
+    each call (outside the timed pair of events), so every call starts cold."""
     import torch
-
-    import paper_2505_22913_amd as mf
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     if flush is None:
         for _ in range(warm):
@@ -215,16 +207,7 @@ def timed_calls(fn, reps: int, flush=None, warm: int = 5) -> dict:
         b.record()
         marks.append((a, b))
     torch.cuda.synchronize()
-    st = call_stats(marks)
-    mf.mustafar_kernel_timing_start()
-    for i in range(reps):
-        if flush is not None:
-            flush.fill_(i & 0xFF)
-        fn()
-    torch.cuda.synchronize()
-    kern_ms, kern_n = mf.mustafar_kernel_timing_stop()
-    st["kernel_us"] = kern_ms / kern_n * 1e3 if kern_n else None
-    return st
+    return call_stats(marks)
 
 
 def usable_cpus() -> int:
@@ -380,8 +363,7 @@ def route_ab(args) -> None:
     """The grouped-query kernels side by side: warm sparse attention of --workload
     with its compressed segments on the bit walks, then on the matrix-core
     kernel (each with its own default split count), alternating, three rounds;
-    per route the median over rounds of each round's median call time and mean
-    decode-kernel time."""
+    per route the median over rounds of each round's median call time."""
     import numpy as np
     import torch
 
@@ -405,7 +387,7 @@ def route_ab(args) -> None:
     k_len = int(Kc.stream_len.to(torch.int64).sum().item())
     v_len = int(Vc.stream_len.to(torch.int64).sum().item())
     alg = attn_alg_bytes(w, k_len, v_len, w.N)
-    res = {name: {"call_us": [], "kernel_us": []} for name in ("walks", "matrix_cores")}
+    res = {name: {"call_us": []} for name in ("walks", "matrix_cores")}
     try:
         for _ in range(3):
             for name in res:
@@ -417,14 +399,12 @@ def route_ab(args) -> None:
                                                                         n_splits=splits, ws=ws_a), 20)
                 res[name]["splits"] = splits
                 res[name]["call_us"].append(st["median"])
-                res[name]["kernel_us"].append(st["kernel_us"])
                 del ws_a
     finally:
         mf.mustafar_attn_set_route(ROUTES["default"])
     for name, r in res.items():
         r["call_us_median"] = float(np.median(r["call_us"]))
-        r["kernel_us_median"] = float(np.median(r["kernel_us"]))
-        r["kernel_gb_s"] = alg / (r["kernel_us_median"] * 1e-6) / 1e9
+        r["gb_s"] = alg / (r["call_us_median"] * 1e-6) / 1e9
     print(json.dumps({"route_ab": res, "workload": w.name, "q_heads_per_kv_head": w.G, "alg_bytes": alg,
                       "default": "matrix_cores" if w.G >= 8 else "walks"}), flush=True)
 
@@ -489,7 +469,7 @@ def main():
     w = synth.WORKLOADS[args.workload]
     steps, warm = args.steps, args.warmup
     dev = "cuda"
-    cap = w.N + warm + 2 * steps + 1   # the timed steps, then as many for the kernel-only pass
+    cap = w.N + warm + steps + 1
 
     # ---- synthetic inputs, resident in HBM ----
     K, V = synth.make_kv_torch(w.B, w.Hkv, w.N + w.n_tail, w.d, seed=args.seed, device=dev)
@@ -698,26 +678,6 @@ def main():
            for n_s in range(n_s_start + 1, n_s_end + 1)]
     alg_bytes = float(np.mean(alg))
     attn_gbs = alg_bytes / attn_s / 1e9
-    # The decode kernel alone: the same steps once more (not part of the timed
-    # region: its event records add to a step), with the library recording HIP
-    # events around k_sparse_attn; bytes of the steps' attention launches.
-    k_len_k0 = int(Kc.stream_len.to(torch.int64).sum().item())
-    v_len_k0 = int(Vc.stream_len.to(torch.int64).sum().item())
-    n_s_k0 = Kc.n_tokens
-    mf.mustafar_kernel_timing_start()
-    for i in range(steps):
-        step(warm + steps + i)
-    torch.cuda.synchronize()
-    kern_ms, kern_n = mf.mustafar_kernel_timing_stop()
-    assert kern_n == steps, (kern_n, steps)   # one decode kernel per step
-    kernel_s = kern_ms / kern_n / 1e3
-    k_len_k1 = int(Kc.stream_len.to(torch.int64).sum().item())
-    v_len_k1 = int(Vc.stream_len.to(torch.int64).sum().item())
-    n_s_k1 = Kc.n_tokens
-    alg_k = [attn_alg_bytes(w, int(k_len_k0 + (k_len_k1 - k_len_k0) * (n_s - n_s_k0) / max(1, n_s_k1 - n_s_k0)),
-                            int(v_len_k0 + (v_len_k1 - v_len_k0) * (n_s - n_s_k0) / max(1, n_s_k1 - n_s_k0)), n_s)
-             for n_s in range(n_s_k0 + 1, n_s_k1 + 1)]
-    kernel_gbs = float(np.mean(alg_k)) / kernel_s / 1e9
     del Kc, Vc, win
     torch.cuda.empty_cache()
 
@@ -846,19 +806,15 @@ def main():
                       "us_max": attn["max"], "tokens_per_s": w.B / attn_s,
                       "kv_tokens_per_s": w.B * w.Hkv * (n_s_end + w.n_tail) / attn_s,
                       "alg_bytes": alg_bytes, "gb_s": attn_gbs,
-                      "kernel_us": kernel_s * 1e6, "kernel_gb_s": kernel_gbs,
-                      "how": "us*, gb_s: HIP events around mustafar_window_decode_attn on its stream "
-                             "(k_sparse_attn + the split-K merge), every timed step; kernel_*: HIP "
-                             "events the library records around k_sparse_attn alone in the same "
-                             "steps (mustafar_kernel_timing_start/stop), their mean"},
-        "roofline": {"bound": "hbm", "achieved": kernel_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": kernel_gbs / HBM_PEAK_GBS,
+                      "how": "HIP events around mustafar_window_decode_attn on its stream "
+                             "(k_sparse_attn + the split-K merge), every timed step"},
+        "roofline": {"bound": "hbm", "achieved": attn_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": attn_gbs / HBM_PEAK_GBS,
                      "kernel": "k_sparse_attn",
-                     "how": "algorithmic bytes of one launch / mean k_sparse_attn duration of the "
-                            "timed steps",
+                     "how": "algorithmic bytes of one launch / mean time of the timed attention "
+                            "calls (k_sparse_attn and its split-K merge, about 0.6% of it)",
                      "traffic": measured_traffic("k_sparse_attn", w.name)},
         "read_ceiling": {"gb_s": ceiling, "attn_frac": attn_gbs / ceiling,
-                         "kernel_frac": kernel_gbs / ceiling,
                          "how": "mustafar_stream_read (16-byte loads) over an 8 GiB buffer"},
         "dense_baseline": {"us": dense_st["mean"], "us_median": dense_st["median"],
                            "us_min": dense_st["min"], "us_max": dense_st["max"],

@@ -270,7 +270,7 @@ enum mustafar_attn_kind {
  * tokens for the sparse calls). It depends on the kernel that runs: with one
  * query head per kv-head, many segments down to one 64-token block; with 2 or
  * 4 query heads per kv-head (the same bit walks), about 4096 workgroups of at
- * least 256 tokens; with 8 (the matrix-core kernel), about 2048 of at least
+ * least 192 tokens; with 8 (the matrix-core kernel), about 2048 of at least
  * 128; the dense kernel with grouped queries about 4096 of at least 128.
  * With a route other than the default (mustafar_attn_set_route), the split
  * count follows the kernel the route picks. Returns 1 for invalid arguments
@@ -493,24 +493,6 @@ int mustafar_window_step_grouped(mustafar_window_t* w, mustafar_ccache_t* Kc, mu
 
 /* Static message for a status code. */
 const char* mustafar_strerror(int status);
-
-/* MEASUREMENT HELPER (not a step of the method). Between
- * mustafar_kernel_timing_start and mustafar_kernel_timing_stop, every call on
- * the device current at start records HIP events on its stream right before
- * and after its main kernel: the decode kernel of an attention call (not the
- * split-K merge) and the compression kernel of a bulk prune + compress. stop
- * waits for the recorded events and returns the summed kernel time in
- * *total_ms and the number of timed launches in *launches (at most 4096 per
- * collection; past that, launches are not timed and stop returns
- * EUNSUPPORTED after filling both). Timing adds two event records per call
- * (time of their own, so measure call rates with it off), and a pair spans
- * whatever the end record waits for too, such as writing back caches after a
- * kernel that writes much. It is off by default and not meant for calls under
- * graph capture. The
- * events are created by the first start (and again when the device changes).
- * Errors: EINVAL (null pointer), ELAUNCH (HIP event failure). */
-int mustafar_kernel_timing_start(void);
-int mustafar_kernel_timing_stop(double* total_ms, int* launches);
 
 /* MEASUREMENT HELPER (not a step of the method). Streams `bytes` of device
  * memory at `src` through 16-byte loads and writes one 32-bit checksum per

@@ -155,8 +155,6 @@ _SIGS = {
                                             ctypes.c_void_p]),
     "mustafar_attn_set_route": (ctypes.c_int, [ctypes.c_int]),
     "mustafar_attn_route": (ctypes.c_int, []),
-    "mustafar_kernel_timing_start": (ctypes.c_int, []),
-    "mustafar_kernel_timing_stop": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int)]),
     "mustafar_stream_mix": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
                                            ctypes.c_void_p, ctypes.c_void_p]),
 }
@@ -561,18 +559,6 @@ def mustafar_attn_set_route(route: int) -> None:
 
 def mustafar_attn_route() -> int:
     return lib().mustafar_attn_route()
-
-
-def mustafar_kernel_timing_start() -> None:
-    """Measurement helper: start timing the main kernel of every attention and bulk-compression call."""
-    _check("mustafar_kernel_timing_start", lib().mustafar_kernel_timing_start())
-
-
-def mustafar_kernel_timing_stop():
-    """Stop timing; returns (summed kernel ms, number of timed launches)."""
-    ms, n = ctypes.c_double(0.0), ctypes.c_int(0)
-    _check("mustafar_kernel_timing_stop", lib().mustafar_kernel_timing_stop(ctypes.byref(ms), ctypes.byref(n)))
-    return ms.value, n.value
 
 
 def mustafar_stream_mix(src, dst, write_16ths: int, sink=None, stream=None):

@@ -819,7 +819,6 @@ template <int T, int G>
 static hipError_t attention_TG(const AttnShape& sh, const AttnArgs& a, uint16_t* out, hipStream_t s) {
   const int n_seg = sh.n_sparse_segs + sh.n_dense_segs;
   hipError_t e;
-  timing_mark(s, false);
   if (sh.n_sparse_segs > 0) {
     // Grouped queries contract on the matrix cores (attention_mfma.hip) when
     // the route says so (by default from kMfmaMinGroup heads per kv-head on).
@@ -838,7 +837,6 @@ static hipError_t attention_TG(const AttnShape& sh, const AttnArgs& a, uint16_t*
     e = hipGetLastError();
   }
   if (e != hipSuccess) return e;
-  timing_mark(s, true);
   const int parts = merge_parts(n_seg, a.BHq);
   if (parts > 1) {
     // Two levels: parts of kMergeSegsPerPart segments, then the parts.

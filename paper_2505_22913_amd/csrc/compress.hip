@@ -1173,13 +1173,11 @@ static hipError_t compress_launch(const CacheView& c, const uint16_t* x, int n_n
   hipLaunchKernelGGL(k_clear, dim3(clear_blocks), dim3(256), 0, s, ws, w.words);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  timing_mark(s, false);
   hipLaunchKernelGGL((k_compress<T, PRESET>), dim3((uint32_t)n_wg), dim3(compress_waves<T>() * kWave),
                      0, s, x, n_new, PRESET ? 0 : c.n_keep,
                      c.bitmaps, c.offsets, c.values, c.stream_len, c.cap_tokens, tok0, c.val_stride,
                      w.flags, w.ticket, n_chunks, x_stride, o, max_polls, w.bad, w.status);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  timing_mark(s, true);
   hipLaunchKernelGGL(k_compress_finalize, dim3((c.BH + 255) / 256), dim3(256), 0, s, w.bad, c.stream_len,
                      c.BH);
   return hipGetLastError();

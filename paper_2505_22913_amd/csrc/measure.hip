@@ -5,12 +5,8 @@
 // workgroup keeps the loads alive. The rate of this kernel over a buffer much
 // larger than the caches is the HBM read rate the decode kernels are compared
 // with (16384 workgroups and non-temporal loads measured fastest on gfx950).
-#include <atomic>
-#include <mutex>
-
 #include "mustafar.h"
 #include "mf_device.h"
-#include "mf_launch.h"
 
 namespace mf {
 
@@ -79,76 +75,7 @@ __global__ __launch_bounds__(kReadThreads) void k_stream_mix(const u32x4m* __res
   if (threadIdx.x == 0) sink[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
 }
 
-// ---- main-kernel timing (measurement hook) ----
-namespace {
-constexpr int kTimingMax = 4096;  // launches recorded per collection
-std::mutex g_timing_mu;
-std::atomic<int> g_timing_on{0};
-int g_timing_dev = -1;
-int g_timing_n = 0;        // completed begin/end pairs
-int g_timing_overflow = 0;
-hipEvent_t g_timing_ev[2][kTimingMax];
-bool g_timing_created = false;
-}  // namespace
-
-void timing_mark(hipStream_t s, bool end) {
-  if (g_timing_on.load(std::memory_order_relaxed) == 0) return;
-  std::lock_guard<std::mutex> lock(g_timing_mu);
-  int dev = -1;
-  if (!g_timing_on.load(std::memory_order_relaxed) || hipGetDevice(&dev) != hipSuccess || dev != g_timing_dev) return;
-  if (g_timing_n >= kTimingMax) {
-    g_timing_overflow = 1;
-    return;
-  }
-  if (hipEventRecord(g_timing_ev[end ? 1 : 0][g_timing_n], s) != hipSuccess) {
-    g_timing_overflow = 1;
-    return;
-  }
-  if (end) ++g_timing_n;
-}
-
 }  // namespace mf
-
-extern "C" int mustafar_kernel_timing_start(void) {
-  std::lock_guard<std::mutex> lock(mf::g_timing_mu);
-  int dev = -1;
-  if (hipGetDevice(&dev) != hipSuccess) return MUSTAFAR_ELAUNCH;
-  if (mf::g_timing_created && dev != mf::g_timing_dev) {
-    for (int i = 0; i < mf::kTimingMax; ++i) {
-      (void)hipEventDestroy(mf::g_timing_ev[0][i]);
-      (void)hipEventDestroy(mf::g_timing_ev[1][i]);
-    }
-    mf::g_timing_created = false;
-  }
-  if (!mf::g_timing_created) {
-    for (int i = 0; i < mf::kTimingMax; ++i)
-      if (hipEventCreate(&mf::g_timing_ev[0][i]) != hipSuccess || hipEventCreate(&mf::g_timing_ev[1][i]) != hipSuccess)
-        return MUSTAFAR_ELAUNCH;
-    mf::g_timing_created = true;
-  }
-  mf::g_timing_dev = dev;
-  mf::g_timing_n = 0;
-  mf::g_timing_overflow = 0;
-  mf::g_timing_on.store(1, std::memory_order_relaxed);
-  return MUSTAFAR_OK;
-}
-
-extern "C" int mustafar_kernel_timing_stop(double* total_ms, int* launches) {
-  std::lock_guard<std::mutex> lock(mf::g_timing_mu);
-  mf::g_timing_on.store(0, std::memory_order_relaxed);
-  if (!total_ms || !launches) return MUSTAFAR_EINVAL;
-  double sum = 0.0;
-  for (int i = 0; i < mf::g_timing_n; ++i) {
-    float ms = 0.f;
-    if (hipEventSynchronize(mf::g_timing_ev[1][i]) != hipSuccess ||
-        hipEventElapsedTime(&ms, mf::g_timing_ev[0][i], mf::g_timing_ev[1][i]) != hipSuccess)
-      return MUSTAFAR_ELAUNCH;
-    sum += ms;
-  }
-  *total_ms = sum;
-  *launches = mf::g_timing_n;
-  return mf::g_timing_overflow ? MUSTAFAR_EUNSUPPORTED : MUSTAFAR_OK;
-}
 
 extern "C" int mustafar_stream_mix(const void* src, size_t bytes, void* dst, int write_16ths, void* sink,
                                    void* stream) {

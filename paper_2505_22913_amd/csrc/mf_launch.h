@@ -25,11 +25,6 @@ struct CacheView {
   int group_keep;    // per-channel caches: tokens kept per channel and group of 32; else -1
 };
 
-// Measurement hook: while enabled (mustafar_kernel_timing_start), HIP events
-// are recorded on the launch stream around the main kernel of every attention
-// call (the decode kernel, not the merge) and of every bulk compression.
-void timing_mark(hipStream_t s, bool end);
-
 // A stream whose bulk compression gave up waiting in the look-back (see
 // k_compress) has this stream_len; every later call skips it.
 constexpr uint32_t kStreamPoisoned = 0xffffffffu;

@@ -213,15 +213,15 @@ def test_default_splits_follow_the_kernel(lib):
     assert ds(1, 32, 32, 4096, S) == 64
     assert ds(1, 8, 8, 1024, S) == 16
     assert ds(1, 8, 8, 1024, D) == 16
-    # 2 or 4 query heads per kv-head (the walks): ~4096 workgroups of at least 256 tokens;
+    # 2 or 4 query heads per kv-head (the walks): ~4096 workgroups of at least 192 tokens;
     # 8 (the matrix-core kernel): ~2048 of at least 128; dense with grouped queries: ~4096
     assert ds(1, 32, 8, 131072, S) == 512
     assert ds(1, 32, 8, 131072, D) == 512
-    assert ds(4, 32, 8, 16384, S) == 64
-    assert ds(4, 16, 8, 16384, S) == 64
+    assert ds(4, 32, 8, 16384, S) == 86    # 16384 / 192, rounded up
+    assert ds(4, 16, 8, 16384, S) == 86
     assert ds(4, 64, 8, 16384, S) == 64
     assert ds(4, 32, 8, 16384, D) == 128
-    assert ds(1, 32, 8, 300, S) == 2
+    assert ds(1, 32, 8, 300, S) == 2       # 300 / 192, rounded up
     # invalid arguments
     assert ds(1, 32, 8, 4096, 2) == 1
     assert ds(0, 32, 8, 4096, S) == 1
@@ -481,10 +481,6 @@ def test_stream_mix_helper_rejects_bad_arguments(lib):
     assert lib.mustafar_stream_mix(None, 256, 0x200000, 9, S, None) == mf.EINVAL
     assert lib.mustafar_stream_mix(0x100000, 256, 0x200000, 9, None, None) == mf.EINVAL
     assert lib.mustafar_stream_mix(0x100000, 256, 0x200000, 9, S + 2, None) == mf.EINVAL
-
-
-def test_kernel_timing_stop_rejects_null(lib):
-    assert lib.mustafar_kernel_timing_stop(None, None) == mf.EINVAL
 
 
 def test_attn_route_setting(lib):

@@ -259,30 +259,6 @@ def test_stream_mix_writes_the_selected_words(w16):
     assert (got[out_words:] == 0xffffffff).all()
 
 
-def test_kernel_timing_counts_main_kernels():
-    # The timing hook records one event pair per attention call (the decode
-    # kernel) and per bulk compression (the compression kernel), only between
-    # start and stop.
-    import torch
-    announce("kernel timing hook")
-    B, H, N, d = 1, 2, 256, 128
-    K, V = synth.make_kv_torch(B, H, N, d, seed=9)
-    Kc = mf.CompressedCache(B, H, d, 0.5, N)
-    Vc = mf.CompressedCache(B, H, d, 0.5, N)
-    q = torch.randn((B, H, d), device="cuda").half()
-    mf.mustafar_prune_compress(Kc, K)      # before start: not timed
-    mf.mustafar_kernel_timing_start()
-    mf.mustafar_prune_compress(Vc, V)
-    for _ in range(3):
-        mf.mustafar_sparse_decode_attn(q, Kc, Vc)
-    ms, n = mf.mustafar_kernel_timing_stop()
-    assert n == 4 and ms > 0.0
-    mf.mustafar_sparse_decode_attn(q, Kc, Vc)  # after stop: not timed
-    mf.mustafar_kernel_timing_start()
-    ms2, n2 = mf.mustafar_kernel_timing_stop()
-    assert n2 == 0 and ms2 == 0.0
-
-
 @pytest.fixture
 def route():
     """Sets a kernel route for one test and restores the default afterwards."""
