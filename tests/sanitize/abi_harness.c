@@ -49,6 +49,19 @@ int main(void) {
     (void)mustafar_compress_workspace_bytes(INT_MAX, INT_MAX, INT_MAX);
     (void)mustafar_attn_workspace_bytes(INT_MAX, INT_MAX, 1, 256, INT_MAX, 0);
     (void)mustafar_attn_default_splits(INT_MAX, INT_MAX, 1, INT_MAX, MUSTAFAR_ATTN_SPARSE);
+    /* kernel routes: every route steers the default splits, extreme sizes included */
+    EXPECT(mustafar_attn_set_route(3), MUSTAFAR_EINVAL);
+    EXPECT(mustafar_attn_set_route(-1), MUSTAFAR_EINVAL);
+    for (int r = MUSTAFAR_ROUTE_DEFAULT; r <= MUSTAFAR_ROUTE_MATRIX_CORES; ++r) {
+        EXPECT(mustafar_attn_set_route(r), MUSTAFAR_OK);
+        EXPECT(mustafar_attn_route(), r);
+        for (int g = 1; g <= 8; g *= 2) {
+            (void)mustafar_attn_default_splits(INT_MAX, 8 * g, 8, INT_MAX, MUSTAFAR_ATTN_SPARSE);
+            (void)mustafar_attn_default_splits(1, 8 * g, 8, 1, MUSTAFAR_ATTN_SPARSE);
+            (void)mustafar_attn_workspace_bytes(INT_MAX, 8 * g, 8, 256, INT_MAX, 0);
+        }
+    }
+    EXPECT(mustafar_attn_set_route(MUSTAFAR_ROUTE_DEFAULT), MUSTAFAR_OK);
     for (int st = -8; st <= 1; ++st) (void)strlen(mustafar_strerror(st));
 
     EXPECT(init_cache(&K, 2, 4, 128, 0.5f, 100), MUSTAFAR_OK);
