@@ -290,11 +290,14 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       {
-        constexpr int n16 = (int)(half_tile_bytes(T) / 16);
+        // Rows 1..32 (the channels p.V reads; row 0 only takes the walks'
+        // surplus writes): 32 rows of 128 bytes, four 16-byte stores per lane.
+        constexpr int n16 = (int)((kHalfSlots - 1) * kPvRow * 4u / 16u);
+        static_assert(n16 % kWave == 0, "whole stores per lane");
         const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int i = 0; i < (n16 + kWave - 1) / kWave; ++i)
-          if (i * kWave + (int)lane < n16) lds_store<u32x4>(base + L.dense + 16u * (i * kWave + lane), z);
+        for (int i = 0; i < n16 / kWave; ++i)
+          lds_store<u32x4>(base + L.dense + kRowB + 16u * (i * kWave + lane), z);
       }
       if (h == 0) {
         value_half<false, kRowB>(wc.vlo, vlo & kLow31, va, d_w, 0u);
@@ -607,11 +610,14 @@ __device__ __forceinline__ void sparse_body_g(const AttnArgs& a, int seg, int bh
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
       {
-        constexpr int n16 = (int)(half_tile_bytes(T) / 16);
+        // Rows 1..32 (the channels p.V reads; row 0 only takes the walks'
+        // surplus writes): 32 rows of 128 bytes, four 16-byte stores per lane.
+        constexpr int n16 = (int)((kHalfSlots - 1) * kPvRow * 4u / 16u);
+        static_assert(n16 % kWave == 0, "whole stores per lane");
         const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int i = 0; i < (n16 + kWave - 1) / kWave; ++i)
-          if (i * kWave + (int)lane < n16) lds_store<u32x4>(base + L.dense + 16u * (i * kWave + lane), z);
+        for (int i = 0; i < n16 / kWave; ++i)
+          lds_store<u32x4>(base + L.dense + kRowB + 16u * (i * kWave + lane), z);
       }
       if (hh == 0) {
         value_half<false, kRowB>(wc.vlo, vlo & kLow31, va, d_w, 0u);
