@@ -1,5 +1,7 @@
 // Decode attention over compressed K/V for grouped queries (G = 2, 4, 8 query
-// heads per kv-head) on gfx950: both contractions of Algorithm 1 on MFMA.
+// heads per kv-head) on gfx950: both contractions of Algorithm 1 on MFMA. The
+// default route takes it from 8 query heads per kv-head on (the bit walks are
+// faster below that); mustafar_attn_set_route can force it for G = 2 and 4.
 //
 // Same split-K scheme, staging and bit walks as the G = 1 kernel, but a
 // compressed block of NB = 64/T tokens is expanded twice in LDS and contracted
@@ -260,7 +262,8 @@ constexpr int mfma_waves() {
   return (T == 4 && STAGE == 16) ? 1 : 2;
 }
 
-// Sparse call with G >= 2: grid (n_sparse_segs + n_dense_segs, BHkv).
+// Sparse call on the matrix cores (G >= 2 query heads per kv-head): grid
+// (n_sparse_segs + n_dense_segs, BHkv).
 template <int T, int G, int STAGE>
 __global__ __launch_bounds__(64, (mfma_waves<T, G, STAGE>())) void k_sparse_attn_mfma(AttnArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];

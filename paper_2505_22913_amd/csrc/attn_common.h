@@ -1,5 +1,6 @@
 // Device helpers shared by the decode-attention kernels (attention.hip: the
-// bit-walk kernel for G = 1, attention_mfma.hip: the MFMA kernel for G >= 2):
+// bit-walk kernel, one or grouped query heads; attention_mfma.hip: the MFMA
+// kernel for grouped queries):
 // types, wave reductions, LDS access, the staging of compressed blocks, the
 // bit-walk primitives, the dense (window) segment body and the partial-result
 // writes of the split-K scheme.
