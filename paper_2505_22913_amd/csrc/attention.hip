@@ -177,24 +177,6 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   const uint32_t lane = lane_id();
   const uint32_t j = lane / T, t = lane % T;
 
-  // q table [t][slot]: slots 0 and 33 are the scratch slots; channels 31 and
-  // 63 read zero in the walks (their products are added once per tile).
-  {
-    const uint16_t* qsrc = a.q + (int64_t)bh * d;
-    for (int i = lane; i < T * kSlots; i += kWave) {
-      const int slot = i % kSlots, tt = i / kSlots;
-      const int c = slot < 33 ? slot - 1 : slot - 2;
-      const bool zero = slot == 0 || slot == 33 || c == 31 || c == 63;
-      uint16_t* qt = reinterpret_cast<uint16_t*>(smem + L.qtab + tt * qtab_stride(1));
-      qt[slot] = zero ? (uint16_t)0 : qsrc[kTile * tt + c];
-    }
-    // The key region follows the value region, whose last 16 bytes the commits
-    // only ever fill with zeros: zero them once, so that the element before the
-    // first key tile (which the channel-31 product of a tile with an empty lower
-    // half reads, times 0) is never stale LDS content.
-    if (lane == 0) lds_store<u32x4>(lds_addr(smem) + L.kst - 16u, (u32x4){0u, 0u, 0u, 0u});
-  }
-
   const int j0 = seg * a.sparse_seg_tokens;
   const int j1 = min(j0 + a.sparse_seg_tokens, stream_tokens(a, bh));
   if (j0 >= j1) return;  // past this stream's tokens: an empty partial
@@ -203,9 +185,47 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   const uint16_t* kv = a.K.values + (int64_t)bh * a.K.val_stride;
   const uint16_t* vv = a.V.values + (int64_t)bh * a.V.val_stride;
 
-  // Prologue: block 0 staged in LDS, metadata of block 1 in flight.
+  // q table [t][slot]: slots 0 and 33 are the scratch slots; channels 31 and
+  // 63 read zero in the walks (their products are added once per tile). Every
+  // load is issued before the first store (a zero slot loads channel 0 and
+  // discards it), and the first block's metadata loads go out with them, so
+  // that the table, this tile's q at channels 31 and 63 and the metadata cost
+  // one memory round trip.
+  constexpr int kQn = T * kSlots, kQr = (kQn + kWave - 1) / kWave;
+  const uint16_t* qrow = a.q + (int64_t)bh * d + kTile * t;
+  const _Float16 q31 = __builtin_bit_cast(_Float16, qrow[31]);
+  const _Float16 q63 = __builtin_bit_cast(_Float16, qrow[63]);
   int nb = min(NB, j1 - j0);
-  TileMeta cur = load_meta<T>(a, kt0, vt0, j0, nb, lane);
+  TileMeta cur;
+  {
+    const uint16_t* qsrc = a.q + (int64_t)bh * d;
+    uint16_t qv[kQr];
+#pragma unroll
+    for (int r = 0; r < kQr; ++r) {
+      const int i = (int)lane + r * kWave;
+      const int slot = i % kSlots, tt = i / kSlots;
+      const int c = slot < 33 ? slot - 1 : slot - 2;
+      const bool zero = i >= kQn || slot == 0 || slot == 33 || c == 31 || c == 63;
+      qv[r] = qsrc[zero ? 0 : kTile * tt + c];
+    }
+    cur = load_meta<T>(a, kt0, vt0, j0, nb, lane);
+#pragma unroll
+    for (int r = 0; r < kQr; ++r) {
+      const int i = (int)lane + r * kWave;
+      const int slot = i % kSlots, tt = i / kSlots;
+      const int c = slot < 33 ? slot - 1 : slot - 2;
+      const bool zero = slot == 0 || slot == 33 || c == 31 || c == 63;
+      uint16_t* qt = reinterpret_cast<uint16_t*>(smem + L.qtab + tt * qtab_stride(1));
+      if (i < kQn) qt[slot] = zero ? (uint16_t)0 : qv[r];
+    }
+    // The key region follows the value region, whose last 16 bytes the commits
+    // only ever fill with zeros: zero them once, so that the element before the
+    // first key tile (which the channel-31 product of a tile with an empty lower
+    // half reads, times 0) is never stale LDS content.
+    if (lane == 0) lds_store<u32x4>(lds_addr(smem) + L.kst - 16u, (u32x4){0u, 0u, 0u, 0u});
+  }
+
+  // Prologue: block 0 staged in LDS, metadata of block 1 in flight.
   Runs rcur = runs_of<T>(cur, nb);
   u32x4 stg[STAGE];
   stage_issue<STAGE>(stg, kv, vv, rcur, lane);
@@ -217,9 +237,6 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   // Per-lane constant addresses: walks (token j, tile t) ...
   const uint32_t q_w0 = base + L.qtab + t * qtab_stride(1) + 2u;
   const uint32_t q_w1 = q_w0 + 33u * 2u;
-  const uint16_t* qrow = a.q + (int64_t)bh * d + kTile * t;
-  const _Float16 q31 = __builtin_bit_cast(_Float16, qrow[31]);
-  const _Float16 q63 = __builtin_bit_cast(_Float16, qrow[63]);
   constexpr uint32_t NBH = PU::NBH;
   constexpr uint32_t kRowB = kPvRow * 4u;  // expanded-tile stride per channel
   const uint32_t d_w = base + L.dense + kRowB + (t * NBH + j % NBH) * 4u + (j / NBH) * 2u;
@@ -481,21 +498,6 @@ __device__ __forceinline__ void sparse_body_g(const AttnArgs& a, int seg, int bh
   constexpr uint32_t QTS = qtab_stride(GW);     // bytes per tile of one head group's table
   constexpr uint32_t QGS = T * QTS;             // bytes per head group
 
-  // q tables [head group][t][slot][GW heads]: slots 0 and 33 and channels 31
-  // and 63 hold zeros (the walks add channels 31 and 63 from their ranks).
-  {
-    const uint16_t* qsrc = a.q + (int64_t)bh * G * d;
-    for (int i = lane; i < G * T * kSlots; i += kWave) {
-      const int gi = i % G, rest = i / G;
-      const int slot = rest % kSlots, tt = rest / kSlots;
-      const int c = slot < 33 ? slot - 1 : slot - 2;
-      const bool zero = slot == 0 || slot == 33 || c == 31 || c == 63;
-      uint16_t* qt = reinterpret_cast<uint16_t*>(smem + L.qtab + (gi / GW) * QGS + tt * QTS + slot * QS);
-      qt[gi % GW] = zero ? (uint16_t)0 : qsrc[(int64_t)gi * d + kTile * tt + c];
-    }
-    if (lane == 0) lds_store<u32x4>(lds_addr(smem) + L.kst - 16u, (u32x4){0u, 0u, 0u, 0u});
-  }
-
   const int j0 = seg * a.sparse_seg_tokens;
   const int j1 = min(j0 + a.sparse_seg_tokens, stream_tokens(a, bh));
   if (j0 >= j1) return;
@@ -504,8 +506,50 @@ __device__ __forceinline__ void sparse_body_g(const AttnArgs& a, int seg, int bh
   const uint16_t* kv = a.K.values + (int64_t)bh * a.K.val_stride;
   const uint16_t* vv = a.V.values + (int64_t)bh * a.V.val_stride;
 
+  // q tables [head group][t][slot][GW heads]: slots 0 and 33 and channels 31
+  // and 63 hold zeros (the walks add channels 31 and 63 from their ranks).
+  // Every load is issued before the first store (a zero slot loads channel 0
+  // and discards it), and the first block's metadata loads go out with them,
+  // so that the tables, this tile's q at channels 31 and 63 and the metadata
+  // cost one memory round trip.
+  constexpr int kQn = G * T * kSlots, kQr = (kQn + kWave - 1) / kWave;
   int nb = min(NB, j1 - j0);
-  TileMeta cur = load_meta<T>(a, kt0, vt0, j0, nb, lane);
+  TileMeta cur;
+  float q31[G], q63[G];
+  {
+    const uint16_t* qrow = a.q + (int64_t)bh * G * d + kTile * t;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      q31[g] = half_bits_to_float(qrow[(int64_t)g * d + 31]);
+      q63[g] = half_bits_to_float(qrow[(int64_t)g * d + 63]);
+    }
+  }
+  {
+    const uint16_t* qsrc = a.q + (int64_t)bh * G * d;
+    uint16_t qv[kQr];
+#pragma unroll
+    for (int r = 0; r < kQr; ++r) {
+      const int i = (int)lane + r * kWave;
+      const int gi = i % G, rest = i / G;
+      const int slot = rest % kSlots, tt = rest / kSlots;
+      const int c = slot < 33 ? slot - 1 : slot - 2;
+      const bool zero = i >= kQn || slot == 0 || slot == 33 || c == 31 || c == 63;
+      qv[r] = qsrc[zero ? 0 : gi * d + kTile * tt + c];
+    }
+    cur = load_meta<T>(a, kt0, vt0, j0, nb, lane);
+#pragma unroll
+    for (int r = 0; r < kQr; ++r) {
+      const int i = (int)lane + r * kWave;
+      const int gi = i % G, rest = i / G;
+      const int slot = rest % kSlots, tt = rest / kSlots;
+      const int c = slot < 33 ? slot - 1 : slot - 2;
+      const bool zero = slot == 0 || slot == 33 || c == 31 || c == 63;
+      uint16_t* qt = reinterpret_cast<uint16_t*>(smem + L.qtab + (gi / GW) * QGS + tt * QTS + slot * QS);
+      if (i < kQn) qt[gi % GW] = zero ? (uint16_t)0 : qv[r];
+    }
+    if (lane == 0) lds_store<u32x4>(lds_addr(smem) + L.kst - 16u, (u32x4){0u, 0u, 0u, 0u});
+  }
+
   Runs rcur = runs_of<T>(cur, nb);
   u32x4 stg[STAGE];
   stage_issue<STAGE>(stg, kv, vv, rcur, lane);
@@ -516,15 +560,6 @@ __device__ __forceinline__ void sparse_body_g(const AttnArgs& a, int seg, int bh
 
   const uint32_t q_w0 = base + L.qtab + t * QTS + QS;   // slot 1: channel 0 of the tile
   const uint32_t q_w1 = q_w0 + 33u * QS;
-  float q31[G], q63[G];
-  {
-    const uint16_t* qrow = a.q + (int64_t)bh * G * d + kTile * t;
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      q31[g] = half_bits_to_float(qrow[(int64_t)g * d + 31]);
-      q63[g] = half_bits_to_float(qrow[(int64_t)g * d + 63]);
-    }
-  }
   constexpr uint32_t NBH = PU::NBH;
   constexpr uint32_t kRowB = kPvRow * 4u;
   const uint32_t d_w = base + L.dense + kRowB + (t * NBH + j % NBH) * 4u + (j / NBH) * 2u;

@@ -184,17 +184,22 @@ __device__ __forceinline__ void dense_body(const AttnArgs& a, int dseg, int bh, 
       if (t == 0) ps[j * G + g] = pj;
     }
     __syncthreads();
+#pragma unroll 8
     for (int jj = 0; jj < nb; ++jj) {
       float pv[G];
 #pragma unroll
       for (int g = 0; g < G; ++g) pv[g] = ps[jj * G + g];
       const uint16_t* vr = vd + (int64_t)(b0 + jj) * d;
       // Skipped ring slots have p = 0 and may hold non-finite bits: read as 0.
+      // Every slot is loaded (all lie inside the window buffer) and the skipped
+      // ones are dropped after the load, so the loads of successive tokens
+      // need not wait for each other.
       const int rj = b0 + jj - w_head;
       const bool live = !RING || (rj < 0 ? rj + a.n_dense : rj) < w_len;
 #pragma unroll
       for (int tt = 0; tt < T; ++tt) {
-        const float v = live ? half_bits_to_float(vr[lane + kTile * tt]) : 0.f;
+        const float vl = half_bits_to_float(vr[lane + kTile * tt]);
+        const float v = live ? vl : 0.f;
 #pragma unroll
         for (int g = 0; g < G; ++g) o[g][tt] = fmaf(pv[g], v, o[g][tt]);
       }
