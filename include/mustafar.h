@@ -269,7 +269,7 @@ enum mustafar_attn_kind {
  * passed n_splits <= 0, for B*Hkv streams of n_tokens tokens (the compressed
  * tokens for the sparse calls). It depends on the kernel that runs: with one
  * query head per kv-head, many segments down to one 64-token block; with 2 or
- * 4 query heads per kv-head (the same bit walks), about 2816 workgroups of at
+ * 4 query heads per kv-head (the same bit walks), about 4096 workgroups of at
  * least 192 tokens; with 8 (the matrix-core kernel), about 2048 of at least
  * 128; the dense kernel with grouped queries about 4096 of at least 128.
  * With a route other than the default (mustafar_attn_set_route), the split

@@ -29,7 +29,7 @@ constexpr int kMaxGrid = 65535;            // grid.y limit for the stream index
 // the grouped-query kernels want fewer, longer segments.
 constexpr int kWalkTargetGroups = 32768;
 constexpr int kWalkMinSegTokens = 64;
-constexpr int kWalkGroupedTargetGroups = 2816;  // the walks with 2 or 4 query heads per kv-head,
+constexpr int kWalkGroupedTargetGroups = 4096;  // the walks with 2 or 4 query heads per kv-head,
 constexpr int kWalkGroupedMinSegTokens = 192;   // segments of at least 192 tokens
 constexpr int kMfmaMinGroup = 8;                // the matrix-core kernel from 8 on (attn_common.h)
 constexpr int kMfmaTargetGroups = 2048;

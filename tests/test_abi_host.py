@@ -213,9 +213,9 @@ def test_default_splits_follow_the_kernel(lib):
     assert ds(1, 32, 32, 4096, S) == 64
     assert ds(1, 8, 8, 1024, S) == 16
     assert ds(1, 8, 8, 1024, D) == 16
-    # 2 or 4 query heads per kv-head (the walks): ~2816 workgroups of at least 192 tokens;
+    # 2 or 4 query heads per kv-head (the walks): ~4096 workgroups of at least 192 tokens;
     # 8 (the matrix-core kernel): ~2048 of at least 128; dense with grouped queries: ~4096
-    assert ds(1, 32, 8, 131072, S) == 352
+    assert ds(1, 32, 8, 131072, S) == 512
     assert ds(1, 32, 8, 131072, D) == 512
     assert ds(4, 32, 8, 16384, S) == 86    # 16384 / 192, rounded up
     assert ds(4, 16, 8, 16384, S) == 86
@@ -497,7 +497,7 @@ def test_attn_route_setting(lib):
         cores_g2 = lib.mustafar_attn_default_splits(1, 16, 8, 131072, 0)
     finally:
         assert lib.mustafar_attn_set_route(mf.ROUTE_DEFAULT) == 0
-    assert (walks, cores) == (352, 256)   # 2816 and 2048 workgroups over 8 streams
+    assert (walks, cores) == (512, 256)   # 4096 and 2048 workgroups over 8 streams
     assert lib.mustafar_attn_default_splits(1, 64, 8, 131072, 0) == cores   # default: cores at G = 8
     assert lib.mustafar_attn_default_splits(1, 16, 8, 131072, 0) == walks   # default: walks at G = 2
     assert cores_g2 == cores
