@@ -752,29 +752,18 @@ __global__ __launch_bounds__(64) void k_dense_attn(AttnArgs a) {
   write_partial<T, G>(a, seg, bh, m_run, l_run, o);
 }
 
-// grid (BHq, parts), 4 waves: log-sum-exp merge of segments [part * per,
-// part * per + per) of one query head. The 256 threads first reduce the
-// segments' maxima and weighted sums; then wave w accumulates the weighted
-// partial outputs of segments w, w+4, ... (lane = channel, four segments'
-// loads in flight) and LDS adds the waves. With FINAL the result is divided
-// by the sum and written as fp16 (RNE); otherwise (max, sum, unnormalised
-// output) is written as one segment of a second, shorter merge -- used when
-// there are many segments and few query heads, so that the merge runs on many
-// workgroups instead of one per head.
-constexpr int kMergeWaves = 4;
+// grid (BHq, parts), 8 waves: log-sum-exp merge of segments [part * per,
+// part * per + per) of one query head. Wave w takes segments w, w + 8, ...,
+// kMergeChunk at a time with every load of a chunk issued before the first is
+// used (lane = channel), and keeps a running (max, sum, weighted output) over
+// them; LDS then combines the eight waves' states. With FINAL the result is
+// divided by the sum and written as fp16 (RNE); otherwise (max, sum,
+// unnormalised output) is written as one segment of a second, shorter merge --
+// used when there are many segments and few query heads, so that the merge runs
+// on many workgroups instead of one per head.
+constexpr int kMergeWaves = 8;
+constexpr int kMergeChunk = 16;
 constexpr int kMergeSegsPerPart = 32;
-
-__device__ __forceinline__ float block_reduce(float v, bool is_max, float* red) {
-  v = is_max ? wave_max_u(v) : wave_sum_u(v);
-  const int wave = threadIdx.x / kWave;
-  if (lane_id() == 0) red[wave] = v;
-  __syncthreads();
-  float r = red[0];
-#pragma unroll
-  for (int w = 1; w < kMergeWaves; ++w) r = is_max ? fmaxf(r, red[w]) : r + red[w];
-  __syncthreads();
-  return r;
-}
 
 template <int T, bool FINAL>
 __global__ __launch_bounds__(kMergeWaves * kWave) void k_merge(const float2* __restrict__ ws_ml,
@@ -785,46 +774,73 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void k_merge(const float2* __r
                                                               float* __restrict__ part_o,
                                                               float* __restrict__ lse2) {
   constexpr int d = kTile * T;
-  __shared__ float red[kMergeWaves];
+  __shared__ float wm[kMergeWaves], wl[kMergeWaves];
   __shared__ float part[kMergeWaves][d];
   const int r = blockIdx.x;
   const int s0 = blockIdx.y * per, s1 = min(n_seg, s0 + per);
-  const int tid = threadIdx.x, wave = tid / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
   const uint32_t lane = lane_id();
-  float M = -INFINITY;
-  for (int s = s0 + tid; s < s1; s += kMergeWaves * kWave) M = fmaxf(M, ws_ml[(int64_t)s * BHq + r].x);
-  M = block_reduce(M, true, red);
-  float L = 0.f;
-  for (int s = s0 + tid; s < s1; s += kMergeWaves * kWave) {
-    const float2 ml = ws_ml[(int64_t)s * BHq + r];
-    L = fmaf(ml.y, ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - M), L);
-  }
-  L = block_reduce(L, false, red);
-
-  float acc[T];
+  float m = -INFINITY, l = 0.f, acc[T];
 #pragma unroll
   for (int tt = 0; tt < T; ++tt) acc[tt] = 0.f;
-#pragma unroll 4
-  for (int s = s0 + wave; s < s1; s += kMergeWaves) {
-    const float2 ml = ws_ml[(int64_t)s * BHq + r];
-    const float w = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml.x - M);
-    const float* o = ws_o + ((int64_t)s * BHq + r) * d + lane;
+  for (int c0 = s0 + wave; c0 < s1; c0 += kMergeChunk * kMergeWaves) {
+    // Lane k < kMergeChunk loads (max, sum) of the chunk's segment k; every lane
+    // loads its channel of each segment's output. Segments past the range load
+    // the first one again and weigh 0.
+    const int sk = c0 + (int)(lane % kMergeChunk) * kMergeWaves;
+    const bool lv = lane < (uint32_t)kMergeChunk && sk < s1;
+    const float2 mlv = ws_ml[(int64_t)(lv ? sk : s0) * BHq + r];
+    float ov[kMergeChunk][T];
 #pragma unroll
-    for (int tt = 0; tt < T; ++tt) acc[tt] = fmaf(o[kTile * tt], w, acc[tt]);
+    for (int k = 0; k < kMergeChunk; ++k) {
+      const int s = c0 + k * kMergeWaves < s1 ? c0 + k * kMergeWaves : s0;
+      const float* o = ws_o + ((int64_t)s * BHq + r) * d + lane;
+#pragma unroll
+      for (int tt = 0; tt < T; ++tt) ov[k][tt] = o[kTile * tt];
+    }
+    const float xv = lv ? mlv.x : -INFINITY;
+    const float cm = fmaxf(m, wave_max_u(xv));
+    // Rescale the running state to the new maximum (m = -inf gives 0; with no
+    // segment seen yet the state is empty and stays so).
+    const float sr = cm == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m - cm);
+    const float wv = xv == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(xv - cm);
+    l = fmaf(l, sr, wave_sum_u(wv * mlv.y));
+#pragma unroll
+    for (int tt = 0; tt < T; ++tt) acc[tt] *= sr;
+#pragma unroll
+    for (int k = 0; k < kMergeChunk; ++k) {
+      const float w = readlane_f(wv, k);
+#pragma unroll
+      for (int tt = 0; tt < T; ++tt) acc[tt] = fmaf(ov[k][tt], w, acc[tt]);
+    }
+    m = cm;
+  }
+  if (lane == 0) {
+    wm[wave] = m;
+    wl[wave] = l;
   }
 #pragma unroll
   for (int tt = 0; tt < T; ++tt) part[wave][lane + kTile * tt] = acc[tt];
   __syncthreads();
   if (wave == 0) {
+    float M = wm[0];
+#pragma unroll
+    for (int w = 1; w < kMergeWaves; ++w) M = fmaxf(M, wm[w]);
+    float sw[kMergeWaves], L = 0.f;
+#pragma unroll
+    for (int w = 0; w < kMergeWaves; ++w) {
+      sw[w] = wm[w] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(wm[w] - M);
+      L = fmaf(wl[w], sw[w], L);
+    }
     const float inv = L > 0.f ? 1.f / L : 0.f;  // no token at all (every stream skipped): 0
     const int64_t prow = (int64_t)blockIdx.y * BHq + r;
     if (!FINAL && lane == 0) part_ml[prow] = make_float2(M, L);
     if (FINAL && lse2 != nullptr && lane == 0) lse2[r] = M + __builtin_log2f(L);
 #pragma unroll
     for (int tt = 0; tt < T; ++tt) {
-      float v = part[0][lane + kTile * tt];
+      float v = 0.f;
 #pragma unroll
-      for (int w = 1; w < kMergeWaves; ++w) v += part[w][lane + kTile * tt];
+      for (int w = 0; w < kMergeWaves; ++w) v = fmaf(part[w][lane + kTile * tt], sw[w], v);
       if constexpr (FINAL)
         out[(int64_t)r * d + lane + kTile * tt] = __builtin_bit_cast(uint16_t, (_Float16)(v * inv));
       else
