@@ -172,6 +172,17 @@ def test_attention_other_head_dims(d, G):
     _attn_case(B=2, Hkv=2, G=G, Ns=333, Nd=32, d=d, sK=0.5, sV=0.5, splits=0, seed=d + G)
 
 
+# k compressed segments of 64 tokens plus the window segment. The merge runs
+# eight waves that take 16 segments at a time: counts around one wave's share
+# (8), a full round (128) and several rounds, in one level (256 query heads, or
+# at most 128 segments) and in two levels (more segments, fewer heads).
+@pytest.mark.parametrize("B,Hkv,G,d,k", [(1, 4, 1, 128, 6), (1, 4, 1, 128, 7), (1, 4, 4, 128, 126),
+                                         (1, 4, 1, 128, 127), (1, 2, 2, 128, 128), (1, 2, 1, 128, 300),
+                                         (2, 64, 2, 64, 127), (2, 64, 2, 64, 140)])
+def test_attention_merge_segment_counts(B, Hkv, G, d, k):
+    _attn_case(B=B, Hkv=Hkv, G=G, Ns=64 * k, Nd=32, d=d, sK=0.7, sV=0.7, splits=k, seed=k + G)
+
+
 @pytest.mark.parametrize("sK,sV", [(0.0, 0.0), (0.9, 0.9), (1.0, 0.5), (0.5, 1.0), (1.0, 1.0)])
 def test_attention_extreme_sparsities(sK, sV):
     _attn_case(B=1, Hkv=2, G=2, Ns=200, Nd=5, d=128, sK=sK, sV=sV, splits=3, seed=31)
