@@ -1,10 +1,16 @@
 // Streaming ceilings the kernels are compared with.
 //
-// Read: every lane reads 16-byte words grid-stride with
-// non-temporal loads (eight in flight) and XORs them; one checksum per
-// workgroup keeps the loads alive. The rate of this kernel over a buffer much
-// larger than the caches is the HBM read rate the decode kernels are compared
-// with (16384 workgroups and non-temporal loads measured fastest on gfx950).
+// Read: each lane reads one 16-byte word per grid-stride step with a
+// non-temporal load and XORs it; one checksum per workgroup keeps the loads
+// alive. The rate of this kernel over a buffer much larger than the caches is
+// the HBM read rate the decode kernels are compared with. A large grid with one
+// word per lane and step, so that the words in flight at any moment form one
+// compact front through the buffer, measured fastest on gfx950 (sweeps over
+// 4096 to 2097152 workgroups of 256, one to 32 words per lane and step,
+// temporal and non-temporal accesses, 8 GiB): reads 6.8-7.25 TB/s against
+// 6.6-7.0 with 16384 workgroups and eight words in flight per lane one grid
+// apart; a read that also writes 9/16 of its bytes 5.9-6.1 TB/s against
+// 5.0-5.2.
 #include "mustafar.h"
 #include "mf_device.h"
 
@@ -12,32 +18,27 @@ namespace mf {
 
 typedef uint32_t u32x4m __attribute__((ext_vector_type(4)));
 
-constexpr int kReadBlocks = 16384;
-constexpr int kReadUnroll = 8;
+constexpr int kReadBlocks = 524288;
 constexpr int kReadThreads = 256;
 
-__global__ __launch_bounds__(kReadThreads) void k_stream_read(const u32x4m* __restrict__ src,
-                                                              int64_t n16, uint32_t* __restrict__ sink) {
-  uint32_t acc = 0;
-  const int64_t g = (int64_t)gridDim.x * kReadThreads;
-  int64_t i = (int64_t)blockIdx.x * kReadThreads + threadIdx.x;
-  for (; i + (kReadUnroll - 1) * g < n16; i += kReadUnroll * g) {
-    u32x4m v[kReadUnroll];
-#pragma unroll
-    for (int u = 0; u < kReadUnroll; ++u) v[u] = __builtin_nontemporal_load(&src[i + u * g]);
-#pragma unroll
-    for (int u = 0; u < kReadUnroll; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
-  }
-  for (; i < n16; i += g) {
-    const u32x4m a = __builtin_nontemporal_load(&src[i]);
-    acc ^= a.x ^ a.y ^ a.z ^ a.w;
-  }
+__device__ __forceinline__ void block_checksum(uint32_t acc, uint32_t* __restrict__ sink) {
   __shared__ uint32_t red[kReadThreads / kWave];
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) acc ^= (uint32_t)__shfl_xor((int)acc, o, kWave);
   if (lane_id() == 0) red[threadIdx.x / kWave] = acc;
   __syncthreads();
   if (threadIdx.x == 0) sink[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
+}
+
+__global__ __launch_bounds__(kReadThreads) void k_stream_read(const u32x4m* __restrict__ src,
+                                                              int64_t n16, uint32_t* __restrict__ sink) {
+  uint32_t acc = 0;
+  const int64_t g = (int64_t)gridDim.x * kReadThreads;
+  for (int64_t i = (int64_t)blockIdx.x * kReadThreads + threadIdx.x; i < n16; i += g) {
+    const u32x4m a = __builtin_nontemporal_load(&src[i]);
+    acc ^= a.x ^ a.y ^ a.z ^ a.w;
+  }
+  block_checksum(acc, sink);
 }
 
 // Streaming read + write: every word is read (and XORed into the workgroup's
@@ -50,29 +51,12 @@ __global__ __launch_bounds__(kReadThreads) void k_stream_mix(const u32x4m* __res
                                                              uint32_t* __restrict__ sink) {
   uint32_t acc = 0;
   const int64_t g = (int64_t)gridDim.x * kReadThreads;
-  int64_t i = (int64_t)blockIdx.x * kReadThreads + threadIdx.x;
-  for (; i + (kReadUnroll - 1) * g < n16; i += kReadUnroll * g) {
-    u32x4m v[kReadUnroll];
-#pragma unroll
-    for (int u = 0; u < kReadUnroll; ++u) v[u] = __builtin_nontemporal_load(&src[i + u * g]);
-#pragma unroll
-    for (int u = 0; u < kReadUnroll; ++u) {
-      const int64_t j = i + u * g;
-      acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
-      if ((int)(j & 15) < w16) __builtin_nontemporal_store(v[u], &dst[(j >> 4) * w16 + (j & 15)]);
-    }
-  }
-  for (; i < n16; i += g) {
+  for (int64_t i = (int64_t)blockIdx.x * kReadThreads + threadIdx.x; i < n16; i += g) {
     const u32x4m a = __builtin_nontemporal_load(&src[i]);
     acc ^= a.x ^ a.y ^ a.z ^ a.w;
     if ((int)(i & 15) < w16) __builtin_nontemporal_store(a, &dst[(i >> 4) * w16 + (i & 15)]);
   }
-  __shared__ uint32_t red[kReadThreads / kWave];
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) acc ^= (uint32_t)__shfl_xor((int)acc, o, kWave);
-  if (lane_id() == 0) red[threadIdx.x / kWave] = acc;
-  __syncthreads();
-  if (threadIdx.x == 0) sink[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
+  block_checksum(acc, sink);
 }
 
 }  // namespace mf
