@@ -113,6 +113,12 @@ def attn_alg_bytes(w, k_len_total: int, v_len_total: int, n_s: int) -> int:
     return meta + vals + window + qo
 
 
+def attn_offset_bytes(w, n_s: int) -> int:
+    """The per-tile offsets inside attn_alg_bytes: the kernels read only the first
+    tile's offset of each segment and derive the others from the bitmaps."""
+    return 4 * w.B * w.Hkv * n_s * (w.d // 64) * 2
+
+
 def dense_alg_bytes(w, n_tokens: int) -> int:
     return 2 * 2 * w.B * w.Hkv * n_tokens * w.d + 4 * w.B * w.Hq * w.d
 
@@ -678,6 +684,8 @@ def main():
            for n_s in range(n_s_start + 1, n_s_end + 1)]
     alg_bytes = float(np.mean(alg))
     attn_gbs = alg_bytes / attn_s / 1e9
+    read_bytes = alg_bytes - float(np.mean([attn_offset_bytes(w, n_s)
+                                            for n_s in range(n_s_start + 1, n_s_end + 1)]))
     del Kc, Vc, win
     torch.cuda.empty_cache()
 
@@ -813,7 +821,11 @@ def main():
                      "kernel": "k_sparse_attn",
                      "how": "algorithmic bytes of one launch / mean time of the timed attention "
                             "calls (k_sparse_attn and its split-K merge, about 0.6% of it)",
-                     "traffic": measured_traffic("k_sparse_attn", w.name)},
+                     "traffic": measured_traffic("k_sparse_attn", w.name),
+                     "needed_bytes": read_bytes,
+                     "frac_of_needed_bytes": read_bytes / attn_s / 1e9 / HBM_PEAK_GBS,
+                     "needed_how": "algorithmic bytes less the per-tile offsets, which the "
+                                   "kernel derives from the bitmaps (one offset per segment)"},
         "read_ceiling": {"gb_s": ceiling, "attn_frac": attn_gbs / ceiling,
                          "how": "mustafar_stream_read (16-byte loads) over an 8 GiB buffer"},
         "dense_baseline": {"us": dense_st["mean"], "us_median": dense_st["median"],

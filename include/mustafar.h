@@ -32,7 +32,12 @@
  *     bitmaps[tile]  u64  bit i set  <=> channel 64t+i of the token is kept
  *     offsets[tile]  u32  index (fp16 elements, relative to the stream's first
  *                         value) of the tile's first packed non-zero; always a
- *                         multiple of 8
+ *                         multiple of 8. A stream's tiles are packed back to
+ *                         back in token (then tile) order: each offset is the
+ *                         previous tile's plus its count padded to 8. The
+ *                         decode calls rely on this: they read the offset of
+ *                         the first tile of each token range they take and
+ *                         derive the others from the bitmaps.
  *     values[s*val_stride + offsets[tile] + r]  r < popcount(bitmap): the
  *                         kept fp16 values of the tile in channel order;
  *                         then zero (+0.0) fill up to the next multiple of 8

@@ -197,6 +197,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   const _Float16 q63 = __builtin_bit_cast(_Float16, qrow[63]);
   int nb = min(NB, j1 - j0);
   TileMeta cur;
+  RunPos pos;
   {
     const uint16_t* qsrc = a.q + (int64_t)bh * d;
     uint16_t qv[kQr];
@@ -209,6 +210,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
       qv[r] = qsrc[zero ? 0 : kTile * tt + c];
     }
     cur = load_meta<T>(a, kt0, vt0, j0, nb, lane);
+    pos = segment_start<T>(a, kt0, vt0, j0);
 #pragma unroll
     for (int r = 0; r < kQr; ++r) {
       const int i = (int)lane + r * kWave;
@@ -226,7 +228,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
   }
 
   // Prologue: block 0 staged in LDS, metadata of block 1 in flight.
-  Runs rcur = runs_of<T>(cur, nb);
+  Runs rcur = runs_of(cur, pos);
   u32x4 stg[STAGE];
   stage_issue<STAGE>(stg, kv, vv, rcur, lane);
   int nb_next = min(NB, j1 - (j0 + NB));
@@ -264,7 +266,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
     Runs rnext = {0u, 0u, 0u, 0u};
     TileMeta nxt2 = {0ull, 0ull, 0u, 0u};
     const int nb_next2 = min(NB, j1 - (b0 + 2 * NB));
-    if (has_next) rnext = runs_of<T>(nxt, nb_next);
+    if (has_next) rnext = runs_of(nxt, pos);
     stage_issue<STAGE>(stg, kv, vv, rnext, lane);
     if (nb_next2 > 0) nxt2 = load_meta<T>(a, kt0, vt0, b0 + 2 * NB, nb_next2, lane);
 
@@ -272,7 +274,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
     const WalkCounts wc = walk_counts(cur.kb, cur.vb);
     float acc = 0.f;
     {
-      const uint32_t va = base + L.kst + ((int)j < nb ? 2u * (cur.ko - rcur.kstart) : 0u);
+      const uint32_t va = base + L.kst + ((int)j < nb ? 2u * cur.ko : 0u);
       key_walk(wc.klo, wc.khi, cur.kb, va, q_w0, q_w1, q31, q63, acc);
     }
     {
@@ -299,7 +301,7 @@ __device__ __forceinline__ void sparse_body(const AttnArgs& a, int seg, int bh, 
 
     // Values, one half of every tile at a time: clear the half tile (it
     // overwrites the staged keys, read above), expand, p.V.
-    const uint32_t va = base + L.vst + ((int)j < nb ? 2u * (cur.vo - rcur.vstart) : 0u);
+    const uint32_t va = base + L.vst + ((int)j < nb ? 2u * cur.vo : 0u);
     const uint32_t vlo = (uint32_t)cur.vb, vhi = (uint32_t)(cur.vb >> 32);
     const uint32_t vs = (uint32_t)__popc(vlo), vm = vs & 3u;
     const _Float16 v31 = lds_load<_Float16>(va + 2u * vs - 2u);
@@ -515,6 +517,7 @@ __device__ __forceinline__ void sparse_body_g(const AttnArgs& a, int seg, int bh
   constexpr int kQn = G * T * kSlots, kQr = (kQn + kWave - 1) / kWave;
   int nb = min(NB, j1 - j0);
   TileMeta cur;
+  RunPos pos;
   float q31[G], q63[G];
   {
     const uint16_t* qrow = a.q + (int64_t)bh * G * d + kTile * t;
@@ -537,6 +540,7 @@ __device__ __forceinline__ void sparse_body_g(const AttnArgs& a, int seg, int bh
       qv[r] = qsrc[zero ? 0 : gi * d + kTile * tt + c];
     }
     cur = load_meta<T>(a, kt0, vt0, j0, nb, lane);
+    pos = segment_start<T>(a, kt0, vt0, j0);
 #pragma unroll
     for (int r = 0; r < kQr; ++r) {
       const int i = (int)lane + r * kWave;
@@ -550,7 +554,7 @@ __device__ __forceinline__ void sparse_body_g(const AttnArgs& a, int seg, int bh
     if (lane == 0) lds_store<u32x4>(lds_addr(smem) + L.kst - 16u, (u32x4){0u, 0u, 0u, 0u});
   }
 
-  Runs rcur = runs_of<T>(cur, nb);
+  Runs rcur = runs_of(cur, pos);
   u32x4 stg[STAGE];
   stage_issue<STAGE>(stg, kv, vv, rcur, lane);
   int nb_next = min(NB, j1 - (j0 + NB));
@@ -589,7 +593,7 @@ __device__ __forceinline__ void sparse_body_g(const AttnArgs& a, int seg, int bh
     Runs rnext = {0u, 0u, 0u, 0u};
     TileMeta nxt2 = {0ull, 0ull, 0u, 0u};
     const int nb_next2 = min(NB, j1 - (b0 + 2 * NB));
-    if (has_next) rnext = runs_of<T>(nxt, nb_next);
+    if (has_next) rnext = runs_of(nxt, pos);
     stage_issue<STAGE>(stg, kv, vv, rnext, lane);
     if (nb_next2 > 0) nxt2 = load_meta<T>(a, kt0, vt0, b0 + 2 * NB, nb_next2, lane);
 
@@ -597,7 +601,7 @@ __device__ __forceinline__ void sparse_body_g(const AttnArgs& a, int seg, int bh
     const WalkCounts wc = walk_counts(cur.kb, cur.vb);
     float acc[G];
     {
-      const uint32_t va = base + L.kst + ((int)j < nb ? 2u * (cur.ko - rcur.kstart) : 0u);
+      const uint32_t va = base + L.kst + ((int)j < nb ? 2u * cur.ko : 0u);
 #pragma unroll
       for (int g0 = 0; g0 < G; g0 += GW) {
         float ag[GW], a31[GW], a63[GW];
@@ -637,7 +641,7 @@ __device__ __forceinline__ void sparse_body_g(const AttnArgs& a, int seg, int bh
     }
 
     // Values, one half of every tile at a time, as in the one-head body.
-    const uint32_t va = base + L.vst + ((int)j < nb ? 2u * (cur.vo - rcur.vstart) : 0u);
+    const uint32_t va = base + L.vst + ((int)j < nb ? 2u * cur.vo : 0u);
     const uint32_t vlo = (uint32_t)cur.vb, vhi = (uint32_t)(cur.vb >> 32);
     const uint32_t vs = (uint32_t)__popc(vlo), vm = vs & 3u;
     const _Float16 v31 = lds_load<_Float16>(va + 2u * vs - 2u);

@@ -119,7 +119,8 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
 
   int nb = min(NB, j1 - j0);
   TileMeta cur = load_meta<T>(a, kt0, vt0, j0, nb, lane);
-  Runs rcur = runs_of<T>(cur, nb);
+  RunPos pos = segment_start<T>(a, kt0, vt0, j0);
+  Runs rcur = runs_of(cur, pos);
   u32x4 stg[STAGE];
   stage_issue<STAGE>(stg, kv, vv, rcur, lane);
   int nb_next = min(NB, j1 - (j0 + NB));
@@ -138,7 +139,7 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
     Runs rnext = {0u, 0u, 0u, 0u};
     TileMeta nxt2 = {0ull, 0ull, 0u, 0u};
     const int nb_next2 = min(NB, j1 - (b0 + 2 * NB));
-    if (has_next) rnext = runs_of<T>(nxt, nb_next);
+    if (has_next) rnext = runs_of(nxt, pos);
     stage_issue<STAGE>(stg, kv, vv, rnext, lane);
     if (nb_next2 > 0) nxt2 = load_meta<T>(a, kt0, vt0, b0 + 2 * NB, nb_next2, lane);
 
@@ -146,7 +147,7 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
     const WalkCounts wc = walk_counts(cur.kb, cur.vb);
     lds_zero(base + L.kd, NB * Geo::KD_ROW, lane);
     {
-      const uint32_t va = base + L.kst + ((int)j < nb ? 2u * (cur.ko - rcur.kstart) : 0u);
+      const uint32_t va = base + L.kst + ((int)j < nb ? 2u * cur.ko : 0u);
       expand_tile<2u>(wc.klo, wc.khi, cur.kb, va, kd_w0, kd_w1);
     }
 
@@ -204,7 +205,7 @@ __device__ __forceinline__ void sparse_body_mfma(const AttnArgs& a, int seg, int
     // Expand the values (VdT overlays the consumed keys).
     lds_zero(base + L.vdt, T * kMSlots * Geo::VD_ROW, lane);
     {
-      const uint32_t va = base + L.vst + ((int)j < nb ? 2u * (cur.vo - rcur.vstart) : 0u);
+      const uint32_t va = base + L.vst + ((int)j < nb ? 2u * cur.vo : 0u);
       expand_tile<Geo::VD_ROW>(wc.vlo, wc.vhi, cur.vb, va, vd_w0, vd_w1);
     }
 

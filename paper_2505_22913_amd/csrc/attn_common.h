@@ -213,9 +213,12 @@ __device__ __forceinline__ void dense_body(const AttnArgs& a, int dseg, int bh, 
 // ------------------------------------------------------------------------------------------
 struct TileMeta {
   uint64_t kb, vb;  // this lane's key / value tile bitmaps (0 past the block end)
-  uint32_t ko, vo;  // their offsets
+  uint32_t ko, vo;  // their offsets from the block's first tile (set by runs_of)
 };
 
+// Bitmaps of the block of nb tokens from token b0. The tile offsets are not
+// read: a stream's tiles are packed back to back in token order, each taking
+// its count padded to 8, so runs_of derives them from the bitmaps.
 template <int T>
 __device__ __forceinline__ TileMeta load_meta(const AttnArgs& a, int64_t kt0, int64_t vt0, int b0,
                                               int nb, uint32_t lane) {
@@ -223,11 +226,23 @@ __device__ __forceinline__ TileMeta load_meta(const AttnArgs& a, int64_t kt0, in
   if ((int)(lane / T) < nb) {
     const int64_t ti = (int64_t)b0 * T + lane;
     m.kb = __builtin_nontemporal_load(&a.K.bitmaps[kt0 + ti]);
-    m.ko = __builtin_nontemporal_load(&a.K.offsets[kt0 + ti]);
     m.vb = __builtin_nontemporal_load(&a.V.bitmaps[vt0 + ti]);
-    m.vo = __builtin_nontemporal_load(&a.V.offsets[vt0 + ti]);
   }
   return m;
+}
+
+// Stream positions (fp16 elements) where the next block's key and value runs
+// start: the offsets of the segment's first tiles, then advanced by runs_of.
+struct RunPos {
+  uint32_t k, v;
+};
+
+template <int T>
+__device__ __forceinline__ RunPos segment_start(const AttnArgs& a, int64_t kt0, int64_t vt0, int j0) {
+  RunPos p;
+  p.k = (uint32_t)__builtin_amdgcn_readfirstlane((int)a.K.offsets[kt0 + (int64_t)j0 * T]);
+  p.v = (uint32_t)__builtin_amdgcn_readfirstlane((int)a.V.offsets[vt0 + (int64_t)j0 * T]);
+  return p;
 }
 
 // Packed-value runs of one block: [kstart, kstart + kn) and [vstart, vstart + vn).
@@ -235,14 +250,21 @@ struct Runs {
   uint32_t kstart, kn, vstart, vn;
 };
 
-template <int T>
-__device__ __forceinline__ Runs runs_of(const TileMeta& m, int nb) {
+// The block's runs and its tiles' offsets: an exclusive wave scan of the
+// padded tile counts (tiles past the block end count 0); the run starts at pos,
+// which then moves to the next block's run.
+__device__ __forceinline__ Runs runs_of(TileMeta& m, RunPos& pos) {
+  const uint32_t ck = pad8((uint32_t)__popcll(m.kb)), cv = pad8((uint32_t)__popcll(m.vb));
+  const uint32_t ik = wave_incl_scan(ck), iv = wave_incl_scan(cv);
+  m.ko = ik - ck;
+  m.vo = iv - cv;
   Runs r;
-  r.kstart = __builtin_amdgcn_readfirstlane(m.ko);
-  r.vstart = __builtin_amdgcn_readfirstlane(m.vo);
-  const int last = nb * T - 1;
-  r.kn = __builtin_amdgcn_readlane(m.ko + pad8((uint32_t)__popcll(m.kb)), last) - r.kstart;
-  r.vn = __builtin_amdgcn_readlane(m.vo + pad8((uint32_t)__popcll(m.vb)), last) - r.vstart;
+  r.kstart = pos.k;
+  r.vstart = pos.v;
+  r.kn = (uint32_t)__builtin_amdgcn_readlane((int)ik, kWave - 1);
+  r.vn = (uint32_t)__builtin_amdgcn_readlane((int)iv, kWave - 1);
+  pos.k += r.kn;
+  pos.v += r.vn;
   return r;
 }
 

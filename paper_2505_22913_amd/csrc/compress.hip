@@ -277,18 +277,6 @@ __device__ __forceinline__ uint32_t interleave_halves(uint32_t x) {
   return x;
 }
 
-// Inclusive prefix sum over the 64 lanes: shifts within rows of 16 lanes,
-// then the last lane of row 0 (of rows 0-1) is added to row 1 and 3 (2-3).
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);  // row_shr:1
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);  // row_shr:2
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);  // row_shr:4
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);  // row_shr:8
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false); // row_bcast:15
-  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false); // row_bcast:31
-  return x;
-}
-
 // The lowest n set bits of w (n >= 0).
 __device__ __forceinline__ uint32_t lowest_bits(uint32_t w, int n) {
   if (n >= (int)__popc(w)) return w;
