@@ -9,14 +9,15 @@ caches and the window (mustafar_window_decode_attn). value = batch * steps /
 time: decode tokens per second of the whole job.
 
 Also measured (reported in the same JSON line):
-  * a clock-settle phase before the timed steps: attention calls alone for a
-    fixed wall time, reported (calls and seconds) -- the GPU's clocks take a
-    few dozen calls to settle under this load, so the result must not depend
-    on --warmup;
+  * a clock-settle phase right before the timed steps: attention calls alone
+    for a fixed wall time, reported (calls and seconds) -- the GPU's clocks
+    take a few dozen calls to settle under this load, so the result must not
+    depend on --warmup;
   * per attention call: mean, median, min and max of the HIP-event times over
-    the timed steps, their algorithmic HBM GB/s and roofline fraction (bytes
-    the format makes the kernel read: 12 B of bitmap + offset per tile, the
-    packed values with padding, the window, q and the output, over the mean);
+    the timed steps, their algorithmic HBM GB/s and roofline fraction (the
+    format's bytes: 12 B of bitmap + offset per tile, the packed values with
+    padding, the window, q and the output, over the mean), and the same over
+    the bytes the kernel needs (it derives the tile offsets from the bitmaps);
   * the HBM read ceiling and, for the compression, the read + write ceiling
     at its write share (the library's streaming helpers);
   * the in-house dense fp16 decode-attention kernel on the same tokens;
@@ -623,26 +624,6 @@ def main():
     attend = lambda: mf.mustafar_window_decode_attn(q, Kc, Vc, win, out=out,  # noqa: E731
                                                     n_splits=args.splits, ws=ws_a)
 
-    # ---- clock settle: attention calls alone for a fixed wall time (reported) ----
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    settle_calls = 0
-    while time.perf_counter() - t0 < args.settle_s:
-        for _ in range(10):
-            attend()
-        settle_calls += 10
-        torch.cuda.synchronize()
-    settle_s = time.perf_counter() - t0
-
-    # ---- dense baseline over the same tokens (compressed prefix + window) ----
-    ws_d = torch.empty(mf.mustafar_attn_workspace_bytes(w.B, w.Hq, w.Hkv, w.d, w.N + w.n_tail,
-                                                        args.splits), dtype=torch.uint8, device=dev)
-    dense_st = timed_calls(lambda: mf.mustafar_dense_decode_attn(q, K, V, out=out, n_splits=args.splits,
-                                                                 ws=ws_d), 20)
-    t_dense = dense_st["mean"] * 1e-6
-    dense_bytes = dense_alg_bytes(w, w.N + w.n_tail)
-    del ws_d
-
     # ---- decode steps: a new token into every window, the oldest one pruned,
     # compressed and appended (a1/a2/a7), then attention (a3-a6) ----
     def step(i, marks=None):
@@ -661,6 +642,18 @@ def main():
     n_s_start = Kc.n_tokens
     k_len_start = int(Kc.stream_len.to(torch.int64).sum().item())
     v_len_start = int(Vc.stream_len.to(torch.int64).sum().item())
+
+    # ---- clock settle, right before the timed steps: attention calls alone for
+    # a fixed wall time (reported; they change no cache) ----
+    t0 = time.perf_counter()
+    settle_calls = 0
+    while time.perf_counter() - t0 < args.settle_s:
+        for _ in range(10):
+            attend()
+        settle_calls += 10
+        torch.cuda.synchronize()
+    settle_s = time.perf_counter() - t0
+
     wall0 = time.perf_counter()
     t_start.record()
     for i in range(steps):
@@ -670,6 +663,16 @@ def main():
     wall = time.perf_counter() - wall0
     total_s = t_start.elapsed_time(t_end) / 1e3
     attn = call_stats(marks)
+
+    # ---- dense baseline over the same tokens (compressed prefix + window), right
+    # after the timed steps, at the same settled clocks ----
+    ws_d = torch.empty(mf.mustafar_attn_workspace_bytes(w.B, w.Hq, w.Hkv, w.d, w.N + w.n_tail,
+                                                        args.splits), dtype=torch.uint8, device=dev)
+    dense_st = timed_calls(lambda: mf.mustafar_dense_decode_attn(q, K, V, out=out, n_splits=args.splits,
+                                                                 ws=ws_d), 20)
+    t_dense = dense_st["mean"] * 1e-6
+    dense_bytes = dense_alg_bytes(w, w.N + w.n_tail)
+    del ws_d
     attn_s = attn["mean"] * 1e-6
     n_s_end = Kc.n_tokens
 
@@ -808,8 +811,9 @@ def main():
         "step": "mustafar_window_step (new token into each 32-token window; the oldest is pruned, "
                 "compressed and appended) + mustafar_window_decode_attn",
         "settle": {"calls": settle_calls, "s": settle_s,
-                   "how": "attention calls alone for a fixed wall time right before the dense "
-                          "baseline and the warmup steps (the GPU clocks settle under load)"},
+                   "how": "attention calls alone for a fixed wall time right before the timed "
+                          "steps, after the warmup steps (the GPU clocks settle under load; the "
+                          "dense baseline runs right after the timed steps)"},
         "attention": {"us": attn["mean"], "us_median": attn["median"], "us_min": attn["min"],
                       "us_max": attn["max"], "tokens_per_s": w.B / attn_s,
                       "kv_tokens_per_s": w.B * w.Hkv * (n_s_end + w.n_tail) / attn_s,
