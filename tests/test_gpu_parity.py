@@ -183,6 +183,37 @@ def test_attention_merge_segment_counts(B, Hkv, G, d, k):
     _attn_case(B=B, Hkv=Hkv, G=G, Ns=64 * k, Nd=32, d=d, sK=0.7, sV=0.7, splits=k, seed=k + G)
 
 
+# The decode kernels read one tile offset per segment and derive the others from
+# the bitmaps (a stream's tiles are packed back to back), so a cache assembled
+# from a bulk compression, a second one starting mid-block, single appends and a
+# third compression must attend exactly like the oracle's compress-all, with
+# segment starts falling in every part (split counts) and on every kernel body
+# (one head: walks; four: grouped walks; eight: matrix cores).
+@pytest.mark.parametrize("d,G", [(128, 1), (128, 4), (128, 8), (64, 1), (256, 4)])
+@pytest.mark.parametrize("splits", [0, 3, 11])
+def test_attention_over_caches_built_in_pieces(d, G, splits):
+    announce(f"attn pieces d={d} G={G} splits={splits}")
+    B, Hkv, Nd = 2, 3, 32
+    n0, n1, n2, n3 = 301, 133, 23, 170
+    N = n0 + n1 + n2 + n3
+    K, V = synth.make_kv(B, Hkv, N, d, seed=d + G)
+    KL, VL = synth.make_tail(B, Hkv, Nd, d, seed=d + G)
+    q = synth.make_q(B, Hkv * G, d, seed=d + G)
+    Kc = mf.CompressedCache(B, Hkv, d, 0.5, N)
+    Vc = mf.CompressedCache(B, Hkv, d, 0.7, N)
+    for c, x in ((Kc, K), (Vc, V)):
+        mf.mustafar_prune_compress(c, to_dev(np.ascontiguousarray(x[:, :, :n0])))
+        mf.mustafar_prune_compress(c, to_dev(np.ascontiguousarray(x[:, :, n0:n0 + n1])))
+        for j in range(n0 + n1, n0 + n1 + n2):
+            mf.mustafar_append(c, to_dev(np.ascontiguousarray(x[:, :, j])))
+        mf.mustafar_prune_compress(c, to_dev(np.ascontiguousarray(x[:, :, n0 + n1 + n2:])))
+        assert c.n_tokens == N
+    out = mf.mustafar_sparse_decode_attn(to_dev(q), Kc, Vc, to_dev(KL), to_dev(VL), n_splits=splits)
+    ref = oracle.sparse_decode_attention(q, oracle.compress(K, 0.5), oracle.compress(V, 0.7), KL, VL)
+    err = attn_error(out.cpu().numpy(), ref)
+    assert err <= ATTN_TOL, err
+
+
 @pytest.mark.parametrize("sK,sV", [(0.0, 0.0), (0.9, 0.9), (1.0, 0.5), (0.5, 1.0), (1.0, 1.0)])
 def test_attention_extreme_sparsities(sK, sV):
     _attn_case(B=1, Hkv=2, G=2, Ns=200, Nd=5, d=128, sK=sK, sV=sV, splits=3, seed=31)
