@@ -19,7 +19,9 @@ Also measured (reported in the same JSON line):
     padding, the window, q and the output, over the mean), and the same over
     the bytes the kernel needs (it derives the tile offsets from the bitmaps);
   * the HBM read ceiling and, for the compression, the read + write ceiling
-    at its write share (the library's streaming helpers);
+    at its write share and the ceiling of its own access order (the same bytes
+    in the same order without its arithmetic) -- the library's streaming
+    helpers;
   * the in-house dense fp16 decode-attention kernel on the same tokens;
   * the bulk prune+compress of the whole prefill cache (K and V): tokens/s =
     batch * context / time, and its algorithmic GB/s;
@@ -184,6 +186,31 @@ def rw_ceiling_gbs(write_16ths: int, n_bytes: int = 8 << 30) -> float:
     torch.cuda.synchronize()
     t = a.elapsed_time(b) / 1e3 / 5
     del x, y
+    torch.cuda.empty_cache()
+    return n_bytes * (1 + write_16ths / 16) / t / 1e9
+
+
+def chunk_order_ceiling_gbs(n_streams: int, n_bytes: int, write_16ths: int) -> float:
+    """HBM read + write rate of the bulk compression's access order: the library's
+    chunk-order helper over n_bytes in n_streams streams of 16 KiB chunks, the
+    streams taking turns chunk by chunk, writing write_16ths/16 of every chunk;
+    the rate counts both directions."""
+    import torch
+
+    import paper_2505_22913_amd as mf
+    x = torch.empty(n_bytes, dtype=torch.uint8, device="cuda")
+    x.fill_(1)
+    y = torch.empty(n_bytes * write_16ths // 16 + 16, dtype=torch.uint8, device="cuda")
+    sink = mf.mustafar_stream_chunks(x, n_streams, y, write_16ths)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(5):
+        mf.mustafar_stream_chunks(x, n_streams, y, write_16ths, sink)
+    b.record()
+    torch.cuda.synchronize()
+    t = a.elapsed_time(b) / 1e3 / 5
+    del x, y, sink
     torch.cuda.empty_cache()
     return n_bytes * (1 + write_16ths / 16) / t / 1e9
 
@@ -790,6 +817,9 @@ def main():
     ceiling = read_ceiling_gbs()
     pc_w16 = max(1, min(16, round(16 * comp_kv / dense_kv)))  # the compression's write share
     rw_ceiling = rw_ceiling_gbs(pc_w16)
+    cache_bytes = w.B * w.Hkv * w.N * w.d * 2
+    order_ceiling = (chunk_order_ceiling_gbs(w.B * w.Hkv, cache_bytes, pc_w16)
+                     if cache_bytes % (w.B * w.Hkv * mf.STREAM_CHUNK_BYTES) == 0 else None)
 
     result = {
         "metric": METRIC,
@@ -842,6 +872,13 @@ def main():
                            "gb_s": (dense_kv + comp_kv) / t_pc / 1e9,
                            "frac": (dense_kv + comp_kv) / t_pc / 1e9 / HBM_PEAK_GBS,
                            "traffic": pc_traffic,
+                           "order_ceiling": None if order_ceiling is None else {
+                               "gb_s": order_ceiling, "write_16ths": pc_w16,
+                               "frac_of_ceiling": (dense_kv + comp_kv) / t_pc / 1e9 / order_ceiling,
+                               "how": "mustafar_stream_chunks over one cache's bytes (batch x kv-heads "
+                                      "streams of 16 KiB chunks, the streams taking turns chunk by "
+                                      "chunk): the compression's chunk size, write share and order "
+                                      "without its arithmetic; rate of both directions"},
                            "rw_ceiling": {"gb_s": rw_ceiling, "write_16ths": pc_w16,
                                           "frac_of_ceiling": (dense_kv + comp_kv) / t_pc / 1e9 / rw_ceiling,
                                           "how": "mustafar_stream_mix over an 8 GiB buffer: every 16-byte "

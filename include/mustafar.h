@@ -519,6 +519,23 @@ int mustafar_stream_read(const void* src, size_t bytes, void* sink, void* stream
 int mustafar_stream_mix(const void* src, size_t bytes, void* dst, int write_16ths, void* sink,
                         void* stream);
 
+/* MEASUREMENT HELPER (not a step of the method). The bytes and access order of
+ * the bulk compression (mustafar_prune_compress at d = 128) without its
+ * arithmetic: `src` holds n_streams streams of n_chunks chunks of
+ * MUSTAFAR_STREAM_CHUNK_BYTES each, stream-major; one two-wave workgroup per
+ * chunk, the streams taking turns chunk by chunk (workgroup g: stream
+ * g % n_streams, chunk g / n_streams), reads its chunk with 16-byte loads,
+ * writes the first write_16ths/16 of the chunk's 16-byte words, packed, to the
+ * chunk's place in `dst` (device, at least n_streams * n_chunks *
+ * MUSTAFAR_STREAM_CHUNK_BYTES * write_16ths / 16 bytes) and one 32-bit checksum
+ * (XOR of the chunk's words) to sink[g] (device, n_streams * n_chunks
+ * entries). Its rate is the ceiling of that access order. `src` and `dst` must
+ * be 16-byte aligned, `sink` 4-byte aligned, n_streams, n_chunks >= 1 with
+ * n_streams * n_chunks < 2^31, 0 <= write_16ths <= 16. Errors: EINVAL. */
+#define MUSTAFAR_STREAM_CHUNK_BYTES 16384
+int mustafar_stream_chunks(const void* src, int n_streams, int n_chunks, void* dst, int write_16ths,
+                           void* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

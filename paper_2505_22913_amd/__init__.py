@@ -157,6 +157,8 @@ _SIGS = {
     "mustafar_attn_route": (ctypes.c_int, []),
     "mustafar_stream_mix": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
                                            ctypes.c_void_p, ctypes.c_void_p]),
+    "mustafar_stream_chunks": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                              ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]),
 }
 
 
@@ -572,6 +574,28 @@ def mustafar_stream_mix(src, dst, write_16ths: int, sink=None, stream=None):
     _check("mustafar_stream_mix", lib().mustafar_stream_mix(
         _dptr(src), src.numel() * src.element_size(), _dptr(dst), int(write_16ths), _dptr(sink),
         _stream(stream)))
+    return sink
+
+
+STREAM_CHUNK_BYTES = 16384  # MUSTAFAR_STREAM_CHUNK_BYTES
+
+
+def mustafar_stream_chunks(src, n_streams: int, dst, write_16ths: int, sink=None, stream=None):
+    """Measurement helper: the bulk compression's access order over device tensor
+    `src` (n_streams streams of 16 KiB chunks), write_16ths/16 of every chunk to `dst`;
+    returns the per-chunk checksums (uint32 as int32, workgroup order)."""
+    import torch
+    nbytes = src.numel() * src.element_size()
+    if n_streams < 1 or nbytes % (n_streams * STREAM_CHUNK_BYTES) != 0:
+        raise ValueError(f"{nbytes} bytes are not {n_streams} streams of whole {STREAM_CHUNK_BYTES}-byte chunks")
+    n_chunks = nbytes // (n_streams * STREAM_CHUNK_BYTES)
+    need = nbytes * write_16ths // 16
+    if dst.numel() * dst.element_size() < need:
+        raise ValueError(f"dst holds {dst.numel() * dst.element_size()} bytes, {need} needed")
+    if sink is None:
+        sink = torch.empty(n_streams * n_chunks, dtype=torch.int32, device=src.device)
+    _check("mustafar_stream_chunks", lib().mustafar_stream_chunks(
+        _dptr(src), int(n_streams), int(n_chunks), _dptr(dst), int(write_16ths), _dptr(sink), _stream(stream)))
     return sink
 
 

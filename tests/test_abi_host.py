@@ -471,6 +471,21 @@ def test_static_scratch_decode_rejects_before_touching_the_gpu(lib):
     assert "static scratch" in mf.strerror(mf.ESCRATCH)
 
 
+def test_stream_chunks_helper_rejects_bad_arguments(lib):
+    S = 0x300000
+    assert lib.mustafar_stream_chunks(0x100008, 2, 3, 0x200000, 9, S, None) == mf.EINVAL   # src not 16-aligned
+    assert lib.mustafar_stream_chunks(0x100000, 2, 3, 0x200008, 9, S, None) == mf.EINVAL   # dst not 16-aligned
+    assert lib.mustafar_stream_chunks(0x100000, 2, 3, 0x200000, 9, S + 2, None) == mf.EINVAL
+    assert lib.mustafar_stream_chunks(0x100000, 0, 3, 0x200000, 9, S, None) == mf.EINVAL
+    assert lib.mustafar_stream_chunks(0x100000, 2, 0, 0x200000, 9, S, None) == mf.EINVAL
+    assert lib.mustafar_stream_chunks(0x100000, 1 << 16, 1 << 15, 0x200000, 9, S, None) == mf.EINVAL
+    assert lib.mustafar_stream_chunks(0x100000, 2, 3, 0x200000, 17, S, None) == mf.EINVAL
+    assert lib.mustafar_stream_chunks(0x100000, 2, 3, 0x200000, -1, S, None) == mf.EINVAL
+    assert lib.mustafar_stream_chunks(None, 2, 3, 0x200000, 9, S, None) == mf.EINVAL
+    assert lib.mustafar_stream_chunks(0x100000, 2, 3, None, 9, S, None) == mf.EINVAL
+    assert lib.mustafar_stream_chunks(0x100000, 2, 3, 0x200000, 9, None, None) == mf.EINVAL
+
+
 def test_stream_mix_helper_rejects_bad_arguments(lib):
     S = 0x300000
     assert lib.mustafar_stream_mix(0x100008, 256, 0x200000, 9, S, None) == mf.EINVAL   # src not 16-aligned

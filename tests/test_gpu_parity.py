@@ -301,6 +301,30 @@ def test_stream_mix_writes_the_selected_words(w16):
     assert (got[out_words:] == 0xffffffff).all()
 
 
+@pytest.mark.parametrize("n_streams,n_chunks,w16", [(3, 5, 9), (1, 2, 16), (4, 1, 0), (7, 3, 5)])
+def test_stream_chunks_writes_each_chunks_share(n_streams, n_chunks, w16):
+    # The compression-order helper: workgroup g reads chunk g / n_streams of
+    # stream g % n_streams (its checksum goes to sink[g]) and stores the first
+    # w16/16 of the chunk's 16-byte words, packed, at the chunk's place.
+    import torch
+    announce(f"stream chunks {n_streams}x{n_chunks} w16={w16}")
+    P = mf.STREAM_CHUNK_BYTES // 16
+    rng = np.random.default_rng(n_streams * 31 + w16)
+    words = rng.integers(0, 2 ** 32, size=(n_streams, n_chunks, P, 4), dtype=np.uint64).astype(np.uint32)
+    src = torch.from_numpy(words.view(np.int32).reshape(-1, 4)).cuda()
+    out_p = P * w16 // 16
+    dst = torch.full((n_streams * n_chunks * out_p + 16, 4), -1, dtype=torch.int32, device="cuda")
+    sink = mf.mustafar_stream_chunks(src, n_streams, dst, w16).cpu().numpy().view(np.uint32)
+    g = np.arange(n_streams * n_chunks)
+    want_sink = np.bitwise_xor.reduce(words.reshape(n_streams, n_chunks, -1), axis=-1)[g % n_streams,
+                                                                                        g // n_streams]
+    assert np.array_equal(sink, want_sink)
+    got = dst.cpu().numpy().view(np.uint32)
+    want = words[:, :, :out_p].reshape(-1, 4)
+    assert np.array_equal(got[:n_streams * n_chunks * out_p], want)
+    assert (got[n_streams * n_chunks * out_p:] == 0xffffffff).all()
+
+
 @pytest.fixture
 def route():
     """Sets a kernel route for one test and restores the default afterwards."""
