@@ -214,6 +214,33 @@ def test_attention_over_caches_built_in_pieces(d, G, splits):
     assert err <= ATTN_TOL, err
 
 
+# The decode kernels read a tile offset only where a segment starts (segments
+# are whole 64-token blocks) and rebuild the others from the bitmaps, which the
+# bench's needed-bytes figure counts on: with every other offset zeroed (a
+# valid position, so a kernel that read them would compute wrong sums rather
+# than fault) the attention must not change.
+@pytest.mark.parametrize("d,G", [(128, 1), (128, 4), (128, 8), (64, 1), (256, 4)])
+def test_attention_reads_offsets_only_at_segment_starts(d, G):
+    announce(f"attn segment-start offsets d={d} G={G}")
+    B, Hkv, N, Nd = 2, 2, 700, 32
+    K, V = synth.make_kv(B, Hkv, N, d, seed=d * 3 + G)
+    KL, VL = synth.make_tail(B, Hkv, Nd, d, seed=d * 3 + G)
+    q = synth.make_q(B, Hkv * G, d, seed=d * 3 + G)
+    Kc = mf.CompressedCache(B, Hkv, d, 0.5, N)
+    Vc = mf.CompressedCache(B, Hkv, d, 0.7, N)
+    mf.mustafar_prune_compress(Kc, to_dev(K))
+    mf.mustafar_prune_compress(Vc, to_dev(V))
+    for c in (Kc, Vc):
+        starts = c.offsets[:, :, ::64, 0].clone()
+        c.offsets.zero_()
+        c.offsets[:, :, ::64, 0] = starts
+    ref = oracle.sparse_decode_attention(q, oracle.compress(K, 0.5), oracle.compress(V, 0.7), KL, VL)
+    for splits in (0, 1, 3, 11):
+        out = mf.mustafar_sparse_decode_attn(to_dev(q), Kc, Vc, to_dev(KL), to_dev(VL), n_splits=splits)
+        err = attn_error(out.cpu().numpy(), ref)
+        assert err <= ATTN_TOL, (splits, err)
+
+
 @pytest.mark.parametrize("sK,sV", [(0.0, 0.0), (0.9, 0.9), (1.0, 0.5), (0.5, 1.0), (1.0, 1.0)])
 def test_attention_extreme_sparsities(sK, sV):
     _attn_case(B=1, Hkv=2, G=2, Ns=200, Nd=5, d=128, sK=sK, sV=sV, splits=3, seed=31)
